@@ -1,0 +1,379 @@
+"""Pins for the CPU oracle: checks against closed forms, hand-derived cases,
+invariants and independent pure-Python brute force.
+
+Each pin takes an oracle-like namespace `ref` (with knn_ref, max_relative_ref,
+mrconv_ref, pool_keys_ref, stack_ref) and raises AssertionError on failure, so
+the same pins run against the oracle (test_oracle_pins.py) and against copies
+of it with planted mistakes (test_oracle_mutants.py), which every mistake must
+fail at least one pin.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def circle5():
+    with open(os.path.join(GOLDEN, "circle5.json")) as f:
+        g = json.load(f)
+    ang = [math.radians(a) for a in g["angles_deg"]]
+    # exact coordinates where they exist
+    pts = []
+    for a, deg in zip(ang, g["angles_deg"]):
+        if deg == 0:
+            pts.append((1.0, 0.0))
+        elif deg == 90:
+            pts.append((0.0, 1.0))
+        elif deg == 180:
+            pts.append((-1.0, 0.0))
+        else:
+            pts.append((math.cos(a), math.sin(a)))
+    return g, ang, np.array(pts)[None]  # [1, 5, 2]
+
+
+# ---------------------------------------------------------------------------
+# pure-Python brute force (no numpy arithmetic), tiny inputs only
+# ---------------------------------------------------------------------------
+def _bf_unit(row):
+    n = math.sqrt(math.fsum(v * v for v in row))
+    n = max(n, 1e-12)
+    return [v / n for v in row]
+
+
+def bf_knn(x, k, d, keys=None):
+    """Brute-force dilated kNN: explicit loops, (distance, index) tuples sorted
+    lexicographically, ranks 0, d, ..., (k-1)d."""
+    x = np.asarray(x).tolist()
+    keys = x if keys is None else np.asarray(keys).tolist()
+    out = []
+    for b in range(len(x)):
+        Ks = [_bf_unit(r) for r in keys[b]]
+        rows = []
+        for q in x[b]:
+            qu = _bf_unit(q)
+            cand = []
+            for j, kv in enumerate(Ks):
+                s = math.fsum((a - c) ** 2 for a, c in zip(qu, kv))
+                cand.append((s, j))
+            cand.sort()
+            rows.append([cand[t * d][1] for t in range(k)])
+        out.append(rows)
+    return np.array(out)
+
+
+def bf_mrconv(x, idx, W, bias, keys=None):
+    x = np.asarray(x).tolist()
+    keys = x if keys is None else np.asarray(keys).tolist()
+    W = np.asarray(W).tolist()
+    idx = np.asarray(idx).tolist()
+    B, N, C = len(x), len(x[0]), len(x[0][0])
+    Cout = len(W)
+    out = np.zeros((B, N, Cout))
+    for b in range(B):
+        for i in range(N):
+            m = []
+            for c in range(C):
+                m.append(max(keys[b][j][c] - x[b][i][c] for j in idx[b][i]))
+            cat = list(x[b][i]) + m
+            for o in range(Cout):
+                s = math.fsum(cat[c] * W[o][c] for c in range(2 * C))
+                out[b, i, o] = s + (0.0 if bias is None else bias[o])
+    return out
+
+
+# ---------------------------------------------------------------------------
+# kNN pins
+# ---------------------------------------------------------------------------
+def pin_circle_closed_form_fixture(ref):
+    """The fixture's lists equal the closed form 2 - 2cos(dtheta), sorted."""
+    g, ang, _ = circle5()
+    n = len(ang)
+    for key, k, d in (("knn_k3_d1", 3, 1), ("knn_k2_d2", 2, 2), ("knn_k2_d1", 2, 1)):
+        rows = []
+        for i in range(n):
+            cand = sorted((round(2 - 2 * math.cos(ang[i] - ang[j]), 12), j) for j in range(n))
+            rows.append([cand[t * d][1] for t in range(k)])
+        assert rows == g[key], key
+
+
+def pin_circle_knn(ref):
+    g, _, x = circle5()
+    for key, k, d in (("knn_k3_d1", 3, 1), ("knn_k2_d2", 2, 2), ("knn_k2_d1", 2, 1)):
+        got = ref.knn_ref(x, k, d)[0].tolist()
+        assert got == g[key], (key, got)
+
+
+def pin_knn_bruteforce(ref):
+    rng = np.random.default_rng(11)
+    for trial in range(6):
+        B, N, C = 2, int(rng.integers(3, 14)), int(rng.integers(1, 7))
+        x = rng.standard_normal((B, N, C))
+        if trial % 2 == 0:
+            x[:, N // 2] = x[:, 0]          # exact duplicate rows -> exact ties
+        k = int(rng.integers(1, 4))
+        d = int(rng.integers(1, 3))
+        if k * d > N:
+            k, d = 1, 1
+        assert np.array_equal(ref.knn_ref(x, k, d), bf_knn(x, k, d)), trial
+        # pooled-style: keys different from queries, M != N
+        M = int(rng.integers(k * d, 12)) if k * d < 12 else k * d
+        keys = rng.standard_normal((B, M, C))
+        assert np.array_equal(ref.knn_ref(x, k, d, keys=keys), bf_knn(x, k, d, keys)), trial
+
+
+def pin_knn_self_first(ref):
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((3, 40, 8))
+    idx, D = ref.knn_ref(x, 5, 1, return_dist=True)
+    assert np.array_equal(idx[:, :, 0], np.broadcast_to(np.arange(40), (3, 40)))
+    assert np.allclose(np.take_along_axis(D, idx[:, :, :1], 2), 0.0, atol=1e-12)
+
+
+def pin_knn_duplicates_lower_index(ref):
+    rng = np.random.default_rng(13)
+    x = rng.standard_normal((1, 30, 6))
+    x[0, 17] = x[0, 4]
+    idx = ref.knn_ref(x, 3, 1)
+    assert idx[0, 17, 0] == 4 and idx[0, 17, 1] == 17
+    assert idx[0, 4, 0] == 4 and idx[0, 4, 1] == 17
+
+
+def _near_tie_free(D, kk, gap=1e-9):
+    s = np.sort(D, axis=-1)
+    return np.all(np.abs(s[..., kk] - s[..., kk - 1]) > gap) if s.shape[-1] > kk else True
+
+
+def pin_knn_permutation_equivariant(ref):
+    rng = np.random.default_rng(14)
+    x = rng.standard_normal((2, 50, 12))
+    k = 6
+    perm = rng.permutation(50)
+    inv = np.argsort(perm)
+    a = ref.knn_ref(x, k, 1)
+    b = ref.knn_ref(x[:, perm], k, 1)          # row p of b is node perm[p]
+    # map b's neighbour ids back to original ids and rows back to original order
+    b_mapped = perm[b][:, inv]
+    assert np.array_equal(np.sort(a, -1), np.sort(b_mapped, -1))
+    assert np.array_equal(a, b_mapped)         # same order too (no near ties here)
+
+
+def pin_knn_scale_invariant(ref):
+    rng = np.random.default_rng(15)
+    x = rng.standard_normal((2, 45, 10))
+    assert np.array_equal(ref.knn_ref(x, 7, 2), ref.knn_ref(3.0 * x, 7, 2))
+    assert np.array_equal(ref.knn_ref(x, 7, 2), ref.knn_ref(0.125 * x, 7, 2))
+
+
+def pin_knn_dilation_consistency(ref):
+    rng = np.random.default_rng(16)
+    x = rng.standard_normal((2, 60, 9))
+    for k, d in ((4, 2), (3, 3), (9, 4)):
+        full = ref.knn_ref(x, k * d, 1)
+        assert np.array_equal(ref.knn_ref(x, k, d), full[:, :, ::d])
+
+
+def pin_knn_full_is_permutation(ref):
+    rng = np.random.default_rng(17)
+    x = rng.standard_normal((2, 23, 5))
+    idx = ref.knn_ref(x, 23, 1)
+    assert np.array_equal(np.sort(idx, -1), np.broadcast_to(np.arange(23), idx.shape))
+
+
+def pin_knn_zero_rows(ref):
+    x = np.zeros((1, 4, 3))
+    x[0, 1] = (1.0, 0.0, 0.0)
+    x[0, 2] = (0.0, 2.0, 0.0)
+    x[0, 3] = (0.0, 0.0, 0.0)
+    idx, D = ref.knn_ref(x, 4, 1, return_dist=True)
+    # zero row 0: distance 0 to the other zero row 3 and to itself, 1 to unit rows
+    assert idx[0, 0].tolist() == [0, 3, 1, 2]
+    assert np.allclose(D[0, 0], [0, 1, 1, 0])
+    assert idx[0, 1].tolist() == [1, 0, 3, 2]   # d(1,0)=1=d(1,3) < d(1,2)=2
+
+
+def pin_knn_sorted_by_distance(ref):
+    rng = np.random.default_rng(18)
+    x = rng.standard_normal((2, 64, 16))
+    idx, D = ref.knn_ref(x, 12, 1, return_dist=True)
+    dsel = np.take_along_axis(D, idx, 2)
+    assert np.all(np.diff(dsel, axis=-1) >= 0)
+    # the k-th selected is no farther than every unselected node
+    mask = np.ones_like(D, dtype=bool)
+    np.put_along_axis(mask, idx, False, 2)
+    assert np.all(dsel[..., -1:] <= np.where(mask, D, np.inf).min(-1, keepdims=True))
+
+
+# ---------------------------------------------------------------------------
+# MRConv pins
+# ---------------------------------------------------------------------------
+def pin_circle_mrconv(ref):
+    g, _, x = circle5()
+    idx = np.array(g["knn_k3_d1"])[None]
+    m = ref.max_relative_ref(x, idx)
+    assert np.allclose(m[0, 0], g["mrconv_k3_m0"], atol=1e-15)
+    assert np.allclose(m[0, 3], g["mrconv_k3_m3"], atol=1e-15)
+    # W = [0 | I]: the output is the max-relative part; W = [I | 0]: the input
+    W = np.hstack([np.zeros((2, 2)), np.eye(2)])
+    assert np.allclose(ref.mrconv_ref(x, idx, W)[0, 0], [0.0, 1.0], atol=1e-15)
+    W = np.hstack([np.eye(2), np.zeros((2, 2))])
+    assert np.allclose(ref.mrconv_ref(x, idx, W), x, atol=0)
+
+
+def pin_mrconv_bruteforce(ref):
+    rng = np.random.default_rng(21)
+    for trial in range(4):
+        B, N, C, Cout, k = 2, 7, 3, 4, 3
+        x = rng.standard_normal((B, N, C))
+        idx = rng.integers(0, N, (B, N, k))
+        W = rng.standard_normal((Cout, 2 * C))
+        bias = rng.standard_normal(Cout)
+        assert np.allclose(ref.mrconv_ref(x, idx, W, bias), bf_mrconv(x, idx, W, bias),
+                           rtol=0, atol=1e-12), trial
+        M = 5
+        keys = rng.standard_normal((B, M, C))
+        idk = rng.integers(0, M, (B, N, k))
+        assert np.allclose(ref.mrconv_ref(x, idk, W, bias, keys=keys),
+                           bf_mrconv(x, idk, W, bias, keys), rtol=0, atol=1e-12), trial
+
+
+def pin_mrconv_self_only(ref):
+    rng = np.random.default_rng(22)
+    x = rng.standard_normal((2, 9, 4))
+    idx = np.broadcast_to(np.arange(9)[None, :, None], (2, 9, 1)).copy()
+    assert np.array_equal(ref.max_relative_ref(x, idx), np.zeros_like(x))
+    W = rng.standard_normal((5, 8))
+    bias = rng.standard_normal(5)
+    want = np.einsum("bnc,oc->bno", x, W[:, :4]) + bias
+    assert np.allclose(ref.mrconv_ref(x, idx, W, bias), want, atol=1e-12)
+
+
+def pin_mrconv_translation(ref):
+    rng = np.random.default_rng(23)
+    x = rng.standard_normal((2, 11, 5))
+    idx = rng.integers(0, 11, (2, 11, 4))
+    v = rng.standard_normal(5)
+    assert np.allclose(ref.max_relative_ref(x + v, idx), ref.max_relative_ref(x, idx), atol=1e-12)
+
+
+def pin_mrconv_max_minus(ref):
+    """max_t (y_t - x) == (max_t y_t) - x exactly (rounding is monotone)."""
+    rng = np.random.default_rng(24)
+    x = rng.standard_normal((1, 13, 6))
+    idx = rng.integers(0, 13, (1, 13, 5))
+    nb = x[0][idx[0]]                      # [13, 5, 6]
+    want = nb.max(axis=1) - x[0]
+    assert np.array_equal(ref.max_relative_ref(x, idx)[0], want)
+
+
+def pin_mrconv_bias_only(ref):
+    rng = np.random.default_rng(25)
+    x = rng.standard_normal((1, 6, 3))
+    idx = rng.integers(0, 6, (1, 6, 2))
+    bias = np.array([0.5, -2.0])
+    out = ref.mrconv_ref(x, idx, np.zeros((2, 6)), bias)
+    assert np.array_equal(out, np.broadcast_to(bias, (1, 6, 2)))
+
+
+# ---------------------------------------------------------------------------
+# key pooling pins
+# ---------------------------------------------------------------------------
+def pin_pool_closed_form(ref):
+    H, W, r, C = 8, 12, 4, 3
+    yy, xx = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    x = np.zeros((2, H * W, C))
+    x[..., 0] = yy.ravel()
+    x[..., 1] = xx.ravel()
+    x[..., 2] = 5.0
+    k = ref.pool_keys_ref(x, H, W, r)
+    Wr = W // r
+    for p in range(H // r):
+        for q in range(Wr):
+            assert np.allclose(k[:, p * Wr + q], [p * r + (r - 1) / 2, q * r + (r - 1) / 2, 5.0])
+    assert np.array_equal(ref.pool_keys_ref(x, H, W, 1), x)
+
+
+# ---------------------------------------------------------------------------
+# stack pins
+# ---------------------------------------------------------------------------
+def pin_stack_single_layer(ref):
+    rng = np.random.default_rng(31)
+    x = rng.standard_normal((2, 16, 4))
+    W = rng.standard_normal((4, 8))
+    out = ref.stack_ref(x, [W], [None], (1,), 3, 4, 4)
+    assert np.allclose(out, ref.mrconv_ref(x, ref.knn_ref(x, 3, 1), W), atol=1e-12)
+
+
+def pin_stack_identity_weights(ref):
+    rng = np.random.default_rng(32)
+    x = rng.standard_normal((2, 16, 4))
+    Wi = np.hstack([np.eye(4), np.zeros((4, 4))])
+    a = ref.stack_ref(x, [Wi] * 4, None, (1, 1, 2, 2), 3, 4, 4, schedule="lookahead")
+    b = ref.stack_ref(x, [Wi] * 4, None, (1, 1, 2, 2), 3, 4, 4, schedule="standard")
+    assert np.array_equal(a, x) and np.array_equal(b, x)
+
+
+def pin_stack_circle_two_blocks(ref):
+    """Two blocks on the circle with W = [0 | I], k = 2, d = 1, worked by hand.
+
+    Block 0 uses G(X^0): neighbours {0,1}, {1,0}, {2,1}, {3,4}, {4,3}, so
+    X^1 = max(0, x_nb - x_i) = (0, 1/2), (1 - c30, 0), (c30, 0), (1 - c20, 0), (0, s20).
+    Lookahead block 1 reuses G(X^0):
+    X^2 = (1 - c30, 0), (0, 1/2), (0, 0), (0, s20), (1 - c20, 0).
+    The standard schedule rebuilds G(X^1).  Normalised, rows 0 and 4 are (0, 1)
+    and rows 1-3 are (1, 0) exactly, so distances are exact 0/2 ties and the
+    lower index wins: neighbours {0,4}, {1,2}, {1,2}, {1,2}, {0,4} (node 3 is
+    not its own neighbour), giving
+    X^2 = (0, 0), (2c30 - 1, 0), (0, 0), (c30 + c20 - 1, 0), (0, 1/2 - s20).
+    """
+    _, _, x = circle5()
+    c30, c20, s20 = math.cos(math.pi / 6), math.cos(math.pi / 9), math.sin(math.pi / 9)
+    W = np.hstack([np.zeros((2, 2)), np.eye(2)])
+    la = ref.stack_ref(x, [W, W], None, (1, 1), 2, 1, 5, schedule="lookahead")[0]
+    want_la = np.array([(1 - c30, 0), (0, 0.5), (0, 0), (0, s20), (1 - c20, 0)])
+    assert np.allclose(la, want_la, atol=1e-12), la
+    st = ref.stack_ref(x, [W, W], None, (1, 1), 2, 1, 5, schedule="standard")[0]
+    want_st = np.array([(0, 0), (2 * c30 - 1, 0), (0, 0), (c30 + c20 - 1, 0),
+                        (0, 0.5 - s20)])
+    assert np.allclose(st, want_st, atol=1e-12), st
+
+
+def pin_stack_pooled_graph_source(ref):
+    """With pooling, block l's graph ranks pooled keys of its source features
+    and MRConv gathers keys pooled from its own input."""
+    rng = np.random.default_rng(33)
+    H = W = 4
+    x = rng.standard_normal((1, 16, 3))
+    Wt = rng.standard_normal((3, 6))
+    xs, graphs = ref.stack_ref(x, [Wt, Wt], None, (1, 1), 2, H, W, pool_r=2,
+                               return_all=True)
+    k0 = ref.pool_keys_ref(x, H, W, 2)
+    assert np.array_equal(graphs[0], ref.knn_ref(x, 2, 1, keys=k0))
+    assert np.array_equal(graphs[1], graphs[0])          # lookahead: both from X^0
+    assert np.allclose(xs[2], ref.mrconv_ref(xs[1], graphs[1], Wt,
+                                             keys=ref.pool_keys_ref(xs[1], H, W, 2)))
+
+
+PINS = [
+    pin_circle_closed_form_fixture, pin_circle_knn, pin_knn_bruteforce, pin_knn_self_first,
+    pin_knn_duplicates_lower_index, pin_knn_permutation_equivariant, pin_knn_scale_invariant,
+    pin_knn_dilation_consistency, pin_knn_full_is_permutation, pin_knn_zero_rows,
+    pin_knn_sorted_by_distance, pin_circle_mrconv, pin_mrconv_bruteforce, pin_mrconv_self_only,
+    pin_mrconv_translation, pin_mrconv_max_minus, pin_mrconv_bias_only, pin_pool_closed_form,
+    pin_stack_single_layer, pin_stack_identity_weights, pin_stack_circle_two_blocks,
+    pin_stack_pooled_graph_source,
+]
+
+
+def failing_pins(ref):
+    bad = []
+    for p in PINS:
+        try:
+            p(ref)
+        except Exception as e:  # noqa: BLE001 - any failure counts
+            bad.append((p.__name__, repr(e)[:200]))
+    return bad

@@ -1,0 +1,145 @@
+"""Planted mistakes in copies of the oracle must each fail at least one pin.
+
+Each mutant replaces one oracle function with a version carrying a plausible
+bug (a dropped normalisation, a wrong sign, a transposed operand, an index off
+by one, the other tie-break, ...).  CPU only; the real oracle is untouched.
+"""
+import types
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import graphleap_ref as R
+from oracle_pins import failing_pins
+
+
+def _ns(**over):
+    base = {n: getattr(oracle, n) for n in dir(oracle) if not n.startswith("_")}
+    base.update(over)
+    ns = types.SimpleNamespace(**base)
+    return ns
+
+
+def _knn_factory(normalize=True, descending=False, dil_offset=0, tie_high=False,
+                 dist="sq"):
+    def knn(x, k, dilation=1, keys=None, rows=None, return_dist=False):
+        x = np.asarray(x, dtype=np.float64)
+        ks = x if keys is None else np.asarray(keys, dtype=np.float64)
+        B, N, _ = x.shape
+        rows_ = np.arange(N) if rows is None else np.asarray(rows)
+        kk = k * dilation
+        idx = np.empty((B, len(rows_), k), dtype=np.int64)
+        dist_all = np.empty((B, len(rows_), ks.shape[1]))
+        for b in range(B):
+            Q = R.l2_normalize(x[b, rows_]) if normalize else x[b, rows_]
+            K = R.l2_normalize(ks[b]) if normalize else ks[b]
+            diff = Q[:, None, :] - K[None, :, :]
+            D = (diff * diff).sum(-1) if dist == "sq" else np.abs(diff).sum(-1)
+            if descending:
+                order = np.argsort(-D, axis=1, kind="stable")
+            elif tie_high:
+                order = (D.shape[1] - 1 - np.argsort(D[:, ::-1], axis=1, kind="stable"))
+            else:
+                order = np.argsort(D, axis=1, kind="stable")
+            sel = order[:, :kk + dil_offset][:, dil_offset::dilation][:, :k]
+            idx[b] = sel
+            dist_all[b] = D
+        return (idx, dist_all) if return_dist else idx
+    return knn
+
+
+def _maxrel_factory(sign=1, use_min=False):
+    def maxrel(x, idx, keys=None):
+        x = np.asarray(x, dtype=np.float64)
+        ks = x if keys is None else np.asarray(keys, dtype=np.float64)
+        out = None
+        for t in range(idx.shape[2]):
+            nb = np.take_along_axis(ks, idx[:, :, t][:, :, None].astype(np.int64), axis=1)
+            v = sign * (nb - x)
+            out = v if out is None else (np.minimum(out, v) if use_min else np.maximum(out, v))
+        return out
+    return maxrel
+
+
+def _mrconv_factory(maxrel=None, swap_halves=False, transpose_w=False, drop_bias=False):
+    mr = maxrel or R.max_relative_ref
+
+    def mrconv(x, idx, W, b=None, keys=None, return_concat=False):
+        x = np.asarray(x, dtype=np.float64)
+        W = np.asarray(W, dtype=np.float64)
+        m = mr(x, idx, keys)
+        cat = np.concatenate([m, x] if swap_halves else [x, m], axis=-1)
+        Wt = W.reshape(W.shape[1], W.shape[0]) if transpose_w else W.T
+        out = cat @ Wt
+        if b is not None and not drop_bias:
+            out = out + np.asarray(b, dtype=np.float64)
+        return (out, cat) if return_concat else out
+    return mrconv
+
+
+def _pool_transposed(x, H, W, r):
+    x = np.asarray(x, dtype=np.float64)
+    B, N, C = x.shape
+    Hr, Wr = H // r, W // r
+    out = np.zeros((B, Hr * Wr, C))
+    for p in range(Hr):
+        for q in range(Wr):
+            acc = 0.0
+            for u in range(r):
+                for v in range(r):
+                    acc = acc + x[:, (p * r + v) * W + (q * r + u), :]   # u/v swapped
+            out[:, q * Hr + p, :] = acc / (r * r)                      # output transposed
+    return out
+
+
+def _stack_factory(schedule_override=None, knn=None, mrconv=None, pool=None):
+    knn = knn or R.knn_ref
+    mrconv = mrconv or R.mrconv_ref
+    pool = pool or R.pool_keys_ref
+
+    def stack(x0, Ws, bs, dilations, k, H, W, pool_r=1, schedule="lookahead",
+              return_all=False):
+        L = len(dilations)
+        sched = schedule_override or schedule
+        src = R.graph_source_blocks(L, sched)
+        xs = [np.asarray(x0, dtype=np.float64)]
+        graphs = []
+        for l in range(L):
+            xg = xs[src[l]]
+            kg = pool(xg, H, W, pool_r) if pool_r > 1 else None
+            idx = knn(xg, k, dilations[l], keys=kg)
+            graphs.append(idx)
+            ku = pool(xs[l], H, W, pool_r) if pool_r > 1 else None
+            xs.append(mrconv(xs[l], idx, Ws[l], bs[l] if bs is not None else None, keys=ku))
+        return (xs, graphs) if return_all else xs[-1]
+    return stack
+
+
+MUTANTS = {
+    "knn_no_normalisation": dict(knn_ref=_knn_factory(normalize=False)),
+    "knn_descending": dict(knn_ref=_knn_factory(descending=True)),
+    "knn_dilation_offset": dict(knn_ref=_knn_factory(dil_offset=1)),
+    "knn_tie_higher_index": dict(knn_ref=_knn_factory(tie_high=True)),
+    "knn_l1_distance": dict(knn_ref=_knn_factory(dist="l1")),
+    "maxrel_sign_flipped": dict(max_relative_ref=_maxrel_factory(sign=-1),
+                                mrconv_ref=_mrconv_factory(_maxrel_factory(sign=-1))),
+    "maxrel_min_not_max": dict(max_relative_ref=_maxrel_factory(use_min=True),
+                               mrconv_ref=_mrconv_factory(_maxrel_factory(use_min=True))),
+    "mrconv_halves_swapped": dict(mrconv_ref=_mrconv_factory(swap_halves=True)),
+    "mrconv_weight_transposed": dict(mrconv_ref=_mrconv_factory(transpose_w=True)),
+    "mrconv_bias_dropped": dict(mrconv_ref=_mrconv_factory(drop_bias=True)),
+    "pool_transposed": dict(pool_keys_ref=_pool_transposed),
+    "stack_standard_not_lookahead": dict(stack_ref=_stack_factory(schedule_override="standard")),
+    "stack_pool_transposed": dict(stack_ref=_stack_factory(pool=_pool_transposed)),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(name):
+    bad = failing_pins(_ns(**MUTANTS[name]))
+    assert bad, f"mutant {name} passed every pin"
+
+
+def test_real_oracle_passes_all():
+    assert failing_pins(oracle) == []
