@@ -1,0 +1,271 @@
+#!/usr/bin/env python3
+"""Benchmark the GraphLeap graph-convolution hot path on one MI355X.
+
+A step is one pass of the whole hot path over one batch: an L-block GraphLeap
+stack (bootstrap kNN build, then per block the kNN build of the next graph on
+the build stream overlapped with the MRConv update on the update stream),
+enqueued natively by gl_graphleap_stack.  Default workload: ViG-Ti shaped,
+12 blocks, B=32 images of 14x14 patches, C=192, k=9, dilation ceil(l/4),
+bf16 storage with fp32 accumulation, synthetic seeded inputs already in HBM.
+
+Prints one JSON line (rank 0): value = layers/s for the whole batch, plus the
+roofline of the dominant kernel (durations measured live with HIP events on
+the stream each kernel runs on) and the CPU oracle's rate on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--workload vig_ti]
+    python bench.py --only knn|mrconv|stack --steps K   (for profiler runs)
+    python bench.py --only copy                          (HBM counter calibration)
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "ViG graph-conv layers/sec at ViG-Ti B=32; Gram MFMA util %; gather HBM GB/s"
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense MFMA peaks (MI355X)
+PEAK_HBM_GBS = 8000.0
+
+DESCR = {
+    "vig_ti": "ViG-Ti isotropic stack: 12 GraphLeap blocks, B=32, 14x14 patches (N=196), C=192, "
+              "k=9, dilation ceil(l/4); kNN graph + MRConv (FC 384->192) per block",
+    "vig_b": "ViG-B isotropic stack: 16 blocks, B=64, N=196, C=640, k=9, dilation 1..4",
+    "pyr_s1": "Pyramid stage 1: 2 blocks, B=32, 56x56 (N=3136), C=80, keys pooled 4x4 -> 196, k=9",
+    "pyr_s2": "Pyramid stage 2: 2 blocks, B=32, 28x28 (N=784), C=160, keys pooled 2x2 -> 196, k=9",
+    "hires": "High-res stress: 4 blocks, B=8, 56x56 (N=3136), C=96, full N x N kNN, k=16, d=2",
+    "single": "Single isotropic layer: B=1, N=196, C=192, fp32, k=9, d=1",
+}
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2604_21290_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from a committed rocprofv3 --pmc summary, only if it
+    was taken on the current kernel sources."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        t = json.load(f)
+    if t.get("source_sha") != kernel_source_sha():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def algorithmic(w, es):
+    """Per-launch algorithmic work (bytes counted once, at their HBM size)."""
+    B, N, M, C, k = w.B, w.N, w.M, w.C, w.k
+    knn_flops = 2.0 * B * N * M * C
+    knn_bytes = B * N * C * es + (B * M * C * es if w.pool_r > 1 else 0) + B * N * k * 4
+    mr_flops = 2.0 * B * N * (2 * C) * C
+    mr_bytes = (B * N * C * es                                   # x read
+                + (B * M * C * es if w.pool_r > 1 else 0)        # pooled keys read
+                + B * N * k * 4                                  # idx read
+                + C * 2 * C * es                                 # W read
+                + B * N * C * es)                                # out write
+    return knn_flops, knn_bytes, mr_flops, mr_bytes
+
+
+def cpu_baseline(w, images: int) -> dict:
+    import numpy as np  # noqa: F401
+    from threadpoolctl import threadpool_limits
+
+    import oracle as O
+    from paper_2604_21290_amd import inputs as I
+
+    S = min(images, w.B)
+    ws = I.with_batch(w, S)
+    x = I.make_features(ws)
+    Ws = [I.make_weight(ws, l).value for l in range(w.L)]
+    bs = [I.make_bias(ws, l).value for l in range(w.L)]
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        O.stack_ref(x.value, Ws, bs, w.dilations, w.k, w.H, w.W, w.pool_r)
+        dt = time.perf_counter() - t0
+    scale = w.B / S
+    return {"value": w.L / (dt * scale), "unit": "layers/s", "cores": 1, "kind": "oracle",
+            "sample": f"oracle.stack_ref (fp64 numpy, lookahead schedule, 1 thread) on {S} of "
+                      f"{w.B} images for all {w.L} blocks in {dt:.2f} s; time scaled x{scale:g} "
+                      f"to the full batch"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="vig_ti")
+    ap.add_argument("--schedule", default="lookahead", choices=["lookahead", "standard"])
+    ap.add_argument("--only", default=None, choices=["stack", "knn", "mrconv", "copy"])
+    ap.add_argument("--cpu-images", type=int, default=16)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is "
+                                   "described in the design notes, not implemented",
+                          "n_gpus": args.gpus}), flush=True)
+        return 2
+
+    import torch
+
+    from paper_2604_21290_amd import api
+    from paper_2604_21290_amd import inputs as I
+
+    assert torch.cuda.is_available(), "bench needs a GPU"
+    api.lib()
+    w = I.WORKLOADS[args.workload]
+    es = 2 if w.dtype == I.BF16 else 4
+    sched = api.GL_SCHED_LOOKAHEAD if args.schedule == "lookahead" else api.GL_SCHED_STANDARD
+
+    def dev(s):
+        import numpy as np
+        if s.dtype == I.F32:
+            return torch.from_numpy(np.ascontiguousarray(s.bits)).cuda()
+        return torch.from_numpy(np.ascontiguousarray(s.bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+    import numpy as np
+    x0 = dev(I.make_features(w))
+    Wd = dev(I.Stored(np.stack([I.make_weight(w, l).bits for l in range(w.L)]), None, w.dtype))
+    bd = dev(I.Stored(np.stack([I.make_bias(w, l).bits for l in range(w.L)]), None, w.dtype))
+    s_up = torch.cuda.current_stream()
+    la = api.Lookahead(s_up, torch.cuda.Stream())
+    ws = api.make_stack_workspace(x0, w.H, w.W, w.k, w.pool_r)
+    out = torch.empty_like(x0)
+    dil = list(w.dilations)
+
+    if args.only == "copy":
+        # plain device copy of a known size, for scaling rocprofv3 FETCH/WRITE counters
+        n = 256 << 20
+        a = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        b = torch.empty_like(a)
+        for _ in range(args.steps):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"copied {n} bytes x {args.steps}")
+        return 0
+    if args.only == "knn":
+        keys = api.pool_keys(x0, w.H, w.W, w.pool_r) if w.pool_r > 1 else None
+        idx = ws["idx"][0]
+        for _ in range(args.steps):
+            api.knn_graph(x0, w.k, dil[-1], keys=keys, out=idx)
+        torch.cuda.synchronize()
+        log(f"knn x {args.steps} (d={dil[-1]})")
+        return 0
+    if args.only == "mrconv":
+        keys = api.pool_keys(x0, w.H, w.W, w.pool_r) if w.pool_r > 1 else None
+        idx = api.knn_graph(x0, w.k, dil[0], keys=keys)
+        for _ in range(args.steps):
+            api.mrconv(x0, idx, Wd[0], bd[0], keys=keys, out=out)
+        torch.cuda.synchronize()
+        log(f"mrconv x {args.steps}")
+        return 0
+
+    def step():
+        la.stack(x0, w.H, w.W, Wd, bd, dil, w.k, w.pool_r, schedule=sched, ws=ws, x_out=out)
+
+    log(f"workload {args.workload}: warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    e0.record(s_up)
+    for _ in range(args.steps):
+        step()
+    e1.record(s_up)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms = e0.elapsed_time(e1)
+    ms_per_step = ms / args.steps
+    value = w.L * args.steps / (ms / 1e3)
+    log(f"{ms_per_step:.4f} ms/step, {value:.1f} layers/s (wall {wall:.3f} s)")
+
+    # per-kernel durations: the same steps again, each kNN build and each MRConv
+    # update bracketed by HIP events on its own stream
+    if args.only == "stack":
+        return 0
+    n_rec = args.steps * w.L + 8
+    la.set_profiling(n_rec)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    tb = la.kernel_times_ms(api.GL_TIME_BUILD, n_rec)
+    tu = la.kernel_times_ms(api.GL_TIME_UPDATE, n_rec)
+    la.set_profiling(0)
+    knn_flops, knn_bytes, mr_flops, mr_bytes = algorithmic(w, es)
+    peak = PEAK_TFLOPS[w.dtype]
+    kernels = {}
+    if tb:
+        t = sum(tb) / len(tb) * 1e-3
+        kernels["knn_graph"] = {
+            "launches_per_step": len(tb) / args.steps, "avg_us": t * 1e6,
+            "gram_tflops": knn_flops / t / 1e12, "gram_mfma_frac": knn_flops / t / 1e12 / peak,
+            "candidates_per_s": w.B * w.N * w.M / t}
+    if tu:
+        t = sum(tu) / len(tu) * 1e-3
+        kernels["mrconv"] = {
+            "launches_per_step": len(tu) / args.steps, "avg_us": t * 1e6,
+            "fc_tflops": mr_flops / t / 1e12, "fc_mfma_frac": mr_flops / t / 1e12 / peak,
+            "hbm_gbs": mr_bytes / t / 1e9, "hbm_frac": mr_bytes / t / 1e9 / PEAK_HBM_GBS,
+            "gather_effective_gbs": (w.B * w.N * w.k * w.C * es) / t / 1e9}
+    tot_b = sum(tb) / args.steps if tb else 0.0
+    tot_u = sum(tu) / args.steps if tu else 0.0
+    if tot_b >= tot_u and tb:
+        t = sum(tb) / len(tb) * 1e-3
+        roof = {"kernel": "knn_graph", "bound": "mfma", "achieved": knn_flops / t / 1e12,
+                "peak": peak, "unit": "TFLOP/s", "frac": knn_flops / t / 1e12 / peak,
+                "traffic": load_traffic("knn_graph", args.workload),
+                "per_launch": f"2*B*N*M*C = {knn_flops:.4g} flop"}
+    else:
+        t = sum(tu) / len(tu) * 1e-3
+        roof = {"kernel": "mrconv", "bound": "hbm", "achieved": mr_bytes / t / 1e9,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": mr_bytes / t / 1e9 / PEAK_HBM_GBS,
+                "traffic": load_traffic("mrconv", args.workload),
+                "per_launch": f"{mr_bytes:.4g} bytes"}
+    log("kernels", json.dumps(kernels))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        cpu = cpu_baseline(w, args.cpu_images)
+        log("cpu", json.dumps(cpu))
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "layers/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {DESCR[args.workload]}", "B": w.B, "N": w.N,
+                   "M": w.M, "C": w.C, "k": w.k, "blocks": w.L, "dilations": dil,
+                   "schedule": args.schedule},
+        "roofline": roof, "cpu_baseline": cpu, "kernels": kernels,
+        "image_layers_per_s": value * w.B, "source_sha": kernel_source_sha(),
+    }
+    print(json.dumps(line), flush=True)
+    la.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,226 @@
+/*
+ * graphleap.h -- C ABI of the MI355X (gfx950) GraphLeap graph-convolution path.
+ *
+ * The operations follow the paper "GraphLeap: Decoupling Graph Construction
+ * and Convolution for Vision GNN Acceleration on FPGA":
+ *   - the dynamic kNN image graph G(X) of Sec. II-B (Eq. 4), built as in the
+ *     Graph Construction Engine of Sec. IV-B (pairwise distances of Alg. 2,
+ *     per-node selection of the k nearest, dilation);
+ *   - max-relative graph convolution MRConv of Sec. II-A (Eq. 2 and Eq. 3),
+ *     with the weight split W_x / W_m of Sec. IV-C2;
+ *   - the GraphLeap lookahead of Sec. III (Eq. 10-12, Alg. 1): block l's
+ *     update uses the graph built from block l-1's features while the graph
+ *     for block l+1 is built concurrently (Sec. IV-A, IV-F).
+ *
+ * Conventions for every call
+ *   Memory.  Every tensor pointer is device memory owned by the caller.  The
+ *     library allocates nothing and keeps no pointer after a call returns.
+ *     Buffers must stay alive until the streams the work was enqueued on have
+ *     finished it.
+ *   Layout.  Row-major, channels last: features [B, N, C], keys [B, M, C],
+ *     neighbour indices int32 [B, N, k], weights [Cout, 2C], bias [Cout].
+ *     Base pointers of feature, key and weight tensors must be 16-byte
+ *     aligned; C must be a multiple of 8 (bf16) or 4 (fp32).
+ *   Numbers.  dt selects the storage type of features, keys, weights, bias
+ *     and outputs: GL_F32 or GL_BF16.  Arithmetic is fp32 (bf16 x bf16
+ *     products are exact in fp32); outputs are rounded once to dt (RNE).
+ *   Errors.  Arguments are validated on the host before anything is
+ *     enqueued: a call either enqueues all of its work or none of it.  A
+ *     failed launch returns GL_ERR_HIP.  Faults inside kernels surface at
+ *     the caller's next synchronisation.  gl_last_error() gives a
+ *     thread-local message for the last non-OK status.
+ *   Streams.  hipStream_t may be 0 (the null stream).  Calls are
+ *     asynchronous with respect to the host.  The library is thread-safe
+ *     except that one lookahead handle must not be used from two threads
+ *     at once.
+ */
+#ifndef GRAPHLEAP_H
+#define GRAPHLEAP_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GL_VERSION 1
+#define GL_MAX_KD 64     /* largest k * dilation of one graph build */
+#define GL_MAX_M 4096    /* largest number of key nodes per image */
+#define GL_MAX_K 64      /* largest neighbour count of one MRConv */
+
+typedef enum gl_dtype { GL_F32 = 0, GL_BF16 = 1 } gl_dtype;
+
+typedef enum gl_status {
+  GL_OK = 0,
+  GL_ERR_NULL_PTR = 1,     /* a required pointer is NULL */
+  GL_ERR_BAD_SHAPE = 2,    /* a size is < 1, inconsistent or too large */
+  GL_ERR_BAD_K = 3,        /* k < 1, dilation < 1, k*dilation > M or > GL_MAX_KD */
+  GL_ERR_UNSUPPORTED = 4,  /* dtype, or C not a multiple of the vector width */
+  GL_ERR_ALIGNMENT = 5,    /* a tensor base pointer is not 16-byte aligned */
+  GL_ERR_ALIAS = 6,        /* an output overlaps an input it must not overlap */
+  GL_ERR_HIP = 7,          /* the HIP runtime reported an error */
+  GL_ERR_BAD_HANDLE = 8    /* NULL or destroyed lookahead handle */
+} gl_status;
+
+typedef enum gl_schedule {
+  GL_SCHED_LOOKAHEAD = 0,  /* GraphLeap: block l uses G(X^(l-1)); build || update */
+  GL_SCHED_STANDARD = 1    /* standard ViG (Eq. 6): block l uses G(X^l); serial */
+} gl_schedule;
+
+/* ---------------------------------------------------------------------------
+ * gl_knn_graph -- dilated kNN graph (Sec. II-B Eq. 4; Sec. IV-B; Alg. 2).
+ *
+ * For every image b and query row i of x[b], ranks the key rows j of
+ * keys[b] by the squared Euclidean distance between the L2-normalised rows
+ * (norm floored at 1e-12), ties going to the lower j, keeps the
+ * K' = k * dilation nearest and writes ranks 0, d, 2d, ..., (k-1)d:
+ *     idx_out[b, i, t] = j of rank t * dilation,   t = 0 .. k-1.
+ * Position 0 is the nearest key (the node itself when keys == x and rows
+ * are distinct).  Distances are ranked at fixed-point resolution
+ * 2^-(30 - ceil(log2 M)) (4e-6 at M = 4096, 2.4e-7 at M = 196); keys closer
+ * than that count as tied and go to the lower index.
+ *
+ *   x       [B, N, C] queries (dt).
+ *   keys    [B, M, C] keys (dt), or NULL for keys = x (then M must equal N).
+ *   idx_out [B, N, k] int32 output; must not overlap x or keys.
+ * Limits: B, N, C >= 1; 1 <= M <= GL_MAX_M; 1 <= k; 1 <= dilation;
+ *         k * dilation <= min(M, GL_MAX_KD).
+ * -------------------------------------------------------------------------*/
+gl_status gl_knn_graph(const void* x, int B, int N, int C, const void* keys, int M,
+                       int k, int dilation, gl_dtype dt, int32_t* idx_out,
+                       hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * gl_pool_keys -- r x r average pooling of the H x W node grid, used as the
+ * key set of pyramid stages (key pooling of the pyramid workloads; the
+ * paper reduces nodes between stages by pooling, Sec. IV-E).
+ *
+ *   keys_out[b, p*(W/r) + q, c] = mean_{u,v<r} x[b, (p*r+u)*W + (q*r+v), c]
+ * accumulated in fp32 and rounded once to dt.
+ *   x [B, H*W, C] (dt); keys_out [B, (H/r)*(W/r), C] (dt), must not overlap x.
+ * Limits: H % r == 0, W % r == 0, r >= 1.
+ * -------------------------------------------------------------------------*/
+gl_status gl_pool_keys(const void* x, int B, int H, int W, int C, int r, gl_dtype dt,
+                       void* keys_out, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * gl_mrconv -- max-relative graph convolution (Sec. II-A Eq. 2 and Eq. 3),
+ * the feature update of one block.
+ *
+ *   m[b,i,c]   = max_t keys[b, idx[b,i,t], c] - x[b,i,c]
+ *   out[b,i,o] = sum_c x[b,i,c] W[o,c] + sum_c m[b,i,c] W[o,C+c] + bias[o]
+ * i.e. [x_i, max_j(x_j - x_i)] W^T + b with W = [W_x | W_m] (Sec. IV-C2).
+ * The neighbour rows are gathered on the fly; no [B,N,k,C] edge tensor and
+ * no [B,N,2C] concatenation is ever written to memory.
+ *
+ *   x    [B, N, C] (dt); keys [B, M, C] (dt) or NULL for keys = x (M == N).
+ *   idx  [B, N, k] int32 in [0, M).  Out-of-range values are clamped into
+ *        [0, M) inside the kernel (no fault; the result is then undefined).
+ *   W    [Cout, 2C] (dt); bias [Cout] (dt) or NULL for zero bias.
+ *   out  [B, N, Cout] (dt); must not overlap x, keys, idx, W or bias.
+ * Limits: 1 <= k <= GL_MAX_K; Cout >= 1.
+ * -------------------------------------------------------------------------*/
+gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
+                    const int32_t* idx, int k, const void* W, const void* bias, int Cout,
+                    gl_dtype dt, void* out, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Lookahead handle (Sec. IV-A, IV-F; the look-ahead buffer of Sec. IV-G).
+ * Holds two HIP events that order the build stream against the update
+ * stream; the caller owns both streams and every tensor.  Streams must be
+ * distinct for the build to overlap the update; they may be equal.
+ * -------------------------------------------------------------------------*/
+typedef struct gl_lookahead* gl_lookahead_t;
+
+gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_lookahead_t* out);
+gl_status gl_lookahead_destroy(gl_lookahead_t h);
+
+/* Profiling: when enabled (max_records > 0), every kNN build and every
+ * MRConv update enqueued through the handle is bracketed by a pair of HIP
+ * events on the stream it runs on (at most max_records pairs of each kind
+ * are kept; later launches are not timed).  gl_lookahead_kernel_times()
+ * synchronises the recorded events of one kind (which = GL_TIME_BUILD or
+ * GL_TIME_UPDATE), writes their durations in milliseconds (at most cap of
+ * them) and clears that kind's records.  max_records == 0 disables it. */
+#define GL_TIME_BUILD 0
+#define GL_TIME_UPDATE 1
+gl_status gl_lookahead_set_profiling(gl_lookahead_t h, int max_records);
+gl_status gl_lookahead_kernel_times(gl_lookahead_t h, int which, float* ms_out, int cap,
+                                    int* n_out);
+
+/* Bootstrap Ghat^0 = G(X^0) with dilation d_0 (Sec. III: the first block
+ * uses the standard construction).  Enqueues [pooling of x0 into keys_ws on
+ * the update stream when pool_r > 1], then the build into idx0 on the build
+ * stream after the update stream's prior work; the next gl_graphleap_block
+ * waits for it.  x0 [B, H*W, C]; keys_ws [B, (H/pool_r)*(W/pool_r), C] or
+ * NULL when pool_r == 1; idx0 [B, H*W, k]. */
+gl_status gl_lookahead_bootstrap(gl_lookahead_t h, const void* x0, int B, int H, int W,
+                                 int C, int pool_r, void* keys_ws, int k, int dilation0,
+                                 gl_dtype dt, int32_t* idx0);
+
+/* ---------------------------------------------------------------------------
+ * gl_graphleap_block -- one GraphLeap block in the reduced form
+ * X^(l+1) = MRConv(X^l; Ghat^l) (Eq. 12-13 with U = X), overlapping the
+ * build of Ghat^(l+1) = G(X^l) (Eq. 11 for the next block) with the update.
+ *
+ * Enqueue order:
+ *   update stream: wait for the previous build through the handle (it made
+ *                  idx_use); [pool x_in -> keys_ws]; record "x_in ready";
+ *   build stream : wait "x_in ready"; kNN(x_in, keys) -> idx_next with
+ *                  dilation_next; record "built" (skipped if idx_next NULL);
+ *   update stream: MRConv(x_in, keys, idx_use, Wt, bias) -> x_out.
+ * Both engines read only x_in (and keys_ws), so they run concurrently.
+ *
+ *   x_in [B, H*W, C]; x_out [B, H*W, C] must not overlap x_in, keys_ws.
+ *   keys_ws [B, M, C] with M = (H/pool_r)*(W/pool_r) when pool_r > 1,
+ *           else NULL (keys = x_in).
+ *   idx_use [B, H*W, k] = Ghat^l; idx_next [B, H*W, k] = Ghat^(l+1) or NULL
+ *           (last block, or when Ghat^(l+1) is the same graph as Ghat^l);
+ *           idx_next must not overlap idx_use.
+ *   Wt [C, 2C], bias [C] or NULL.
+ * The caller double-buffers features and graphs (two of each, Sec. IV-G
+ * N_buf = 2): the handle's waits make reuse of the buffers of block l-1 by
+ * block l+1 safe.
+ * -------------------------------------------------------------------------*/
+gl_status gl_graphleap_block(gl_lookahead_t h, const void* x_in, int B, int H, int W, int C,
+                             int pool_r, void* keys_ws, const int32_t* idx_use, int k,
+                             const void* Wt, const void* bias, gl_dtype dt, void* x_out,
+                             int32_t* idx_next, int dilation_next);
+
+/* ---------------------------------------------------------------------------
+ * gl_graphleap_stack -- L blocks of X^(l+1) = MRConv(X^l; Ghat^l) enqueued
+ * natively (Alg. 1 reduced to graph + MRConv, looped over blocks).
+ *
+ *   schedule GL_SCHED_LOOKAHEAD: Ghat^0 = G(X^0, d_0); Ghat^1 = G(X^0, d_1)
+ *     (the same graph when d_1 == d_0, built once); Ghat^l = G(X^(l-1), d_l)
+ *     for l >= 2, each built on the build stream while the previous block
+ *     updates.  L - 1 builds when d_1 == d_0; G(X^(L-1)) is never built.
+ *   schedule GL_SCHED_STANDARD: Ghat^l = G(X^l, d_l), build then update,
+ *     all on the update stream (Eq. 5-7 with U = X).
+ *
+ *   x0 [B, N, C] input, N = H*W.  Ws [L, C, 2C]; bs [L, C] or NULL.
+ *   dilations: host array of L ints (the dilation of the block that uses
+ *     each graph).
+ *   x_ws [2, B, N, C] feature ping-pong workspace; idx_ws [2, B, N, k];
+ *   keys_ws [B, M, C] when pool_r > 1 else NULL;  x_out [B, N, C] = X^L.
+ *   x_out, x_ws, idx_ws and keys_ws must not overlap each other or x0.
+ * -------------------------------------------------------------------------*/
+gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int W, int C,
+                             int pool_r, int L, int k, const int* dilations, const void* Ws,
+                             const void* bs, gl_dtype dt, gl_schedule schedule, void* x_ws,
+                             int32_t* idx_ws, void* keys_ws, void* x_out);
+
+/* ---------------------------------------------------------------------------
+ * Diagnostics.
+ * -------------------------------------------------------------------------*/
+const char* gl_status_string(gl_status s);
+const char* gl_last_error(void);   /* thread-local detail of the last non-OK status */
+int gl_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GRAPHLEAP_H */

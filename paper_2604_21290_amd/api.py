@@ -1,0 +1,229 @@
+"""Thin ctypes binding of libgraphleap.so (include/graphleap.h).
+
+Argument marshalling only: tensors are passed as device pointers, streams as
+hipStream_t; every step of the path runs in the library's HIP kernels.  The
+binding allocates outputs and workspaces with torch when the caller does not
+pass them (PyTorch supplies device memory and streams, nothing else).
+
+The library must have been built (python -m paper_2604_21290_amd.build);
+loading raises if it is missing -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgraphleap.so")
+
+GL_F32, GL_BF16 = 0, 1
+GL_SCHED_LOOKAHEAD, GL_SCHED_STANDARD = 0, 1
+GL_TIME_BUILD, GL_TIME_UPDATE = 0, 1
+GL_MAX_KD, GL_MAX_M, GL_MAX_K = 64, 4096, 64
+
+STATUS = {0: "GL_OK", 1: "GL_ERR_NULL_PTR", 2: "GL_ERR_BAD_SHAPE", 3: "GL_ERR_BAD_K",
+          4: "GL_ERR_UNSUPPORTED", 5: "GL_ERR_ALIGNMENT", 6: "GL_ERR_ALIAS", 7: "GL_ERR_HIP",
+          8: "GL_ERR_BAD_HANDLE"}
+
+_vp, _i, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+
+# name -> argtypes (every entry point returns gl_status as int unless noted)
+SIGNATURES = {
+    "gl_knn_graph": [_vp, _i, _i, _i, _vp, _i, _i, _i, _i, _vp, _vp],
+    "gl_pool_keys": [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp],
+    "gl_mrconv": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp],
+    "gl_lookahead_create": [_vp, _vp, ctypes.POINTER(_vp)],
+    "gl_lookahead_destroy": [_vp],
+    "gl_lookahead_set_profiling": [_vp, _i],
+    "gl_lookahead_kernel_times": [_vp, _i, ctypes.POINTER(_f), _i, ctypes.POINTER(_i)],
+    "gl_lookahead_bootstrap": [_vp, _vp, _i, _i, _i, _i, _i, _vp, _i, _i, _i, _vp],
+    "gl_graphleap_block": [_vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _i, _vp, _vp, _i, _vp, _vp, _i],
+    "gl_graphleap_stack": [_vp, _vp, _i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i), _vp, _vp, _i,
+                           _i, _vp, _vp, _vp, _vp],
+    "gl_status_string": [_i],
+    "gl_last_error": [],
+    "gl_version": [],
+}
+RESTYPES = {"gl_status_string": ctypes.c_char_p, "gl_last_error": ctypes.c_char_p}
+
+_lib = None
+
+
+class GraphLeapError(RuntimeError):
+    def __init__(self, name: str, status: int, detail: str):
+        super().__init__(f"{name}: {STATUS.get(status, status)}: {detail}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2604_21290_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, args in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = RESTYPES.get(name, ctypes.c_int)
+        _lib = L
+    return _lib
+
+
+def _check(name: str, status: int):
+    if status != 0:
+        raise GraphLeapError(name, status, lib().gl_last_error().decode())
+
+
+def _call(name: str, *args):
+    _check(name, getattr(lib(), name)(*args))
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return GL_F32
+    if t.dtype == torch.bfloat16:
+        return GL_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _p(t):
+    if t is None:
+        return None
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("tensors must be contiguous device tensors")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _s(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+# ---------------------------------------------------------------------------
+# single calls
+# ---------------------------------------------------------------------------
+def knn_graph(x: torch.Tensor, k: int, dilation: int = 1, keys: torch.Tensor | None = None,
+              out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """idx[B, N, k] int32: dilated kNN of each row of x among keys (or x)."""
+    B, N, C = x.shape
+    M = N if keys is None else keys.shape[1]
+    if out is None:
+        out = torch.empty((B, N, k), dtype=torch.int32, device=x.device)
+    _call("gl_knn_graph", _p(x), B, N, C, _p(keys), M, k, dilation, _dt(x), _p(out), _s(stream))
+    return out
+
+
+def pool_keys(x: torch.Tensor, H: int, W: int, r: int, out: torch.Tensor | None = None,
+              stream=None) -> torch.Tensor:
+    B, N, C = x.shape
+    if out is None:
+        out = torch.empty((B, (H // r) * (W // r), C), dtype=x.dtype, device=x.device)
+    _call("gl_pool_keys", _p(x), B, H, W, C, r, _dt(x), _p(out), _s(stream))
+    return out
+
+
+def mrconv(x: torch.Tensor, idx: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = None,
+           keys: torch.Tensor | None = None, out: torch.Tensor | None = None,
+           stream=None) -> torch.Tensor:
+    """out[B, N, Cout] = [x_i, max_j (keys_j - x_i)] W^T + bias."""
+    B, N, C = x.shape
+    M = N if keys is None else keys.shape[1]
+    k = idx.shape[2]
+    Cout = W.shape[0]
+    if out is None:
+        out = torch.empty((B, N, Cout), dtype=x.dtype, device=x.device)
+    _call("gl_mrconv", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(W), _p(bias), Cout, _dt(x),
+          _p(out), _s(stream))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# lookahead
+# ---------------------------------------------------------------------------
+class Lookahead:
+    """Owns a gl_lookahead handle bound to an update stream and a build stream."""
+
+    def __init__(self, s_update=None, s_build=None):
+        self.s_update = s_update if s_update is not None else torch.cuda.current_stream()
+        self.s_build = s_build if s_build is not None else torch.cuda.Stream()
+        h = ctypes.c_void_p()
+        _call("gl_lookahead_create", _s(self.s_update), _s(self.s_build), ctypes.byref(h))
+        self._h = h
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            _call("gl_lookahead_destroy", self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _keep(self, *ts):
+        for t in ts:
+            if t is not None:
+                t.record_stream(self.s_build)
+
+    def set_profiling(self, max_records: int):
+        _call("gl_lookahead_set_profiling", self._h, max_records)
+
+    def kernel_times_ms(self, which: int = GL_TIME_BUILD, cap: int = 1 << 16) -> list:
+        """Durations (ms) of the profiled builds (GL_TIME_BUILD) or updates."""
+        buf = (ctypes.c_float * cap)()
+        n = ctypes.c_int()
+        _call("gl_lookahead_kernel_times", self._h, which, buf, cap, ctypes.byref(n))
+        return list(buf[: n.value])
+
+    def bootstrap(self, x0, H, W, k, dilation0, pool_r=1, keys_ws=None, idx0=None):
+        B, N, C = x0.shape
+        if idx0 is None:
+            idx0 = torch.empty((B, N, k), dtype=torch.int32, device=x0.device)
+        self._keep(x0, keys_ws, idx0)
+        _call("gl_lookahead_bootstrap", self._h, _p(x0), B, H, W, C, pool_r, _p(keys_ws), k,
+              dilation0, _dt(x0), _p(idx0))
+        return idx0
+
+    def block(self, x_in, H, W, idx_use, Wt, bias=None, pool_r=1, keys_ws=None, x_out=None,
+              idx_next=None, dilation_next=1):
+        B, N, C = x_in.shape
+        k = idx_use.shape[2]
+        if x_out is None:
+            x_out = torch.empty_like(x_in)
+        self._keep(x_in, keys_ws, idx_next)
+        _call("gl_graphleap_block", self._h, _p(x_in), B, H, W, C, pool_r, _p(keys_ws),
+              _p(idx_use), k, _p(Wt), _p(bias), _dt(x_in), _p(x_out), _p(idx_next),
+              dilation_next)
+        return x_out
+
+    def stack(self, x0, H, W, Ws, bs, dilations, k, pool_r=1, schedule=GL_SCHED_LOOKAHEAD,
+              ws=None, x_out=None):
+        """Run len(dilations) blocks; Ws [L, C, 2C], bs [L, C] or None."""
+        B, N, C = x0.shape
+        L = len(dilations)
+        if ws is None:
+            ws = make_stack_workspace(x0, H, W, k, pool_r)
+        if x_out is None:
+            x_out = torch.empty_like(x0)
+        dil = (ctypes.c_int * L)(*dilations)
+        self._keep(x0, ws["x"], ws["idx"], ws["keys"])
+        _call("gl_graphleap_stack", self._h, _p(x0), B, H, W, C, pool_r, L, k, dil, _p(Ws),
+              _p(bs), _dt(x0), schedule, _p(ws["x"]), _p(ws["idx"]), _p(ws["keys"]), _p(x_out))
+        return x_out
+
+
+def make_stack_workspace(x0: torch.Tensor, H: int, W: int, k: int, pool_r: int = 1) -> dict:
+    B, N, C = x0.shape
+    M = (H // pool_r) * (W // pool_r)
+    return {
+        "x": torch.empty((2, B, N, C), dtype=x0.dtype, device=x0.device),
+        "idx": torch.empty((2, B, N, k), dtype=torch.int32, device=x0.device),
+        "keys": torch.empty((B, M, C), dtype=x0.dtype, device=x0.device) if pool_r > 1 else None,
+    }
+
+
+def version() -> int:
+    return lib().gl_version()

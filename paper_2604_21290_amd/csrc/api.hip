@@ -1,0 +1,532 @@
+// Host side of the C ABI declared in include/graphleap.h: argument checks,
+// kernel dispatch and the lookahead schedule (Sec. III, Sec. IV-A/F).
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <climits>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "graphleap.h"
+#include "gl_kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+gl_status fail(gl_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+gl_status hip_fail(hipError_t e, const char* what) {
+  return fail(GL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t esize(gl_dtype dt) { return dt == GL_BF16 ? 2 : 4; }
+int vec_width(gl_dtype dt) { return dt == GL_BF16 ? 8 : 4; }
+bool dtype_ok(gl_dtype dt) { return dt == GL_F32 || dt == GL_BF16; }
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+// Tensors must be indexable with the kernels' 32-bit row counters.
+bool size_ok(long long a, long long b, long long c) {
+  const long long r = a * b;
+  return a > 0 && b > 0 && c > 0 && r <= INT_MAX && r * c <= (1LL << 40);
+}
+
+gl_status check_knn(const void* x, int B, int N, int C, const void* keys, int M, int k, int dil,
+                    gl_dtype dt, const int32_t* idx_out) {
+  if (!x || !idx_out) return fail(GL_ERR_NULL_PTR, "knn: x and idx_out are required");
+  if (!dtype_ok(dt)) return fail(GL_ERR_UNSUPPORTED, "knn: unknown dtype %d", (int)dt);
+  if (B < 1 || N < 1 || C < 1 || B > 65535 || !size_ok(B, N, C))
+    return fail(GL_ERR_BAD_SHAPE, "knn: bad shape B=%d N=%d C=%d", B, N, C);
+  if (!keys && M != N) return fail(GL_ERR_BAD_SHAPE, "knn: keys=NULL needs M == N (M=%d N=%d)", M, N);
+  if (M < 1 || M > GL_MAX_M || !size_ok(B, M, C))
+    return fail(GL_ERR_BAD_SHAPE, "knn: M=%d outside [1, %d]", M, GL_MAX_M);
+  if (C % vec_width(dt))
+    return fail(GL_ERR_UNSUPPORTED, "knn: C=%d must be a multiple of %d", C, vec_width(dt));
+  if (k < 1 || dil < 1 || (long long)k * dil > M || (long long)k * dil > GL_MAX_KD)
+    return fail(GL_ERR_BAD_K, "knn: need 1<=k, 1<=dilation, k*dilation <= min(M=%d, %d); got k=%d d=%d",
+                M, GL_MAX_KD, k, dil);
+  if (!aligned(x, 16) || (keys && !aligned(keys, 16)) || !aligned(idx_out, 4))
+    return fail(GL_ERR_ALIGNMENT, "knn: x/keys need 16-byte, idx_out 4-byte alignment");
+  const size_t ib = (size_t)B * N * k * 4, xb = (size_t)B * N * C * esize(dt),
+               kb = keys ? (size_t)B * M * C * esize(dt) : 0;
+  if (overlap(idx_out, ib, x, xb) || overlap(idx_out, ib, keys, kb))
+    return fail(GL_ERR_ALIAS, "knn: idx_out overlaps x or keys");
+  return GL_OK;
+}
+
+gl_status check_pool(const void* x, int B, int H, int W, int C, int r, gl_dtype dt,
+                     const void* keys_out) {
+  if (!x || !keys_out) return fail(GL_ERR_NULL_PTR, "pool: x and keys_out are required");
+  if (!dtype_ok(dt)) return fail(GL_ERR_UNSUPPORTED, "pool: unknown dtype %d", (int)dt);
+  if (B < 1 || H < 1 || W < 1 || C < 1 || r < 1 || H % r || W % r || !size_ok(B, (long long)H * W, C))
+    return fail(GL_ERR_BAD_SHAPE, "pool: bad shape B=%d H=%d W=%d C=%d r=%d", B, H, W, C, r);
+  if (C % vec_width(dt))
+    return fail(GL_ERR_UNSUPPORTED, "pool: C=%d must be a multiple of %d", C, vec_width(dt));
+  if (!aligned(x, 16) || !aligned(keys_out, 16))
+    return fail(GL_ERR_ALIGNMENT, "pool: x/keys_out need 16-byte alignment");
+  const size_t xb = (size_t)B * H * W * C * esize(dt);
+  const size_t kb = (size_t)B * (H / r) * (W / r) * C * esize(dt);
+  if (overlap(x, xb, keys_out, kb)) return fail(GL_ERR_ALIAS, "pool: keys_out overlaps x");
+  return GL_OK;
+}
+
+gl_status check_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
+                       const int32_t* idx, int k, const void* W, const void* bias, int Cout,
+                       gl_dtype dt, const void* out, int* rt_out) {
+  if (!x || !idx || !W || !out) return fail(GL_ERR_NULL_PTR, "mrconv: x, idx, W and out are required");
+  if (!dtype_ok(dt)) return fail(GL_ERR_UNSUPPORTED, "mrconv: unknown dtype %d", (int)dt);
+  if (B < 1 || N < 1 || C < 1 || Cout < 1 || !size_ok(B, N, C) || !size_ok(B, N, Cout))
+    return fail(GL_ERR_BAD_SHAPE, "mrconv: bad shape B=%d N=%d C=%d Cout=%d", B, N, C, Cout);
+  if (!keys && M != N) return fail(GL_ERR_BAD_SHAPE, "mrconv: keys=NULL needs M == N");
+  if (M < 1 || !size_ok(B, M, C)) return fail(GL_ERR_BAD_SHAPE, "mrconv: bad M=%d", M);
+  if (k < 1 || k > GL_MAX_K) return fail(GL_ERR_BAD_K, "mrconv: k=%d outside [1, %d]", k, GL_MAX_K);
+  if (C % vec_width(dt))
+    return fail(GL_ERR_UNSUPPORTED, "mrconv: C=%d must be a multiple of %d", C, vec_width(dt));
+  const int dtb = dt == GL_BF16;
+  int rt = gl::mrconv_row_tiles(C, k, dtb, 65536);
+  if (!rt) rt = gl::mrconv_row_tiles(C, k, dtb, 160 * 1024);
+  if (!rt) return fail(GL_ERR_UNSUPPORTED, "mrconv: C=%d too wide for one LDS tile", C);
+  if (!aligned(x, 16) || (keys && !aligned(keys, 16)) || !aligned(W, 16) || !aligned(out, 16) ||
+      !aligned(idx, 4) || (bias && !aligned(bias, esize(dt))))
+    return fail(GL_ERR_ALIGNMENT, "mrconv: x/keys/W/out need 16-byte alignment");
+  const size_t es = esize(dt);
+  const size_t ob = (size_t)B * N * Cout * es;
+  if (overlap(out, ob, x, (size_t)B * N * C * es) ||
+      overlap(out, ob, keys, keys ? (size_t)B * M * C * es : 0) ||
+      overlap(out, ob, idx, (size_t)B * N * k * 4) || overlap(out, ob, W, (size_t)Cout * 2 * C * es) ||
+      overlap(out, ob, bias, bias ? (size_t)Cout * es : 0))
+    return fail(GL_ERR_ALIAS, "mrconv: out overlaps an input");
+  if (rt_out) *rt_out = rt;
+  return GL_OK;
+}
+
+constexpr uint32_t kHandleMagic = 0x474c4c41u;  // "GLLA"
+
+}  // namespace
+
+struct gl_lookahead {
+  uint32_t magic;
+  hipStream_t su, sb;
+  hipEvent_t ev_ready, ev_built;
+  bool pending;
+  int prof_max;
+  int prof_n[2];                                           // builds, updates
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> prof[2];
+};
+
+namespace {
+
+bool handle_ok(gl_lookahead_t h) { return h && h->magic == kHandleMagic; }
+
+void free_profiling(gl_lookahead_t h) {
+  for (int w = 0; w < 2; ++w) {
+    for (auto& p : h->prof[w]) {
+      (void)hipEventDestroy(p.first);
+      (void)hipEventDestroy(p.second);
+    }
+    h->prof[w].clear();
+    h->prof_n[w] = 0;
+  }
+  h->prof_max = 0;
+}
+
+// Bracket one launch with profiling events when enabled (which: 0 build, 1 update).
+template <class Launch>
+gl_status timed_launch(gl_lookahead_t h, int which, hipStream_t s, const char* what,
+                       Launch&& launch) {
+  hipError_t e;
+  const int i = h->prof_n[which];
+  const bool prof = i < h->prof_max;
+  if (prof && (e = hipEventRecord(h->prof[which][i].first, s)) != hipSuccess)
+    return hip_fail(e, "hipEventRecord");
+  if ((e = launch()) != hipSuccess) return hip_fail(e, what);
+  if (prof) {
+    if ((e = hipEventRecord(h->prof[which][i].second, s)) != hipSuccess)
+      return hip_fail(e, "hipEventRecord");
+    h->prof_n[which] = i + 1;
+  }
+  return GL_OK;
+}
+
+// kNN build on the build stream.
+gl_status enqueue_build(gl_lookahead_t h, const void* x, int B, int N, int C, const void* keys,
+                        int M, int k, int dil, gl_dtype dt, int32_t* idx) {
+  return timed_launch(h, GL_TIME_BUILD, h->sb, "knn launch", [&] {
+    return gl::launch_knn(x, keys ? keys : x, B, N, C, M, k, dil, dt == GL_BF16, idx, h->sb);
+  });
+}
+
+// Order the build stream after the update stream's work so far.
+gl_status fork_build(gl_lookahead_t h) {
+  hipError_t e;
+  if ((e = hipEventRecord(h->ev_ready, h->su)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if ((e = hipStreamWaitEvent(h->sb, h->ev_ready, 0)) != hipSuccess)
+    return hip_fail(e, "hipStreamWaitEvent");
+  return GL_OK;
+}
+
+gl_status mark_built(gl_lookahead_t h) {
+  hipError_t e = hipEventRecord(h->ev_built, h->sb);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  h->pending = true;
+  return GL_OK;
+}
+
+gl_status join_build(gl_lookahead_t h) {
+  if (!h->pending) return GL_OK;
+  hipError_t e = hipStreamWaitEvent(h->su, h->ev_built, 0);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+  h->pending = false;
+  return GL_OK;
+}
+
+struct BlockArgs {
+  const void* x_in;
+  int B, H, W, C, pool_r;
+  void* keys_ws;
+  const int32_t* idx_use;
+  int k;
+  const void* Wt;
+  const void* bias;
+  gl_dtype dt;
+  void* x_out;
+  int32_t* idx_next;
+  int dil_next;
+};
+
+gl_status check_block(const BlockArgs& a, int* rt) {
+  const int N = a.H * a.W;
+  const bool pooled = a.pool_r > 1;
+  const int M = pooled ? (a.H / a.pool_r) * (a.W / a.pool_r) : N;
+  gl_status s;
+  if (a.H < 1 || a.W < 1 || a.pool_r < 1)
+    return fail(GL_ERR_BAD_SHAPE, "block: bad grid H=%d W=%d r=%d", a.H, a.W, a.pool_r);
+  if (pooled) {
+    if (!a.keys_ws) return fail(GL_ERR_NULL_PTR, "block: pool_r > 1 needs keys_ws");
+    if ((s = check_pool(a.x_in, a.B, a.H, a.W, a.C, a.pool_r, a.dt, a.keys_ws)) != GL_OK) return s;
+  }
+  const void* keys = pooled ? a.keys_ws : nullptr;
+  if ((s = check_mrconv(a.x_in, a.B, N, a.C, keys, M, a.idx_use, a.k, a.Wt, a.bias, a.C, a.dt,
+                        a.x_out, rt)) != GL_OK)
+    return s;
+  if (pooled && overlap(a.x_out, (size_t)a.B * N * a.C * esize(a.dt), a.keys_ws,
+                        (size_t)a.B * M * a.C * esize(a.dt)))
+    return fail(GL_ERR_ALIAS, "block: x_out overlaps keys_ws");
+  if (a.idx_next) {
+    if ((s = check_knn(a.x_in, a.B, N, a.C, keys, M, a.k, a.dil_next, a.dt, a.idx_next)) != GL_OK)
+      return s;
+    const size_t ib = (size_t)a.B * N * a.k * 4;
+    if (overlap(a.idx_next, ib, a.idx_use, ib))
+      return fail(GL_ERR_ALIAS, "block: idx_next overlaps idx_use");
+    if (overlap(a.idx_next, ib, a.x_out, (size_t)a.B * N * a.C * esize(a.dt)))
+      return fail(GL_ERR_ALIAS, "block: idx_next overlaps x_out");
+  }
+  return GL_OK;
+}
+
+// Enqueue one lookahead block whose arguments were checked.
+gl_status enqueue_block(gl_lookahead_t h, const BlockArgs& a, int rt, bool do_pool) {
+  const int N = a.H * a.W;
+  const bool pooled = a.pool_r > 1;
+  const int M = pooled ? (a.H / a.pool_r) * (a.W / a.pool_r) : N;
+  const void* keys = pooled ? a.keys_ws : a.x_in;
+  gl_status s;
+  hipError_t e;
+  if ((s = join_build(h)) != GL_OK) return s;  // idx_use is ready; old buffers are free
+  if (pooled && do_pool) {
+    e = gl::launch_pool(a.x_in, a.keys_ws, a.B, a.H, a.W, a.C, a.pool_r, a.dt == GL_BF16, h->su);
+    if (e != hipSuccess) return hip_fail(e, "pool launch");
+  }
+  if (a.idx_next) {
+    if ((s = fork_build(h)) != GL_OK) return s;
+    if ((s = enqueue_build(h, a.x_in, a.B, N, a.C, pooled ? a.keys_ws : nullptr, M, a.k,
+                           a.dil_next, a.dt, a.idx_next)) != GL_OK)
+      return s;
+    if ((s = mark_built(h)) != GL_OK) return s;
+  }
+  return timed_launch(h, GL_TIME_UPDATE, h->su, "mrconv launch", [&] {
+    return gl::launch_mrconv(a.x_in, keys, a.idx_use, a.Wt, a.bias, a.x_out, a.B, N, M, a.C, a.C,
+                             a.k, a.dt == GL_BF16, rt, h->su);
+  });
+}
+
+}  // namespace
+
+extern "C" {
+
+int gl_version(void) { return GL_VERSION; }
+
+const char* gl_status_string(gl_status s) {
+  switch (s) {
+    case GL_OK: return "GL_OK";
+    case GL_ERR_NULL_PTR: return "GL_ERR_NULL_PTR";
+    case GL_ERR_BAD_SHAPE: return "GL_ERR_BAD_SHAPE";
+    case GL_ERR_BAD_K: return "GL_ERR_BAD_K";
+    case GL_ERR_UNSUPPORTED: return "GL_ERR_UNSUPPORTED";
+    case GL_ERR_ALIGNMENT: return "GL_ERR_ALIGNMENT";
+    case GL_ERR_ALIAS: return "GL_ERR_ALIAS";
+    case GL_ERR_HIP: return "GL_ERR_HIP";
+    case GL_ERR_BAD_HANDLE: return "GL_ERR_BAD_HANDLE";
+  }
+  return "GL_ERR_UNKNOWN";
+}
+
+const char* gl_last_error(void) { return g_last_error.c_str(); }
+
+gl_status gl_knn_graph(const void* x, int B, int N, int C, const void* keys, int M, int k,
+                       int dilation, gl_dtype dt, int32_t* idx_out, hipStream_t stream) {
+  gl_status s = check_knn(x, B, N, C, keys, M, k, dilation, dt, idx_out);
+  if (s != GL_OK) return s;
+  hipError_t e = gl::launch_knn(x, keys ? keys : x, B, N, C, M, k, dilation, dt == GL_BF16,
+                                idx_out, stream);
+  return e == hipSuccess ? GL_OK : hip_fail(e, "knn launch");
+}
+
+gl_status gl_pool_keys(const void* x, int B, int H, int W, int C, int r, gl_dtype dt,
+                       void* keys_out, hipStream_t stream) {
+  gl_status s = check_pool(x, B, H, W, C, r, dt, keys_out);
+  if (s != GL_OK) return s;
+  hipError_t e = gl::launch_pool(x, keys_out, B, H, W, C, r, dt == GL_BF16, stream);
+  return e == hipSuccess ? GL_OK : hip_fail(e, "pool launch");
+}
+
+gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
+                    const int32_t* idx, int k, const void* W, const void* bias, int Cout,
+                    gl_dtype dt, void* out, hipStream_t stream) {
+  int rt = 0;
+  gl_status s = check_mrconv(x, B, N, C, keys, M, idx, k, W, bias, Cout, dt, out, &rt);
+  if (s != GL_OK) return s;
+  hipError_t e = gl::launch_mrconv(x, keys ? keys : x, idx, W, bias, out, B, N, M, C, Cout, k,
+                                   dt == GL_BF16, rt, stream);
+  return e == hipSuccess ? GL_OK : hip_fail(e, "mrconv launch");
+}
+
+gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_lookahead_t* out) {
+  if (!out) return fail(GL_ERR_NULL_PTR, "lookahead_create: out is NULL");
+  *out = nullptr;
+  gl_lookahead* h = new gl_lookahead();
+  h->magic = kHandleMagic;
+  h->su = s_update;
+  h->sb = s_build;
+  h->pending = false;
+  h->prof_max = 0;
+  h->prof_n[0] = h->prof_n[1] = 0;
+  hipError_t e = hipEventCreateWithFlags(&h->ev_ready, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    delete h;
+    return hip_fail(e, "hipEventCreate");
+  }
+  e = hipEventCreateWithFlags(&h->ev_built, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    (void)hipEventDestroy(h->ev_ready);
+    delete h;
+    return hip_fail(e, "hipEventCreate");
+  }
+  *out = h;
+  return GL_OK;
+}
+
+gl_status gl_lookahead_destroy(gl_lookahead_t h) {
+  if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "lookahead_destroy: bad handle");
+  free_profiling(h);
+  (void)hipEventDestroy(h->ev_ready);
+  (void)hipEventDestroy(h->ev_built);
+  h->magic = 0;
+  delete h;
+  return GL_OK;
+}
+
+gl_status gl_lookahead_set_profiling(gl_lookahead_t h, int max_records) {
+  if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "set_profiling: bad handle");
+  if (max_records < 0 || max_records > 1 << 20)
+    return fail(GL_ERR_BAD_SHAPE, "set_profiling: max_records=%d", max_records);
+  free_profiling(h);
+  for (int w = 0; w < 2; ++w) {
+    for (int i = 0; i < max_records; ++i) {
+      hipEvent_t a, b;
+      hipError_t e = hipEventCreate(&a);
+      if (e != hipSuccess) {
+        free_profiling(h);
+        return hip_fail(e, "hipEventCreate");
+      }
+      if ((e = hipEventCreate(&b)) != hipSuccess) {
+        (void)hipEventDestroy(a);
+        free_profiling(h);
+        return hip_fail(e, "hipEventCreate");
+      }
+      h->prof[w].emplace_back(a, b);
+    }
+  }
+  h->prof_max = max_records;
+  return GL_OK;
+}
+
+gl_status gl_lookahead_kernel_times(gl_lookahead_t h, int which, float* ms_out, int cap,
+                                    int* n_out) {
+  if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "kernel_times: bad handle");
+  if (which != GL_TIME_BUILD && which != GL_TIME_UPDATE)
+    return fail(GL_ERR_UNSUPPORTED, "kernel_times: which=%d", which);
+  if (!n_out || (cap > 0 && !ms_out)) return fail(GL_ERR_NULL_PTR, "kernel_times: null output");
+  const int n = h->prof_n[which] < cap ? h->prof_n[which] : cap;
+  for (int i = 0; i < n; ++i) {
+    const auto& p = h->prof[which][i];
+    hipError_t e = hipEventSynchronize(p.second);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    if ((e = hipEventElapsedTime(&ms_out[i], p.first, p.second)) != hipSuccess)
+      return hip_fail(e, "hipEventElapsedTime");
+  }
+  *n_out = n;
+  h->prof_n[which] = 0;
+  return GL_OK;
+}
+
+gl_status gl_lookahead_bootstrap(gl_lookahead_t h, const void* x0, int B, int H, int W, int C,
+                                 int pool_r, void* keys_ws, int k, int dilation0, gl_dtype dt,
+                                 int32_t* idx0) {
+  if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "bootstrap: bad handle");
+  if (H < 1 || W < 1 || pool_r < 1) return fail(GL_ERR_BAD_SHAPE, "bootstrap: bad grid");
+  const bool pooled = pool_r > 1;
+  const int N = H * W, M = pooled ? (H / pool_r) * (W / pool_r) : N;
+  gl_status s;
+  if (pooled) {
+    if (!keys_ws) return fail(GL_ERR_NULL_PTR, "bootstrap: pool_r > 1 needs keys_ws");
+    if ((s = check_pool(x0, B, H, W, C, pool_r, dt, keys_ws)) != GL_OK) return s;
+  }
+  if ((s = check_knn(x0, B, N, C, pooled ? keys_ws : nullptr, M, k, dilation0, dt, idx0)) != GL_OK)
+    return s;
+  if ((s = join_build(h)) != GL_OK) return s;
+  if (pooled) {
+    hipError_t e = gl::launch_pool(x0, keys_ws, B, H, W, C, pool_r, dt == GL_BF16, h->su);
+    if (e != hipSuccess) return hip_fail(e, "pool launch");
+  }
+  if ((s = fork_build(h)) != GL_OK) return s;
+  if ((s = enqueue_build(h, x0, B, N, C, pooled ? keys_ws : nullptr, M, k, dilation0, dt, idx0)) !=
+      GL_OK)
+    return s;
+  return mark_built(h);
+}
+
+gl_status gl_graphleap_block(gl_lookahead_t h, const void* x_in, int B, int H, int W, int C,
+                             int pool_r, void* keys_ws, const int32_t* idx_use, int k,
+                             const void* Wt, const void* bias, gl_dtype dt, void* x_out,
+                             int32_t* idx_next, int dilation_next) {
+  if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "graphleap_block: bad handle");
+  BlockArgs a{x_in, B, H, W, C, pool_r, keys_ws, idx_use, k, Wt, bias, dt, x_out, idx_next,
+              dilation_next};
+  int rt = 0;
+  gl_status s = check_block(a, &rt);
+  if (s != GL_OK) return s;
+  return enqueue_block(h, a, rt, true);
+}
+
+gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int W, int C,
+                             int pool_r, int L, int k, const int* dilations, const void* Ws,
+                             const void* bs, gl_dtype dt, gl_schedule schedule, void* x_ws,
+                             int32_t* idx_ws, void* keys_ws, void* x_out) {
+  if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "graphleap_stack: bad handle");
+  if (!x0 || !dilations || !Ws || !x_ws || !idx_ws || !x_out)
+    return fail(GL_ERR_NULL_PTR, "graphleap_stack: x0, dilations, Ws, x_ws, idx_ws, x_out required");
+  if (schedule != GL_SCHED_LOOKAHEAD && schedule != GL_SCHED_STANDARD)
+    return fail(GL_ERR_UNSUPPORTED, "graphleap_stack: unknown schedule %d", (int)schedule);
+  if (L < 1 || L > 4096) return fail(GL_ERR_BAD_SHAPE, "graphleap_stack: L=%d", L);
+  if (!dtype_ok(dt)) return fail(GL_ERR_UNSUPPORTED, "graphleap_stack: unknown dtype");
+  if (H < 1 || W < 1 || pool_r < 1 || B < 1 || C < 1 || !size_ok(B, (long long)H * W, C))
+    return fail(GL_ERR_BAD_SHAPE, "graphleap_stack: bad shape");
+  const int N = H * W;
+  const bool pooled = pool_r > 1;
+  const size_t es = esize(dt);
+  const size_t xbytes = (size_t)B * N * C * es, ibytes = (size_t)B * N * k * 4;
+  const size_t wbytes = (size_t)C * 2 * C * es, bbytes = (size_t)C * es;
+  const int M = pooled ? (H / pool_r) * (W / pool_r) : N;
+  const size_t kbytes = pooled ? (size_t)B * M * C * es : 0;
+  if (overlap(x_out, xbytes, x_ws, 2 * xbytes) || overlap(x_out, xbytes, idx_ws, 2 * ibytes) ||
+      overlap(x_out, xbytes, keys_ws, kbytes) || overlap(x_out, xbytes, x0, xbytes) ||
+      overlap(x_ws, 2 * xbytes, idx_ws, 2 * ibytes) || overlap(x_ws, 2 * xbytes, keys_ws, kbytes) ||
+      overlap(x_ws, 2 * xbytes, x0, xbytes) || overlap(idx_ws, 2 * ibytes, keys_ws, kbytes) ||
+      overlap(idx_ws, 2 * ibytes, x0, xbytes) || overlap(keys_ws, kbytes, x0, xbytes))
+    return fail(GL_ERR_ALIAS, "graphleap_stack: workspaces overlap each other or x0");
+  char* xw[2] = {static_cast<char*>(x_ws), static_cast<char*>(x_ws) + xbytes};
+  int32_t* iw[2] = {idx_ws, idx_ws + (size_t)B * N * k};
+  const char* Wb = static_cast<const char*>(Ws);
+  const char* bb = static_cast<const char*>(bs);
+
+  // check every block before enqueuing anything
+  std::vector<BlockArgs> blocks(L);
+  std::vector<int> rts(L);
+  for (int l = 0; l < L; ++l) {
+    BlockArgs& a = blocks[l];
+    a = BlockArgs{l == 0 ? x0 : xw[(l - 1) & 1], B, H, W, C, pool_r, keys_ws, iw[0], k,
+                  Wb + l * wbytes, bb ? bb + l * bbytes : nullptr, dt,
+                  l == L - 1 ? x_out : static_cast<void*>(xw[l & 1]), nullptr, 1};
+    if (schedule == GL_SCHED_LOOKAHEAD && l + 1 < L) {
+      a.idx_next = iw[1];
+      a.dil_next = dilations[l + 1];
+    }
+    gl_status s = check_block(a, &rts[l]);
+    if (s != GL_OK) return s;
+    if ((s = check_knn(a.x_in, B, N, C, pooled ? keys_ws : nullptr, M, k, dilations[l], dt, iw[0])) !=
+        GL_OK)
+      return s;
+  }
+
+  gl_status s;
+  if (schedule == GL_SCHED_STANDARD) {
+    if ((s = join_build(h)) != GL_OK) return s;
+    for (int l = 0; l < L; ++l) {
+      BlockArgs a = blocks[l];
+      hipError_t e;
+      if (pooled) {
+        e = gl::launch_pool(a.x_in, keys_ws, B, H, W, C, pool_r, dt == GL_BF16, h->su);
+        if (e != hipSuccess) return hip_fail(e, "pool launch");
+      }
+      e = gl::launch_knn(a.x_in, pooled ? keys_ws : a.x_in, B, N, C, M, k, dilations[l],
+                         dt == GL_BF16, iw[0], h->su);
+      if (e != hipSuccess) return hip_fail(e, "knn launch");
+      e = gl::launch_mrconv(a.x_in, pooled ? keys_ws : a.x_in, iw[0], a.Wt, a.bias, a.x_out, B, N,
+                            M, C, C, k, dt == GL_BF16, rts[l], h->su);
+      if (e != hipSuccess) return hip_fail(e, "mrconv launch");
+    }
+    return GL_OK;
+  }
+
+  // lookahead: Ghat^0 = G(X^0, d_0) into iw[0]
+  if ((s = gl_lookahead_bootstrap(h, x0, B, H, W, C, pool_r, keys_ws, k, dilations[0], dt, iw[0])) !=
+      GL_OK)
+    return s;
+  int cur = 0;  // buffer holding Ghat^l
+  for (int l = 0; l < L; ++l) {
+    BlockArgs a = blocks[l];
+    a.idx_use = iw[cur];
+    int next = cur;
+    a.idx_next = nullptr;
+    if (l + 1 < L) {
+      if (l == 0 && dilations[1] == dilations[0]) {
+        next = cur;  // Ghat^1 = G(X^0, d_1) is the bootstrap graph itself
+      } else {
+        next = 1 - cur;
+        a.idx_next = iw[next];
+        a.dil_next = dilations[l + 1];
+      }
+    }
+    if ((s = enqueue_block(h, a, rts[l], /*do_pool=*/l > 0)) != GL_OK) return s;
+    cur = next;
+  }
+  return GL_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,128 @@
+"""C ABI checks that need no GPU: the library loads, exports every entry point
+the header declares, and rejects bad arguments on the host before any HIP
+call (fake, never-dereferenced addresses stand in for device pointers)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2604_21290_amd import api
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "graphleap.h")
+
+import torch  # noqa: E402
+
+pytestmark = pytest.mark.skipif(not os.path.exists(api.LIB_PATH),
+                                reason="libgraphleap.so not built")
+# Fake addresses must never reach a real device: the validation checks run
+# only where no GPU is visible (device_count does not initialise the runtime).
+host_only = pytest.mark.skipif(torch.cuda.device_count() > 0,
+                               reason="host-only checks (fake pointers)")
+
+A = 1 << 20          # fake 16-byte-aligned device addresses, far apart
+P = lambda i: ctypes.c_void_p(A * (i + 1))  # noqa: E731
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:gl_status|const char\*|int)\s+(gl_\w+)\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = header_functions()
+    assert len(names) >= 12
+    L = api.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(api.SIGNATURES), "binding and header disagree"
+
+
+def test_header_constants_match_binding():
+    text = open(HEADER).read()
+    for name in ("GL_MAX_KD", "GL_MAX_M", "GL_MAX_K"):
+        v = int(re.search(rf"#define {name} (\d+)", text).group(1))
+        assert v == getattr(api, name)
+
+
+def _knn(x=P(0), B=2, N=196, C=192, keys=None, M=196, k=9, d=1, dt=1, out=P(40)):
+    st = api.lib().gl_knn_graph(x, B, N, C, keys, M, k, d, dt, out, None)
+    return api.STATUS[st], api.lib().gl_last_error().decode()
+
+
+@host_only
+def test_knn_validation():
+    assert _knn(x=None)[0] == "GL_ERR_NULL_PTR"
+    assert _knn(out=None)[0] == "GL_ERR_NULL_PTR"
+    assert _knn(dt=7)[0] == "GL_ERR_UNSUPPORTED"
+    assert _knn(B=0)[0] == "GL_ERR_BAD_SHAPE"
+    assert _knn(N=0, M=0)[0] == "GL_ERR_BAD_SHAPE"
+    assert _knn(M=100)[0] == "GL_ERR_BAD_SHAPE"           # keys = x needs M == N
+    assert _knn(keys=P(10), M=5000)[0] == "GL_ERR_BAD_SHAPE"
+    assert _knn(C=12)[0] == "GL_ERR_UNSUPPORTED"           # bf16 needs C % 8 == 0
+    assert _knn(C=10, dt=0)[0] == "GL_ERR_UNSUPPORTED"     # fp32 needs C % 4 == 0
+    assert _knn(k=0)[0] == "GL_ERR_BAD_K"
+    assert _knn(d=0)[0] == "GL_ERR_BAD_K"
+    assert _knn(k=33, d=2)[0] == "GL_ERR_BAD_K"             # k*d > 64
+    assert _knn(keys=P(10), M=10, k=6, d=2)[0] == "GL_ERR_BAD_K"   # k*d > M
+    assert _knn(x=ctypes.c_void_p(A + 8))[0] == "GL_ERR_ALIGNMENT"
+    assert _knn(out=ctypes.c_void_p(A * 41 + 2))[0] == "GL_ERR_ALIGNMENT"
+    assert _knn(out=ctypes.c_void_p(A + 4096))[0] == "GL_ERR_ALIAS"  # idx inside x
+    st, msg = _knn(k=65)
+    assert st == "GL_ERR_BAD_K" and "k*dilation" in msg
+
+
+def _mr(x=P(0), B=2, N=196, C=192, keys=None, M=196, idx=P(20), k=9, W=P(30), bias=None,
+        Cout=192, dt=1, out=P(40)):
+    st = api.lib().gl_mrconv(x, B, N, C, keys, M, idx, k, W, bias, Cout, dt, out, None)
+    return api.STATUS[st]
+
+
+@host_only
+def test_mrconv_validation():
+    assert _mr(x=None) == "GL_ERR_NULL_PTR"
+    assert _mr(idx=None) == "GL_ERR_NULL_PTR"
+    assert _mr(W=None) == "GL_ERR_NULL_PTR"
+    assert _mr(out=None) == "GL_ERR_NULL_PTR"
+    assert _mr(dt=2) == "GL_ERR_UNSUPPORTED"
+    assert _mr(Cout=0) == "GL_ERR_BAD_SHAPE"
+    assert _mr(M=10) == "GL_ERR_BAD_SHAPE"
+    assert _mr(k=0) == "GL_ERR_BAD_K"
+    assert _mr(k=65) == "GL_ERR_BAD_K"
+    assert _mr(C=20) == "GL_ERR_UNSUPPORTED"
+    assert _mr(C=8192) == "GL_ERR_UNSUPPORTED"               # too wide for one LDS tile
+    assert _mr(W=ctypes.c_void_p(A * 31 + 4)) == "GL_ERR_ALIGNMENT"
+    assert _mr(bias=ctypes.c_void_p(A * 50 + 1)) == "GL_ERR_ALIGNMENT"
+    assert _mr(out=ctypes.c_void_p(A + 64)) == "GL_ERR_ALIAS"    # out inside x
+    assert _mr(out=ctypes.c_void_p(A * 31 + 64)) == "GL_ERR_ALIAS"  # out inside W
+
+
+def _pool(x=P(0), B=2, H=56, W=56, C=80, r=4, dt=1, out=P(40)):
+    return api.STATUS[api.lib().gl_pool_keys(x, B, H, W, C, r, dt, out, None)]
+
+
+@host_only
+def test_pool_validation():
+    assert _pool(out=None) == "GL_ERR_NULL_PTR"
+    assert _pool(r=3) == "GL_ERR_BAD_SHAPE"
+    assert _pool(r=0) == "GL_ERR_BAD_SHAPE"
+    assert _pool(C=12) == "GL_ERR_UNSUPPORTED"
+    assert _pool(out=ctypes.c_void_p(A + 16)) == "GL_ERR_ALIAS"
+
+
+@host_only
+def test_handle_validation():
+    L = api.lib()
+    assert api.STATUS[L.gl_lookahead_destroy(None)] == "GL_ERR_BAD_HANDLE"
+    assert api.STATUS[L.gl_lookahead_set_profiling(None, 4)] == "GL_ERR_BAD_HANDLE"
+    assert api.STATUS[L.gl_graphleap_block(None, P(0), 1, 14, 14, 192, 1, None, P(1), 9, P(2),
+                                           None, 1, P(3), None, 1)] == "GL_ERR_BAD_HANDLE"
+    assert api.STATUS[L.gl_lookahead_create(None, None, None)] == "GL_ERR_NULL_PTR"
+
+
+def test_status_strings():
+    L = api.lib()
+    for code, name in api.STATUS.items():
+        assert L.gl_status_string(code).decode() == name
+    assert L.gl_status_string(99).decode() == "GL_ERR_UNKNOWN"

@@ -1,0 +1,102 @@
+"""GPU parity of gl_mrconv (fused gather-max + FC) against the CPU oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from gpu_helpers import check_close, from_dev, require_gpu, to_dev
+from paper_2604_21290_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[gpu-test]", *a, flush=True)
+
+
+def _mr_case(x, idx, Wt, bias=None, keys=None, label=""):
+    from paper_2604_21290_amd import api
+    _say("mrconv", label, tuple(x.shape), "k", idx.shape[2], "Cout", Wt.shape[0])
+    out = api.mrconv(to_dev(x), torch.from_numpy(idx).cuda(), to_dev(Wt),
+                     None if bias is None else to_dev(bias),
+                     keys=None if keys is None else to_dev(keys))
+    torch.cuda.synchronize()
+    got = from_dev(out).value
+    ref = O.mrconv_ref(x.value, idx, Wt.value, None if bias is None else bias.value,
+                       keys=None if keys is None else keys.value)
+    return check_close(got, ref, x.dtype, label)
+
+
+@pytest.mark.parametrize("name", ["single", "vig_ti", "vig_b", "pyr_s1", "pyr_s2", "hires"])
+def test_mrconv_workload_full(name):
+    """Full-size update with the workload's own graph (built by the oracle on
+    a sample of images for speed; indices are inputs here)."""
+    require_gpu()
+    w = I.WORKLOADS[name]
+    x = I.make_features(w)
+    keys = None
+    if w.pool_r > 1:
+        keys = I.store(O.pool_keys_ref(x.value, w.H, w.W, w.pool_r), w.dtype)
+    idx = I.random_indices(w.seed, w.B, w.N, w.k, w.M)
+    # self-loop in slot 0 for the unpooled graphs, as the kNN graph has it
+    if w.pool_r == 1:
+        idx[:, :, 0] = np.arange(w.N)[None, :]
+    Wt = I.make_weight(w, 0)
+    rel = _mr_case(x, idx, Wt, I.make_bias(w, 0, zero=False), keys, label=name)
+    _say(name, "max rel err", rel)
+
+
+EDGE = [
+    # label, B, N, M (None: keys = x), C, Cout, k, dtype, bias
+    ("k1_self", 2, 30, None, 16, 16, 1, I.BF16, False),
+    ("ragged_tile_rows", 3, 37, None, 24, 40, 5, I.BF16, True),
+    ("cout_8", 1, 50, None, 32, 8, 3, I.BF16, True),
+    ("cout_wide", 1, 20, None, 32, 200, 4, I.BF16, False),
+    ("pooled_keys", 2, 64, 16, 40, 40, 9, I.BF16, True),
+    ("fp32_small", 2, 21, None, 12, 20, 7, I.F32, True),
+    ("fp32_vig", 1, 196, None, 192, 192, 9, I.F32, False),
+    ("k_max_64", 1, 70, None, 16, 16, 64, I.BF16, True),
+    ("wide_C_1024", 1, 40, None, 1024, 64, 9, I.BF16, True),
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=[c[0] for c in EDGE])
+def test_mrconv_edges(case):
+    require_gpu()
+    label, B, N, M, C, Cout, k, dt, with_bias = case
+    g = np.random.default_rng(C * 7 + N)
+    x = I.store(g.standard_normal((B, N, C)), dt)
+    keys = None if M is None else I.store(g.standard_normal((B, M, C)), dt)
+    Mk = N if M is None else M
+    idx = g.integers(0, Mk, (B, N, k)).astype(np.int32)
+    if label == "k1_self":
+        idx[:, :, 0] = np.arange(N)
+    Wt = I.store(g.uniform(-0.2, 0.2, (Cout, 2 * C)), dt)
+    bias = I.store(g.uniform(-1, 1, Cout), dt) if with_bias else None
+    _mr_case(x, idx, Wt, bias, keys, label=label)
+
+
+def test_mrconv_self_only_is_x_times_Wx():
+    """k = 1 with each node its own neighbour: m = 0, out = x W_x^T (exact parts)."""
+    require_gpu()
+    from paper_2604_21290_amd import api
+    g = np.random.default_rng(3)
+    x = I.store(g.standard_normal((1, 32, 16)), I.BF16)
+    idx = np.arange(32, dtype=np.int32)[None, :, None]
+    Wi = I.store(np.hstack([np.eye(16), g.standard_normal((16, 16))]), I.BF16)
+    out = api.mrconv(to_dev(x), torch.from_numpy(idx).cuda(), to_dev(Wi))
+    torch.cuda.synchronize()
+    assert np.array_equal(from_dev(out).value, x.value)
+
+
+def test_mrconv_deterministic():
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = I.with_batch(I.WORKLOADS["vig_ti"], 4)
+    x = to_dev(I.make_features(w))
+    idx = torch.from_numpy(I.random_indices(1, 4, w.N, w.k, w.M)).cuda()
+    Wt = to_dev(I.make_weight(w, 0))
+    a = api.mrconv(x, idx, Wt)
+    b = api.mrconv(x, idx, Wt)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)

@@ -1,0 +1,193 @@
+"""GPU parity of the GraphLeap lookahead (gl_lookahead_bootstrap,
+gl_graphleap_block, gl_graphleap_stack) and of the standard schedule.
+
+Every block is teacher-forced: the graph it used is checked against the oracle
+kNN of the exact stored features (and pooled keys) it was built from, and its
+output against the oracle MRConv of its exact stored inputs.  Free-running
+fp64 stacks are not compared (near-tie flips may legitimately diverge)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from gpu_helpers import check_close, check_idx, from_dev, require_gpu, to_dev
+from paper_2604_21290_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[gpu-test]", *a, flush=True)
+
+
+def _weights(w, L, zero_bias=True):
+    Ws = [I.make_weight(w, l) for l in range(L)]
+    bs = [I.make_bias(w, l, zero=zero_bias) for l in range(L)]
+    Wst = I.Stored(np.stack([s.bits for s in Ws]), np.stack([s.value for s in Ws]), w.dtype)
+    bst = I.Stored(np.stack([s.bits for s in bs]), np.stack([s.value for s in bs]), w.dtype)
+    return Wst, bst
+
+
+def run_blocks(w, x0d, Wd, bd, same_stream=False):
+    """Drive the lookahead block by block; return (features, graphs used)."""
+    from paper_2604_21290_amd import api
+    B, N, C = x0d.shape
+    L, dil = w.L, w.dilations
+    s_up = torch.cuda.current_stream()
+    la = api.Lookahead(s_up, s_up if same_stream else torch.cuda.Stream())
+    bufs = [torch.empty((B, N, w.k), dtype=torch.int32, device="cuda") for _ in range(2)]
+    keys_ws = (torch.empty((B, w.M, C), dtype=x0d.dtype, device="cuda") if w.pool_r > 1 else None)
+    la.bootstrap(x0d, w.H, w.W, w.k, dil[0], w.pool_r, keys_ws, bufs[0])
+    xs, graphs, cur = [x0d], [], 0
+    for l in range(L):
+        idx_next, nxt = None, cur
+        if l + 1 < L:
+            if not (l == 0 and dil[1] == dil[0]):
+                nxt = 1 - cur
+                idx_next = bufs[nxt]
+        torch.cuda.synchronize()
+        graphs.append(bufs[cur].clone())
+        x_out = torch.empty_like(x0d)
+        la.block(xs[-1], w.H, w.W, bufs[cur], Wd[l], bd[l], w.pool_r, keys_ws, x_out,
+                 idx_next, dil[l + 1] if idx_next is not None else 1)
+        xs.append(x_out)
+        cur = nxt
+    torch.cuda.synchronize()
+    la.close()
+    return xs, graphs
+
+
+def teacher_forced_checks(w, xs, graphs, Wst, bst, schedule="lookahead", n_img=None,
+                          rows=None):
+    """xs: GPU features X^0..X^L; graphs: GPU graph used by each block."""
+    from paper_2604_21290_amd import api
+    src = O.graph_source_blocks(w.L, schedule)
+    sl = slice(None) if n_img is None else slice(0, n_img)
+    host = [from_dev(x) for x in xs]
+    stats = []
+    for l in range(w.L):
+        xg = host[src[l]].value[sl]
+        keys_g = keys_u = None
+        if w.pool_r > 1:
+            kg = from_dev(api.pool_keys(xs[src[l]], w.H, w.W, w.pool_r))
+            check_close(kg.value[sl], O.pool_keys_ref(xg, w.H, w.W, w.pool_r), w.dtype,
+                        f"pool block {l}")
+            keys_g = kg.value[sl]
+            keys_u = from_dev(api.pool_keys(xs[l], w.H, w.W, w.pool_r)).value[sl]
+        g = graphs[l].cpu().numpy()[sl]
+        D = O.knn_distances(xg, keys_g, rows=rows)
+        st = check_idx(g, D, w.k, w.dilations[l], rows=rows, label=f"{w.name} graph {l}")
+        ref = O.mrconv_ref(host[l].value[sl], g, Wst.value[l], bst.value[l], keys=keys_u)
+        rel = check_close(host[l + 1].value[sl], ref, w.dtype, f"{w.name} block {l}")
+        stats.append((l, st["near_tie_rows"], rel))
+    _say(w.name, schedule, "per-block (block, near-tie rows, rel err):", stats)
+
+
+CASES = [
+    # name, batch used on the GPU, images checked against the oracle, sampled rows
+    ("single", None, None, None),
+    ("vig_ti", None, None, None),
+    ("vig_b", 16, 4, None),
+    ("pyr_s1", 8, 4, 384),
+    ("pyr_s2", 8, 4, None),
+    ("hires", None, 2, 384),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_lookahead_blocks_teacher_forced(case):
+    require_gpu()
+    name, B, n_img, nrows = case
+    w = I.WORKLOADS[name] if B is None else I.with_batch(I.WORKLOADS[name], B)
+    rows = None
+    if nrows is not None:
+        rows = np.sort(np.random.default_rng(7).choice(w.N, nrows, replace=False))
+    x0 = I.make_features(w)
+    Wst, bst = _weights(w, w.L)
+    x0d, Wd, bd = to_dev(x0), to_dev(Wst), to_dev(bst)
+    _say("lookahead blocks", name, "B", w.B)
+    xs, graphs = run_blocks(w, x0d, Wd, bd)
+    teacher_forced_checks(w, xs, graphs, Wst, bst, n_img=n_img, rows=rows)
+
+
+@pytest.mark.parametrize("name", ["vig_ti", "vig_b", "pyr_s1", "hires"])
+def test_stack_entry_matches_blocks_and_serial(name):
+    """gl_graphleap_stack at the full workload size (the launch configuration
+    the benchmark times) equals the block-by-block run bit for bit, and the
+    overlapped run equals the same kernels on one stream."""
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = I.WORKLOADS[name]
+    x0 = I.make_features(w)
+    Wst, bst = _weights(w, w.L)
+    x0d, Wd, bd = to_dev(x0), to_dev(Wst), to_dev(bst)
+    _say("stack entry", name)
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    out = la.stack(x0d, w.H, w.W, Wd, bd, list(w.dilations), w.k, w.pool_r)
+    out2 = la.stack(x0d, w.H, w.W, Wd, bd, list(w.dilations), w.k, w.pool_r)
+    torch.cuda.synchronize()
+    la.close()
+    assert torch.equal(out, out2), "stack not deterministic"
+    xs, _ = run_blocks(w, x0d, Wd, bd)
+    assert torch.equal(out, xs[-1]), "stack entry differs from block-by-block"
+    xs1, _ = run_blocks(w, x0d, Wd, bd, same_stream=True)
+    assert torch.equal(xs1[-1], xs[-1]), "one-stream run differs from overlapped run"
+
+
+@pytest.mark.parametrize("name", ["vig_ti", "pyr_s2"])
+def test_standard_schedule_teacher_forced(name):
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = I.with_batch(I.WORKLOADS[name], 8)
+    x0 = I.make_features(w)
+    Wst, bst = _weights(w, w.L)
+    x0d, Wd, bd = to_dev(x0), to_dev(Wst), to_dev(bst)
+    xs, graphs = [x0d], []
+    for l in range(w.L):
+        keys = api.pool_keys(xs[l], w.H, w.W, w.pool_r) if w.pool_r > 1 else None
+        idx = api.knn_graph(xs[l], w.k, w.dilations[l], keys=keys)
+        graphs.append(idx)
+        xs.append(api.mrconv(xs[l], idx, Wd[l], bd[l], keys=keys))
+    torch.cuda.synchronize()
+    teacher_forced_checks(w, xs, graphs, Wst, bst, schedule="standard")
+    la = api.Lookahead()
+    out = la.stack(x0d, w.H, w.W, Wd, bd, list(w.dilations), w.k, w.pool_r,
+                   schedule=api.GL_SCHED_STANDARD)
+    torch.cuda.synchronize()
+    la.close()
+    assert torch.equal(out, xs[-1])
+
+
+def test_identity_weights_schedules_agree():
+    """W = [I | 0], b = 0 keeps every block's features equal to X^0, so the
+    lookahead and standard schedules give X^0 back bit for bit."""
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = I.with_batch(I.WORKLOADS["vig_ti"], 4)
+    x0d = to_dev(I.make_features(w))
+    eye = np.hstack([np.eye(w.C), np.zeros((w.C, w.C))])
+    Wd = to_dev(I.store(np.stack([eye] * w.L), w.dtype))
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    a = la.stack(x0d, w.H, w.W, Wd, None, list(w.dilations), w.k)
+    b = la.stack(x0d, w.H, w.W, Wd, None, list(w.dilations), w.k, schedule=api.GL_SCHED_STANDARD)
+    torch.cuda.synchronize()
+    la.close()
+    assert torch.equal(a, x0d) and torch.equal(b, x0d)
+
+
+def test_profiling_records_builds():
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = I.with_batch(I.WORKLOADS["vig_ti"], 4)
+    x0 = I.make_features(w)
+    Wst, bst = _weights(w, w.L)
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    la.set_profiling(64)
+    la.stack(to_dev(x0), w.H, w.W, to_dev(Wst), to_dev(bst), list(w.dilations), w.k)
+    torch.cuda.synchronize()
+    times = la.kernel_times_ms(api.GL_TIME_BUILD)
+    upd = la.kernel_times_ms(api.GL_TIME_UPDATE)
+    la.close()
+    assert len(times) == w.L - 1          # bootstrap + L-2 lookahead builds (d_1 == d_0)
+    assert len(upd) == w.L
+    assert all(t > 0 for t in times) and all(t > 0 for t in upd)
