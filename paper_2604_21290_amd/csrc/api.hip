@@ -60,6 +60,8 @@ gl_status check_knn(const void* x, int B, int N, int C, const void* keys, int M,
   if (k < 1 || dil < 1 || (long long)k * dil > M || (long long)k * dil > GL_MAX_KD)
     return fail(GL_ERR_BAD_K, "knn: need 1<=k, 1<=dilation, k*dilation <= min(M=%d, %d); got k=%d d=%d",
                 M, GL_MAX_KD, k, dil);
+  if (gl::knn_smem_bytes(C, dt == GL_BF16) > 160 * 1024)
+    return fail(GL_ERR_UNSUPPORTED, "knn: C=%d too wide for the LDS query tile", C);
   if (!aligned(x, 16) || (keys && !aligned(keys, 16)) || !aligned(idx_out, 4))
     return fail(GL_ERR_ALIGNMENT, "knn: x/keys need 16-byte, idx_out 4-byte alignment");
   const size_t ib = (size_t)B * N * k * 4, xb = (size_t)B * N * C * esize(dt),
@@ -145,29 +147,26 @@ void free_profiling(gl_lookahead_t h) {
   h->prof_max = 0;
 }
 
-// Bracket one launch with profiling events when enabled (which: 0 build, 1 update).
+// One launch, stamped with a pair of profiling events when enabled
+// (which: 0 build, 1 update).  The events are recorded by the dispatch itself.
 template <class Launch>
-gl_status timed_launch(gl_lookahead_t h, int which, hipStream_t s, const char* what,
-                       Launch&& launch) {
-  hipError_t e;
+gl_status timed_launch(gl_lookahead_t h, int which, const char* what, Launch&& launch) {
   const int i = h->prof_n[which];
   const bool prof = i < h->prof_max;
-  if (prof && (e = hipEventRecord(h->prof[which][i].first, s)) != hipSuccess)
-    return hip_fail(e, "hipEventRecord");
-  if ((e = launch()) != hipSuccess) return hip_fail(e, what);
-  if (prof) {
-    if ((e = hipEventRecord(h->prof[which][i].second, s)) != hipSuccess)
-      return hip_fail(e, "hipEventRecord");
-    h->prof_n[which] = i + 1;
-  }
+  hipEvent_t e0 = prof ? h->prof[which][i].first : nullptr;
+  hipEvent_t e1 = prof ? h->prof[which][i].second : nullptr;
+  hipError_t e = launch(e0, e1);
+  if (e != hipSuccess) return hip_fail(e, what);
+  if (prof) h->prof_n[which] = i + 1;
   return GL_OK;
 }
 
 // kNN build on the build stream.
 gl_status enqueue_build(gl_lookahead_t h, const void* x, int B, int N, int C, const void* keys,
                         int M, int k, int dil, gl_dtype dt, int32_t* idx) {
-  return timed_launch(h, GL_TIME_BUILD, h->sb, "knn launch", [&] {
-    return gl::launch_knn(x, keys ? keys : x, B, N, C, M, k, dil, dt == GL_BF16, idx, h->sb);
+  return timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
+    return gl::launch_knn(x, keys ? keys : x, B, N, C, M, k, dil, dt == GL_BF16, idx, h->sb, e0,
+                          e1);
   });
 }
 
@@ -259,9 +258,9 @@ gl_status enqueue_block(gl_lookahead_t h, const BlockArgs& a, int rt, bool do_po
       return s;
     if ((s = mark_built(h)) != GL_OK) return s;
   }
-  return timed_launch(h, GL_TIME_UPDATE, h->su, "mrconv launch", [&] {
+  return timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {
     return gl::launch_mrconv(a.x_in, keys, a.idx_use, a.Wt, a.bias, a.x_out, a.B, N, M, a.C, a.C,
-                             a.k, a.dt == GL_BF16, rt, h->su);
+                             a.k, a.dt == GL_BF16, rt, h->su, e0, e1);
   });
 }
 

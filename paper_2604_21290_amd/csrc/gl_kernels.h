@@ -2,23 +2,72 @@
 // by the C ABI layer before any of these is called).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
 namespace gl {
 
+struct KnnArgs {
+  const void* x;      // [B, N, C] queries
+  const void* keys;   // [B, M, C] keys (== x when unpooled)
+  int32_t* idx;       // [B, N, k]
+  int B, N, C, M, k, dil, KK, ib;
+  float qscale;       // 2^(30 - ib): fixed-point scale of the packed distance
+  uint32_t qmax;      // largest packed distance of a real key
+};
+
+struct MrArgs {
+  const void* x;      // [B*N, C]
+  const void* keys;   // [B, M, C]
+  const int32_t* idx; // [B*N, k]
+  const void* W;      // [Cout, 2C]
+  const void* bias;   // [Cout] or null
+  void* out;          // [B*N, Cout]
+  int R, N, M, C, Cout, k;
+};
+
+// Workgroups are dispatched round-robin over the 8 XCDs (workgroup id mod 8).
+// Map dispatch ids so that consecutive logical ids (neighbouring tiles of the
+// same image, which share key rows) land on the same XCD and its L2.
+__device__ __forceinline__ int xcd_remap(int L, int nb) {
+  const int q = nb >> 3, r = nb & 7;
+  const int xcd = L & 7, slot = L >> 3;
+  return xcd < r ? xcd * (q + 1) + slot : r * (q + 1) + (xcd - r) * q + slot;
+}
+
+// Launch fn(args) with `smem` bytes of dynamic LDS.  When ev0/ev1 are given the
+// launch itself stamps them (start and end of this dispatch).
+template <class A>
+hipError_t launch_with_smem(const void* fn, dim3 grid, dim3 block, size_t smem, hipStream_t s,
+                            hipEvent_t ev0, hipEvent_t ev1, const A& args) {
+  if (smem > 65536) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+  }
+  void* argv[] = {const_cast<A*>(&args)};
+  if (ev0 || ev1) return hipExtLaunchKernel(fn, grid, block, argv, smem, s, ev0, ev1, 0);
+  return hipLaunchKernel(fn, grid, block, argv, smem, s);
+}
+
+size_t knn_smem_bytes(int C, int dt_bf16);
+int knn_list_regs(int KK);
+KnnArgs make_knn_args(const void* x, const void* keys, int B, int N, int C, int M, int k, int dil,
+                      int32_t* idx);
 hipError_t launch_knn(const void* x, const void* keys, int B, int N, int C, int M, int k,
-                      int dil, int dt_bf16, int32_t* idx_out, hipStream_t stream);
+                      int dil, int dt_bf16, int32_t* idx_out, hipStream_t stream,
+                      hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 int mrconv_lds_row_bytes(int C, int dt_bf16);
-// Largest row-tile count (1, 2 or 4 tiles of 16 nodes) whose LDS need fits
-// lds_limit bytes; 0 if none does.
+size_t mrconv_smem_bytes(int C, int k, int dt_bf16, int rt);
+// Row tiles of 16 nodes per workgroup (2 or 1) whose LDS need fits lds_limit; 0 if none.
 int mrconv_row_tiles(int C, int k, int dt_bf16, size_t lds_limit);
-
+int mrconv_k_bucket(int k);
 hipError_t launch_mrconv(const void* x, const void* keys, const int32_t* idx, const void* W,
                          const void* bias, void* out, int B, int N, int M, int C, int Cout, int k,
-                         int dt_bf16, int rt, hipStream_t stream);
+                         int dt_bf16, int rt, hipStream_t stream, hipEvent_t ev0 = nullptr,
+                         hipEvent_t ev1 = nullptr);
 
 hipError_t launch_pool(const void* x, void* keys, int B, int H, int W, int C, int r, int dt_bf16,
                        hipStream_t stream);

@@ -1,25 +1,29 @@
 // Fused max-relative graph convolution for gfx950 (Sec. II-A Eq. 2-3; the
-// W_x / W_m split of Sec. IV-C2).
+// W_x / W_m split of Sec. IV-C2), and r x r key pooling for pyramid stages.
 //
-// One workgroup = 4 waves = TM = 16*RT consecutive nodes of the flattened
-// [B*N] node axis.
-//   1. gather: for each node and each 16-byte channel vector, the k neighbour
-//      key rows are read (consecutive lanes read consecutive vectors of the
-//      same row, so every neighbour row is one coalesced burst), their
-//      elementwise maximum is taken (exact in the storage type), x_i is
-//      subtracted in fp32 and the result rounded once.  [x_i | m_i] is
-//      written straight into the LDS A-tile; no edge tensor and no [B,N,2C]
-//      concatenation is ever written to memory.
+// One MRConv workgroup = 4 waves = TM = 16*RT consecutive nodes of the
+// flattened [B*N] node axis.
+//   1. gather: for each node and each 16-byte channel vector, the neighbour
+//      key rows are read with all loads of the vector in flight at once
+//      (the neighbour loop is unrolled to a compile-time bucket KB >= k; the
+//      slots past k repeat the first neighbour, which leaves the maximum
+//      unchanged).  Consecutive lanes read consecutive vectors of the same
+//      row, so every neighbour row is one coalesced burst.  The maximum is
+//      exact in the storage type; x_i is subtracted in fp32 and the result
+//      rounded once.  [x_i | m_i] goes straight into the LDS A-tile: no edge
+//      tensor and no [B,N,2C] concatenation is ever written to memory.
 //   2. FC on MFMA: out[TM, Cout] = A[TM, 2C] W^T + b.  The contraction runs
-//      over the concatenated axis, so columns 0..C-1 of W meet x_i and
-//      columns C..2C-1 meet m_i in one accumulation.  Each wave owns every
-//      4th 16-column output tile; W rows are read from L2 as MFMA B operands.
+//      over the concatenated axis, so columns 0..C-1 of W meet x_i and columns
+//      C..2C-1 meet m_i in one accumulation.  Each wave owns every 4th
+//      16-column output tile; W rows stream from L2 as MFMA B operands, a
+//      batch of k-steps at a time.
 #include "gl_device.h"
 #include "gl_kernels.h"
 
 namespace gl {
 
 constexpr int kMrThreads = 256;
+constexpr int kMrKU = 2;  // k-steps of W operands loaded as one batch
 
 template <int DT>
 __device__ __forceinline__ void load_vec(const char* p, float* f) {
@@ -37,116 +41,141 @@ __device__ __forceinline__ void store_vec(char* p, const float* f) {
   else *reinterpret_cast<float4*>(p) = make_float4(f[0], f[1], f[2], f[3]);
 }
 
-template <int DT, int RT>
-__global__ __launch_bounds__(kMrThreads) void mrconv_kernel(
-    const void* __restrict__ x, const void* __restrict__ keys, const int32_t* __restrict__ idx,
-    const void* __restrict__ W, const void* __restrict__ bias, void* __restrict__ out, int R,
-    int N, int M, int C, int Cout, int k, int lds_row) {
-  extern __shared__ __align__(16) char smem[];
+int mrconv_lds_row_bytes(int C, int dt_bf16) { return 2 * C * (dt_bf16 ? 2 : 4) + 16; }
+
+size_t mrconv_smem_bytes(int C, int k, int dt_bf16, int rt) {
+  return (size_t)16 * rt * (mrconv_lds_row_bytes(C, dt_bf16) + 4 * k);
+}
+
+int mrconv_row_tiles(int C, int k, int dt_bf16, size_t lds_limit) {
+  // two row tiles (32 nodes) per workgroup unless the LDS tile does not fit
+  for (int rt = 2; rt >= 1; rt >>= 1)
+    if (mrconv_smem_bytes(C, k, dt_bf16, rt) <= lds_limit) return rt;
+  return 0;
+}
+
+int mrconv_k_bucket(int k) { return k <= 9 ? 9 : k <= 16 ? 16 : k <= 32 ? 32 : 64; }
+
+// TM = 16*RT nodes starting at flattened node row0.  smem holds
+// mrconv_smem_bytes(C, k, RT) bytes.  Called by all 256 threads.
+template <int DT, int RT, int KB>
+__device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row0) {
   constexpr int TM = 16 * RT;
   constexpr int ES = DT ? 2 : 4;
   constexpr int VEC = 16 / ES;
+  const int C = a.C, k = a.k, M = a.M, N = a.N, R = a.R, Cout = a.Cout;
+  const int lds_row = 2 * C * ES + 16;
   char* sA = smem;
   int32_t* sIdx = reinterpret_cast<int32_t*>(smem + TM * lds_row);
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, t = lane & 15;
-  const int row0 = blockIdx.x * TM;
   const int CG = C / VEC;
 
-  // -- neighbour lists of the tile -------------------------------------------
+  // -- neighbour lists of the tile ---------------------------------------------
   for (int e = tid; e < TM * k; e += kMrThreads) {
     const int r = e / k, tt = e - r * k, row = row0 + r;
-    const int j = row < R ? idx[(size_t)row * k + tt] : 0;
+    const int j = row < R ? a.idx[(size_t)row * k + tt] : 0;
     sIdx[e] = min(max(j, 0), M - 1);
   }
   __syncthreads();
 
   // -- gather-max into the LDS A-tile ------------------------------------------
   for (int e = tid; e < TM * CG; e += kMrThreads) {
-    const int r = e / CG, cg = e - r * CG, row = row0 + r;
-    char* dst = sA + r * lds_row + cg * 16;
+    const int r = e / CG, cg = e - r * CG;
+    const int row = min(row0 + r, R - 1);
+    const int b = row / N;
+    const char* xrow = static_cast<const char*>(a.x) + ((size_t)row * C + cg * VEC) * ES;
+    const char* kbase = static_cast<const char*>(a.keys) + ((size_t)b * M * C + cg * VEC) * ES;
+    const int32_t* nb = sIdx + r * k;
+    const uint4 xraw = *reinterpret_cast<const uint4*>(xrow);
     float xf[VEC], mx[VEC];
-    if (row < R) {
-      const int b = row / N;
-      load_vec<DT>(static_cast<const char*>(x) + ((size_t)row * C + cg * VEC) * ES, xf);
-      const char* kbase = static_cast<const char*>(keys) + ((size_t)b * M * C + cg * VEC) * ES;
+    if (DT) unpack_bf16x8(xraw, xf);
+    else { const float4 v = __builtin_bit_cast(float4, xraw); xf[0] = v.x; xf[1] = v.y; xf[2] = v.z; xf[3] = v.w; }
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) mx[i] = -INFINITY;
-      const int32_t* nb = sIdx + r * k;
-      for (int tt = 0; tt < k; ++tt) {
+    for (int i = 0; i < VEC; ++i) mx[i] = -INFINITY;
+    constexpr int KG = KB < 16 ? KB : 16;  // neighbour loads in flight per group
+#pragma unroll 1
+    for (int t0 = 0; t0 < KB; t0 += KG) {
+      uint4 raw[KG];
+#pragma unroll
+      for (int u = 0; u < KG; ++u) {
+        const int tt = t0 + u;
+        const int j = nb[tt < k ? tt : 0];
+        raw[u] = *reinterpret_cast<const uint4*>(kbase + (size_t)j * C * ES);
+      }
+#pragma unroll
+      for (int u = 0; u < KG; ++u) {
         float kf[VEC];
-        load_vec<DT>(kbase + (size_t)nb[tt] * C * ES, kf);
+        if (DT) unpack_bf16x8(raw[u], kf);
+        else { const float4 v = __builtin_bit_cast(float4, raw[u]); kf[0] = v.x; kf[1] = v.y; kf[2] = v.z; kf[3] = v.w; }
 #pragma unroll
         for (int i = 0; i < VEC; ++i) mx[i] = fmaxf(mx[i], kf[i]);
       }
-#pragma unroll
-      for (int i = 0; i < VEC; ++i) mx[i] -= xf[i];
-    } else {
-#pragma unroll
-      for (int i = 0; i < VEC; ++i) xf[i] = mx[i] = 0.f;
     }
-    store_vec<DT>(dst, xf);
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) mx[i] -= xf[i];
+    char* dst = sA + r * lds_row + cg * 16;
+    *reinterpret_cast<uint4*>(dst) = xraw;
     store_vec<DT>(dst + C * ES, mx);
   }
   __syncthreads();
 
-  // -- FC on MFMA ---------------------------------------------------------------
+  // -- FC on MFMA -----------------------------------------------------------------
   const int K2 = 2 * C;
+  const int KSTEP = DT ? 32 : 16;
+  const int ksteps = (K2 + KSTEP - 1) / KSTEP;
   const int NCT = (Cout + 15) >> 4;
-  const char* Wb = static_cast<const char*>(W);
-  for (int p = 0; 4 * (4 * p) + w < NCT; ++p) {
+  const char* Wb = static_cast<const char*>(a.W);
+  for (int p = 0; w + 16 * p < NCT; ++p) {
     f32x4 acc[RT][4];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int c4 = 0; c4 < 4; ++c4) acc[rt][c4] = f32x4{0.f, 0.f, 0.f, 0.f};
-    int nrow[4];
+    const char* wrow[4];
     bool nvalid[4];
 #pragma unroll
     for (int c4 = 0; c4 < 4; ++c4) {
-      const int ct = w + 4 * (4 * p + c4);
-      nrow[c4] = ct * 16 + t;
-      nvalid[c4] = ct < NCT && nrow[c4] < Cout;
+      const int n = (w + 4 * (4 * p + c4)) * 16 + t;
+      nvalid[c4] = n < Cout;
+      wrow[c4] = Wb + (size_t)min(n, Cout - 1) * K2 * ES;
     }
-    if (DT) {
-      for (int s = 0; s < (K2 + 31) / 32; ++s) {
-        const int kk = s * 32 + g * 8;
-        const bool kin = kk < K2;
-        uint4 a[RT];
+    for (int s0 = 0; s0 < ksteps; s0 += kMrKU) {
+      uint4 bw[kMrKU][4];
+      bool kin[kMrKU];
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-          a[rt] = kin ? *reinterpret_cast<const uint4*>(sA + (rt * 16 + t) * lds_row + kk * 2)
-                      : make_uint4(0, 0, 0, 0);
+      for (int u = 0; u < kMrKU; ++u) {
+        const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
+        kin[u] = kk < K2;
+        const int kl = kin[u] ? kk : 0;
 #pragma unroll
-        for (int c4 = 0; c4 < 4; ++c4) {
-          const uint4 bw = (kin && nvalid[c4])
-                               ? *reinterpret_cast<const uint4*>(Wb + ((size_t)nrow[c4] * K2 + kk) * 2)
-                               : make_uint4(0, 0, 0, 0);
-#pragma unroll
-          for (int rt = 0; rt < RT; ++rt) acc[rt][c4] = mfma_bf16(a[rt], bw, acc[rt][c4]);
-        }
+        for (int c4 = 0; c4 < 4; ++c4)
+          bw[u][c4] = *reinterpret_cast<const uint4*>(wrow[c4] + (size_t)kl * ES);
       }
-    } else {
-      for (int s = 0; s < (K2 + 15) / 16; ++s) {
-        const int kk = s * 16 + g * 4;
-        const bool kin = kk < K2;
-        float4 a[RT];
+#pragma unroll
+      for (int u = 0; u < kMrKU; ++u) {
+        const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
+        uint4 af[RT];
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
-          a[rt] = kin ? *reinterpret_cast<const float4*>(sA + (rt * 16 + t) * lds_row + kk * 4)
-                      : make_float4(0.f, 0.f, 0.f, 0.f);
+          af[rt] = kin[u] ? *reinterpret_cast<const uint4*>(sA + (rt * 16 + t) * lds_row + kk * ES)
+                          : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int c4 = 0; c4 < 4; ++c4) {
-          const float4 bw = (kin && nvalid[c4])
-                                ? *reinterpret_cast<const float4*>(Wb + ((size_t)nrow[c4] * K2 + kk) * 4)
-                                : make_float4(0.f, 0.f, 0.f, 0.f);
+          const uint4 bv = (kin[u] && nvalid[c4]) ? bw[u][c4] : make_uint4(0, 0, 0, 0);
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt) {
-            acc[rt][c4] = mfma_f32(a[rt].x, bw.x, acc[rt][c4]);
-            acc[rt][c4] = mfma_f32(a[rt].y, bw.y, acc[rt][c4]);
-            acc[rt][c4] = mfma_f32(a[rt].z, bw.z, acc[rt][c4]);
-            acc[rt][c4] = mfma_f32(a[rt].w, bw.w, acc[rt][c4]);
+            if (DT) {
+              acc[rt][c4] = mfma_bf16(af[rt], bv, acc[rt][c4]);
+            } else {
+              const float4 x4 = __builtin_bit_cast(float4, af[rt]);
+              const float4 w4 = __builtin_bit_cast(float4, bv);
+              acc[rt][c4] = mfma_f32(x4.x, w4.x, acc[rt][c4]);
+              acc[rt][c4] = mfma_f32(x4.y, w4.y, acc[rt][c4]);
+              acc[rt][c4] = mfma_f32(x4.z, w4.z, acc[rt][c4]);
+              acc[rt][c4] = mfma_f32(x4.w, w4.w, acc[rt][c4]);
+            }
           }
         }
       }
@@ -155,11 +184,11 @@ __global__ __launch_bounds__(kMrThreads) void mrconv_kernel(
 #pragma unroll
     for (int c4 = 0; c4 < 4; ++c4) {
       if (!nvalid[c4]) continue;
-      const int n = nrow[c4];
+      const int n = (w + 4 * (4 * p + c4)) * 16 + t;
       float bn = 0.f;
-      if (bias) {
-        bn = DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(bias)[n])
-                : static_cast<const float*>(bias)[n];
+      if (a.bias) {
+        bn = DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(a.bias)[n])
+                : static_cast<const float*>(a.bias)[n];
       }
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
@@ -168,54 +197,54 @@ __global__ __launch_bounds__(kMrThreads) void mrconv_kernel(
           const int row = row0 + rt * 16 + 4 * g + v;
           if (row >= R) continue;
           const float y = acc[rt][c4][v] + bn;
-          if (DT) static_cast<uint16_t*>(out)[(size_t)row * Cout + n] = (uint16_t)f32_to_bf16_bits(y);
-          else static_cast<float*>(out)[(size_t)row * Cout + n] = y;
+          if (DT) static_cast<uint16_t*>(a.out)[(size_t)row * Cout + n] = (uint16_t)f32_to_bf16_bits(y);
+          else static_cast<float*>(a.out)[(size_t)row * Cout + n] = y;
         }
       }
     }
   }
 }
 
-int mrconv_lds_row_bytes(int C, int dt_bf16) { return 2 * C * (dt_bf16 ? 2 : 4) + 16; }
+template <int DT, int RT, int KB>
+__global__ __launch_bounds__(kMrThreads) void mrconv_kernel(MrArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  const int blk = xcd_remap(blockIdx.x, gridDim.x);
+  mrconv_tile<DT, RT, KB>(smem, a, blk * 16 * RT);
+}
 
-int mrconv_row_tiles(int C, int k, int dt_bf16, size_t lds_limit) {
-  const int row = mrconv_lds_row_bytes(C, dt_bf16);
-  for (int rt = 4; rt >= 1; rt >>= 1) {
-    const size_t need = (size_t)16 * rt * (row + 4 * k);
-    if (need <= lds_limit) return rt;
+template <int DT, int RT>
+const void* mrconv_fn_kb(int KB) {
+  switch (KB) {
+    case 9: return (const void*)&mrconv_kernel<DT, RT, 9>;
+    case 16: return (const void*)&mrconv_kernel<DT, RT, 16>;
+    case 32: return (const void*)&mrconv_kernel<DT, RT, 32>;
+    default: return (const void*)&mrconv_kernel<DT, RT, 64>;
   }
-  return 0;
 }
 
 hipError_t launch_mrconv(const void* x, const void* keys, const int32_t* idx, const void* W,
                          const void* bias, void* out, int B, int N, int M, int C, int Cout, int k,
-                         int dt_bf16, int rt, hipStream_t stream) {
-  const int R = B * N;
-  const int lds_row = mrconv_lds_row_bytes(C, dt_bf16);
+                         int dt_bf16, int rt, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  MrArgs a;
+  a.x = x;
+  a.keys = keys;
+  a.idx = idx;
+  a.W = W;
+  a.bias = bias;
+  a.out = out;
+  a.R = B * N;
+  a.N = N;
+  a.M = M;
+  a.C = C;
+  a.Cout = Cout;
+  a.k = k;
   const int TM = 16 * rt;
-  const size_t lds = (size_t)TM * (lds_row + 4 * k);
-  dim3 grid((R + TM - 1) / TM), block(kMrThreads);
-#define GL_MR_LAUNCH(DT, RT)                                                                     \
-  do {                                                                                           \
-    if (lds > 65536) {                                                                           \
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&mrconv_kernel<DT, RT>),  \
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);  \
-      if (e != hipSuccess) return e;                                                             \
-    }                                                                                            \
-    hipLaunchKernelGGL((mrconv_kernel<DT, RT>), grid, block, lds, stream, x, keys, idx, W, bias, \
-                       out, R, N, M, C, Cout, k, lds_row);                                       \
-  } while (0)
-  if (dt_bf16) {
-    if (rt == 4) GL_MR_LAUNCH(1, 4);
-    else if (rt == 2) GL_MR_LAUNCH(1, 2);
-    else GL_MR_LAUNCH(1, 1);
-  } else {
-    if (rt == 4) GL_MR_LAUNCH(0, 4);
-    else if (rt == 2) GL_MR_LAUNCH(0, 2);
-    else GL_MR_LAUNCH(0, 1);
-  }
-#undef GL_MR_LAUNCH
-  return hipGetLastError();
+  const size_t smem = mrconv_smem_bytes(C, k, dt_bf16, rt);
+  const dim3 grid((a.R + TM - 1) / TM), block(kMrThreads);
+  const int KB = mrconv_k_bucket(k);
+  const void* fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2>(KB) : mrconv_fn_kb<1, 1>(KB))
+                           : (rt == 2 ? mrconv_fn_kb<0, 2>(KB) : mrconv_fn_kb<0, 1>(KB));
+  return launch_with_smem(fn, grid, block, smem, stream, ev0, ev1, a);
 }
 
 // ---------------------------------------------------------------------------
