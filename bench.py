@@ -2,9 +2,11 @@
 """Benchmark the GraphLeap graph-convolution hot path on one MI355X.
 
 A step is one pass of the whole hot path over one batch: an L-block GraphLeap
-stack (bootstrap kNN build, then per block the kNN build of the next graph on
-the build stream overlapped with the MRConv update on the update stream),
-enqueued natively by gl_graphleap_stack.  Default workload: ViG-Ti shaped,
+stack (bootstrap kNN build, then per block the kNN build of the next graph
+running concurrently with the MRConv update of this block), enqueued natively
+by gl_graphleap_stack.  The default schedule puts both in one launch per block
+(GL_SCHED_LOOKAHEAD_FUSED); the two-stream lookahead and the standard serial
+ViG schedule run the same kernels and are timed beside it for context.  Default workload: ViG-Ti shaped,
 12 blocks, B=32 images of 14x14 patches, C=192, k=9, dilation ceil(l/4),
 bf16 storage with fp32 accumulation, synthetic seeded inputs already in HBM.
 
@@ -113,7 +115,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="vig_ti")
-    ap.add_argument("--schedule", default="lookahead", choices=["lookahead", "standard"])
+    ap.add_argument("--schedule", default="fused", choices=["fused", "lookahead", "standard"])
     ap.add_argument("--only", default=None, choices=["stack", "knn", "mrconv", "copy"])
     ap.add_argument("--cpu-images", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -135,7 +137,9 @@ def main() -> int:
     api.lib()
     w = I.WORKLOADS[args.workload]
     es = 2 if w.dtype == I.BF16 else 4
-    sched = api.GL_SCHED_LOOKAHEAD if args.schedule == "lookahead" else api.GL_SCHED_STANDARD
+    SCHED = {"fused": api.GL_SCHED_LOOKAHEAD_FUSED, "lookahead": api.GL_SCHED_LOOKAHEAD,
+             "standard": api.GL_SCHED_STANDARD}
+    sched = SCHED[args.schedule]
 
     def dev(s):
         import numpy as np
@@ -180,30 +184,45 @@ def main() -> int:
         log(f"mrconv x {args.steps}")
         return 0
 
-    def step():
-        la.stack(x0, w.H, w.W, Wd, bd, dil, w.k, w.pool_r, schedule=sched, ws=ws, x_out=out)
+    def step(sc=None):
+        la.stack(x0, w.H, w.W, Wd, bd, dil, w.k, w.pool_r, schedule=sched if sc is None else sc,
+                 ws=ws, x_out=out)
+
+    def time_steps(n, sc=None):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(s_up)
+        for _ in range(n):
+            step(sc)
+        e1.record(s_up)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
 
     log(f"workload {args.workload}: warmup {args.warmup}")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    log(f"timing {args.steps} steps")
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps ({args.schedule})")
     t_wall = time.perf_counter()
-    e0.record(s_up)
-    for _ in range(args.steps):
-        step()
-    e1.record(s_up)
-    torch.cuda.synchronize()
+    ms_per_step = time_steps(args.steps)
     wall = time.perf_counter() - t_wall
-    ms = e0.elapsed_time(e1)
-    ms_per_step = ms / args.steps
-    value = w.L * args.steps / (ms / 1e3)
+    value = w.L / (ms_per_step / 1e3)
     log(f"{ms_per_step:.4f} ms/step, {value:.1f} layers/s (wall {wall:.3f} s)")
 
-    # per-kernel durations: the same steps again, each kNN build and each MRConv
-    # update bracketed by HIP events on its own stream
+    # the other schedules, same kernels, for context
+    schedules = {args.schedule: {"ms_per_step": ms_per_step, "layers_per_s": value}}
+    if args.only != "stack":
+        for name, sc in SCHED.items():
+            if name == args.schedule:
+                continue
+            for _ in range(max(2, args.warmup // 4)):
+                step(sc)
+            m = time_steps(max(10, args.steps // 4), sc)
+            schedules[name] = {"ms_per_step": m, "layers_per_s": w.L / (m / 1e3)}
+        log("schedules", json.dumps(schedules))
+
+    # per-kernel durations: the same steps again, every launch stamped with a
+    # start and an end HIP event by its own dispatch, on its own stream
     if args.only == "stack":
         return 0
     n_rec = args.steps * w.L + 8
@@ -213,6 +232,7 @@ def main() -> int:
     torch.cuda.synchronize()
     tb = la.kernel_times_ms(api.GL_TIME_BUILD, n_rec)
     tu = la.kernel_times_ms(api.GL_TIME_UPDATE, n_rec)
+    tf = la.kernel_times_ms(api.GL_TIME_FUSED, n_rec)
     la.set_profiling(0)
     knn_flops, knn_bytes, mr_flops, mr_bytes = algorithmic(w, es)
     peak = PEAK_TFLOPS[w.dtype]
@@ -230,20 +250,43 @@ def main() -> int:
             "fc_tflops": mr_flops / t / 1e12, "fc_mfma_frac": mr_flops / t / 1e12 / peak,
             "hbm_gbs": mr_bytes / t / 1e9, "hbm_frac": mr_bytes / t / 1e9 / PEAK_HBM_GBS,
             "gather_effective_gbs": (w.B * w.N * w.k * w.C * es) / t / 1e9}
-    tot_b = sum(tb) / args.steps if tb else 0.0
-    tot_u = sum(tu) / args.steps if tu else 0.0
-    if tot_b >= tot_u and tb:
+    # one-launch block: X read once by both roles, the used graph read, the next
+    # graph written, W read, X^(l+1) written
+    fb_flops = knn_flops + mr_flops
+    fb_bytes = mr_bytes + w.B * w.N * w.k * 4
+    if tf:
+        t = sum(tf) / len(tf) * 1e-3
+        kernels["graphleap_block"] = {
+            "launches_per_step": len(tf) / args.steps, "avg_us": t * 1e6,
+            "tflops": fb_flops / t / 1e12, "mfma_frac": fb_flops / t / 1e12 / peak,
+            "hbm_gbs": fb_bytes / t / 1e9, "hbm_frac": fb_bytes / t / 1e9 / PEAK_HBM_GBS}
+    totals = {"knn_graph": sum(tb), "mrconv": sum(tu), "graphleap_block": sum(tf)}
+    dom = max(totals, key=totals.get)
+    if dom == "knn_graph":
         t = sum(tb) / len(tb) * 1e-3
         roof = {"kernel": "knn_graph", "bound": "mfma", "achieved": knn_flops / t / 1e12,
                 "peak": peak, "unit": "TFLOP/s", "frac": knn_flops / t / 1e12 / peak,
                 "traffic": load_traffic("knn_graph", args.workload),
-                "per_launch": f"2*B*N*M*C = {knn_flops:.4g} flop"}
-    else:
+                "per_launch": f"Gram 2*B*N*M*C = {knn_flops:.4g} flop"}
+    elif dom == "mrconv":
         t = sum(tu) / len(tu) * 1e-3
         roof = {"kernel": "mrconv", "bound": "hbm", "achieved": mr_bytes / t / 1e9,
                 "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": mr_bytes / t / 1e9 / PEAK_HBM_GBS,
                 "traffic": load_traffic("mrconv", args.workload),
                 "per_launch": f"{mr_bytes:.4g} bytes"}
+    else:
+        t = sum(tf) / len(tf) * 1e-3
+        if fb_bytes / (PEAK_HBM_GBS * 1e9) >= fb_flops / (peak * 1e12):
+            roof = {"kernel": "graphleap_block", "bound": "hbm", "achieved": fb_bytes / t / 1e9,
+                    "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": fb_bytes / t / 1e9 / PEAK_HBM_GBS,
+                    "traffic": load_traffic("graphleap_block", args.workload),
+                    "per_launch": f"{fb_bytes:.4g} bytes (flop floor {fb_flops:.4g})"}
+        else:
+            roof = {"kernel": "graphleap_block", "bound": "mfma", "achieved": fb_flops / t / 1e12,
+                    "peak": peak, "unit": "TFLOP/s", "frac": fb_flops / t / 1e12 / peak,
+                    "traffic": load_traffic("graphleap_block", args.workload),
+                    "per_launch": f"{fb_flops:.4g} flop (byte floor {fb_bytes:.4g})"}
     log("kernels", json.dumps(kernels))
 
     cpu = None
@@ -259,7 +302,7 @@ def main() -> int:
         "config": {"workload": f"{args.workload}: {DESCR[args.workload]}", "B": w.B, "N": w.N,
                    "M": w.M, "C": w.C, "k": w.k, "blocks": w.L, "dilations": dil,
                    "schedule": args.schedule},
-        "roofline": roof, "cpu_baseline": cpu, "kernels": kernels,
+        "roofline": roof, "cpu_baseline": cpu, "kernels": kernels, "schedules": schedules,
         "image_layers_per_s": value * w.B, "source_sha": kernel_source_sha(),
     }
     print(json.dumps(line), flush=True)

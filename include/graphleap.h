@@ -65,8 +65,14 @@ typedef enum gl_status {
 } gl_status;
 
 typedef enum gl_schedule {
-  GL_SCHED_LOOKAHEAD = 0,  /* GraphLeap: block l uses G(X^(l-1)); build || update */
-  GL_SCHED_STANDARD = 1    /* standard ViG (Eq. 6): block l uses G(X^l); serial */
+  GL_SCHED_LOOKAHEAD = 0,        /* GraphLeap: block l uses G(X^(l-1)); the build of the
+                                    next graph runs on the build stream while the update
+                                    runs on the update stream */
+  GL_SCHED_STANDARD = 1,         /* standard ViG (Eq. 6): block l uses G(X^l); build then
+                                    update, serial, on the update stream */
+  GL_SCHED_LOOKAHEAD_FUSED = 2   /* GraphLeap in one launch per block: the build tiles of
+                                    the next graph and the update tiles of this block share
+                                    one grid on the update stream (bit-identical results) */
 } gl_schedule;
 
 /* ---------------------------------------------------------------------------
@@ -137,15 +143,17 @@ typedef struct gl_lookahead* gl_lookahead_t;
 gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_lookahead_t* out);
 gl_status gl_lookahead_destroy(gl_lookahead_t h);
 
-/* Profiling: when enabled (max_records > 0), every kNN build and every
- * MRConv update enqueued through the handle is bracketed by a pair of HIP
- * events on the stream it runs on (at most max_records pairs of each kind
- * are kept; later launches are not timed).  gl_lookahead_kernel_times()
- * synchronises the recorded events of one kind (which = GL_TIME_BUILD or
- * GL_TIME_UPDATE), writes their durations in milliseconds (at most cap of
- * them) and clears that kind's records.  max_records == 0 disables it. */
+/* Profiling: when enabled (max_records > 0), every kNN build, MRConv update
+ * and one-launch block enqueued through the handle is stamped by its own
+ * dispatch with a start and an end HIP event (at most max_records pairs of
+ * each kind are kept; later launches are not timed).
+ * gl_lookahead_kernel_times() synchronises the recorded events of one kind
+ * (which = GL_TIME_BUILD, GL_TIME_UPDATE or GL_TIME_FUSED), writes their
+ * durations in milliseconds (at most cap of them) and clears that kind's
+ * records.  max_records == 0 disables it. */
 #define GL_TIME_BUILD 0
 #define GL_TIME_UPDATE 1
+#define GL_TIME_FUSED 2   /* one-launch blocks of GL_SCHED_LOOKAHEAD_FUSED */
 gl_status gl_lookahead_set_profiling(gl_lookahead_t h, int max_records);
 gl_status gl_lookahead_kernel_times(gl_lookahead_t h, int which, float* ms_out, int cap,
                                     int* n_out);
@@ -199,6 +207,10 @@ gl_status gl_graphleap_block(gl_lookahead_t h, const void* x_in, int B, int H, i
  *     updates.  L - 1 builds when d_1 == d_0; G(X^(L-1)) is never built.
  *   schedule GL_SCHED_STANDARD: Ghat^l = G(X^l, d_l), build then update,
  *     all on the update stream (Eq. 5-7 with U = X).
+ *   schedule GL_SCHED_LOOKAHEAD_FUSED: the lookahead graphs as above, but each
+ *     block is one launch on the update stream whose grid holds both the
+ *     build tiles of Ghat^(l+1) and the update tiles of X^(l+1); the results
+ *     are bit-identical to GL_SCHED_LOOKAHEAD.
  *
  *   x0 [B, N, C] input, N = H*W.  Ws [L, C, 2C]; bs [L, C] or NULL.
  *   dilations: host array of L ints (the dilation of the block that uses

@@ -19,8 +19,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgraphleap.so")
 
 GL_F32, GL_BF16 = 0, 1
-GL_SCHED_LOOKAHEAD, GL_SCHED_STANDARD = 0, 1
-GL_TIME_BUILD, GL_TIME_UPDATE = 0, 1
+GL_SCHED_LOOKAHEAD, GL_SCHED_STANDARD, GL_SCHED_LOOKAHEAD_FUSED = 0, 1, 2
+GL_TIME_BUILD, GL_TIME_UPDATE, GL_TIME_FUSED = 0, 1, 2
 GL_MAX_KD, GL_MAX_M, GL_MAX_K = 64, 4096, 64
 
 STATUS = {0: "GL_OK", 1: "GL_ERR_NULL_PTR", 2: "GL_ERR_BAD_SHAPE", 3: "GL_ERR_BAD_K",
@@ -172,7 +172,8 @@ class Lookahead:
         _call("gl_lookahead_set_profiling", self._h, max_records)
 
     def kernel_times_ms(self, which: int = GL_TIME_BUILD, cap: int = 1 << 16) -> list:
-        """Durations (ms) of the profiled builds (GL_TIME_BUILD) or updates."""
+        """Durations (ms) of the profiled builds (GL_TIME_BUILD), updates
+        (GL_TIME_UPDATE) or one-launch blocks (GL_TIME_FUSED)."""
         buf = (ctypes.c_float * cap)()
         n = ctypes.c_int()
         _call("gl_lookahead_kernel_times", self._h, which, buf, cap, ctypes.byref(n))

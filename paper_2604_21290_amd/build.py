@@ -4,6 +4,7 @@
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import glob
 import os
 import subprocess
@@ -29,20 +30,44 @@ def sources() -> list:
     return sorted(glob.glob(os.path.join(PKG, "csrc", "*.hip")))
 
 
-def build_library(verbose: bool = True) -> str:
-    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB + ".tmp"
-    cmd = [hipcc, *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"),
-           "-I", os.path.join(PKG, "csrc"), *sources(), "-o", tmp]
-    if verbose:
-        print("[build]", " ".join(cmd), flush=True)
+NOISE = "is not a recognized feature for this target"
+
+
+def _run(cmd):
     res = subprocess.run(cmd, capture_output=True, text=True)
-    noise = "is not a recognized feature for this target"
-    err = "\n".join(l for l in res.stderr.splitlines() if noise not in l)
-    if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
-    if verbose and err.strip():
-        print(err, file=sys.stderr)
+    err = "\n".join(l for l in res.stderr.splitlines() if NOISE not in l)
+    return res.returncode, err
+
+
+def build_library(verbose: bool = True, jobs: int | None = None) -> str:
+    """Compile each source to an object in parallel, then link the library."""
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    objdir = os.path.join(ROOT, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc")]
+    flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+    jobs = jobs or min(8, os.cpu_count() or 1)
+    cmds = []
+    for src in sources():
+        obj = os.path.join(objdir, os.path.basename(src) + ".o")
+        cmds.append(([hipcc, *flags, *inc, "-c", src, "-o", obj], obj))
+    if verbose:
+        for c, _ in cmds:
+            print("[build]", " ".join(c), flush=True)
+    with cf.ThreadPoolExecutor(jobs) as ex:
+        results = list(ex.map(lambda c: _run(c[0]), cmds))
+    for (cmd, _), (rc, err) in zip(cmds, results):
+        if rc != 0:
+            raise RuntimeError(f"hipcc failed ({rc}) on {cmd[-3]}:\n{err}")
+        if verbose and err.strip():
+            print(err, file=sys.stderr)
+    tmp = LIB + ".tmp"
+    link = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *[o for _, o in cmds], "-o", tmp]
+    if verbose:
+        print("[build]", " ".join(link), flush=True)
+    rc, err = _run(link)
+    if rc != 0:
+        raise RuntimeError(f"link failed ({rc}):\n{err}")
     os.replace(tmp, LIB)
     return LIB
 

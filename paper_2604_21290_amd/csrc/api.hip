@@ -127,8 +127,8 @@ struct gl_lookahead {
   hipEvent_t ev_ready, ev_built;
   bool pending;
   int prof_max;
-  int prof_n[2];                                           // builds, updates
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> prof[2];
+  int prof_n[3];                                           // builds, updates, fused
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> prof[3];
 };
 
 namespace {
@@ -136,7 +136,7 @@ namespace {
 bool handle_ok(gl_lookahead_t h) { return h && h->magic == kHandleMagic; }
 
 void free_profiling(gl_lookahead_t h) {
-  for (int w = 0; w < 2; ++w) {
+  for (int w = 0; w < 3; ++w) {
     for (auto& p : h->prof[w]) {
       (void)hipEventDestroy(p.first);
       (void)hipEventDestroy(p.second);
@@ -324,7 +324,7 @@ gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_look
   h->sb = s_build;
   h->pending = false;
   h->prof_max = 0;
-  h->prof_n[0] = h->prof_n[1] = 0;
+  h->prof_n[0] = h->prof_n[1] = h->prof_n[2] = 0;
   hipError_t e = hipEventCreateWithFlags(&h->ev_ready, hipEventDisableTiming);
   if (e != hipSuccess) {
     delete h;
@@ -355,7 +355,7 @@ gl_status gl_lookahead_set_profiling(gl_lookahead_t h, int max_records) {
   if (max_records < 0 || max_records > 1 << 20)
     return fail(GL_ERR_BAD_SHAPE, "set_profiling: max_records=%d", max_records);
   free_profiling(h);
-  for (int w = 0; w < 2; ++w) {
+  for (int w = 0; w < 3; ++w) {
     for (int i = 0; i < max_records; ++i) {
       hipEvent_t a, b;
       hipError_t e = hipEventCreate(&a);
@@ -378,7 +378,7 @@ gl_status gl_lookahead_set_profiling(gl_lookahead_t h, int max_records) {
 gl_status gl_lookahead_kernel_times(gl_lookahead_t h, int which, float* ms_out, int cap,
                                     int* n_out) {
   if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "kernel_times: bad handle");
-  if (which != GL_TIME_BUILD && which != GL_TIME_UPDATE)
+  if (which != GL_TIME_BUILD && which != GL_TIME_UPDATE && which != GL_TIME_FUSED)
     return fail(GL_ERR_UNSUPPORTED, "kernel_times: which=%d", which);
   if (!n_out || (cap > 0 && !ms_out)) return fail(GL_ERR_NULL_PTR, "kernel_times: null output");
   const int n = h->prof_n[which] < cap ? h->prof_n[which] : cap;
@@ -440,7 +440,8 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
   if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "graphleap_stack: bad handle");
   if (!x0 || !dilations || !Ws || !x_ws || !idx_ws || !x_out)
     return fail(GL_ERR_NULL_PTR, "graphleap_stack: x0, dilations, Ws, x_ws, idx_ws, x_out required");
-  if (schedule != GL_SCHED_LOOKAHEAD && schedule != GL_SCHED_STANDARD)
+  if (schedule != GL_SCHED_LOOKAHEAD && schedule != GL_SCHED_STANDARD &&
+      schedule != GL_SCHED_LOOKAHEAD_FUSED)
     return fail(GL_ERR_UNSUPPORTED, "graphleap_stack: unknown schedule %d", (int)schedule);
   if (L < 1 || L > 4096) return fail(GL_ERR_BAD_SHAPE, "graphleap_stack: L=%d", L);
   if (!dtype_ok(dt)) return fail(GL_ERR_UNSUPPORTED, "graphleap_stack: unknown dtype");
@@ -472,7 +473,7 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
     a = BlockArgs{l == 0 ? x0 : xw[(l - 1) & 1], B, H, W, C, pool_r, keys_ws, iw[0], k,
                   Wb + l * wbytes, bb ? bb + l * bbytes : nullptr, dt,
                   l == L - 1 ? x_out : static_cast<void*>(xw[l & 1]), nullptr, 1};
-    if (schedule == GL_SCHED_LOOKAHEAD && l + 1 < L) {
+    if (schedule != GL_SCHED_STANDARD && l + 1 < L) {
       a.idx_next = iw[1];
       a.dil_next = dilations[l + 1];
     }
@@ -499,6 +500,49 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
       e = gl::launch_mrconv(a.x_in, pooled ? keys_ws : a.x_in, iw[0], a.Wt, a.bias, a.x_out, B, N,
                             M, C, C, k, dt == GL_BF16, rts[l], h->su);
       if (e != hipSuccess) return hip_fail(e, "mrconv launch");
+    }
+    return GL_OK;
+  }
+
+  if (schedule == GL_SCHED_LOOKAHEAD_FUSED) {
+    // everything on the update stream; each block is one launch holding the
+    // build tiles of the next graph and the update tiles of this block
+    if ((s = join_build(h)) != GL_OK) return s;
+    hipError_t e;
+    const int dtb = dt == GL_BF16;
+    const void* keys0 = pooled ? keys_ws : x0;
+    if (pooled && (e = gl::launch_pool(x0, keys_ws, B, H, W, C, pool_r, dtb, h->su)) != hipSuccess)
+      return hip_fail(e, "pool launch");
+    if ((s = timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
+           return gl::launch_knn(x0, keys0, B, N, C, M, k, dilations[0], dtb, iw[0], h->su, e0, e1);
+         })) != GL_OK)
+      return s;
+    int cur = 0;
+    for (int l = 0; l < L; ++l) {
+      const BlockArgs& a = blocks[l];
+      const void* keys = pooled ? keys_ws : a.x_in;
+      if (l > 0 && pooled &&
+          (e = gl::launch_pool(a.x_in, keys_ws, B, H, W, C, pool_r, dtb, h->su)) != hipSuccess)
+        return hip_fail(e, "pool launch");
+      int next = cur;
+      const bool build = l + 1 < L && !(l == 0 && dilations[1] == dilations[0]);
+      const gl::MrArgs ma = gl::make_mr_args(a.x_in, keys, iw[cur], a.Wt, a.bias, a.x_out, B, N, M,
+                                             C, C, k);
+      if (build) {
+        next = 1 - cur;
+        const gl::KnnArgs ka = gl::make_knn_args(a.x_in, keys, B, N, C, M, k, dilations[l + 1],
+                                                 iw[next]);
+        s = timed_launch(h, GL_TIME_FUSED, "block launch", [&](hipEvent_t e0, hipEvent_t e1) {
+          return gl::launch_block(ka, ma, dtb, rts[l], h->su, e0, e1);
+        });
+      } else {
+        s = timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {
+          return gl::launch_mrconv(a.x_in, keys, iw[cur], a.Wt, a.bias, a.x_out, B, N, M, C, C, k,
+                                   dtb, rts[l], h->su, e0, e1);
+        });
+      }
+      if (s != GL_OK) return s;
+      cur = next;
     }
     return GL_OK;
   }

@@ -1,0 +1,118 @@
+// One GraphLeap block in a single launch (Sec. III Eq. 10-12; Sec. IV-A).
+//
+// The lookahead makes the graph build for block l+1 and the feature update of
+// block l independent: both read only X^l.  So one grid holds both kinds of
+// workgroup -- kNN build tiles writing Ghat^(l+1) and MRConv update tiles
+// writing X^(l+1) -- and they run side by side on the CUs, the one-GPU
+// counterpart of the paper's concurrently running Graph Construction Engine
+// and Feature Update Engine.  No event or second stream orders them; the next
+// block's launch follows in stream order.
+//
+// Workgroup ids are split between the roles in groups of 8 (one per XCD), so
+// both roles spread over every XCD from the first wave of dispatch on.
+#include "knn_tile.h"
+#include "mrconv_tile.h"
+
+namespace gl {
+
+// Role of dispatch id i among nb build and nu update workgroups; j is the
+// workgroup's index within its role.
+__device__ __forceinline__ bool block_role_is_build(int i, int nb, int nu, int* j) {
+  const int P = (min(nb, nu) >> 3) << 3;
+  if (i < 2 * P) {
+    const int grp = i >> 4, pos = i & 15;
+    *j = grp * 8 + (pos & 7);
+    return pos < 8;
+  }
+  const int i2 = i - 2 * P;
+  if (i2 < nb - P) {
+    *j = P + i2;
+    return true;
+  }
+  *j = P + i2 - (nb - P);
+  return false;
+}
+
+template <int DT, int R, int RT, int KB>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void block_kernel(KnnArgs ka, MrArgs ma, int nb, int nu) {
+  extern __shared__ __align__(16) char smem[];
+  constexpr int ES = DT ? 2 : 4;
+  int j;
+  if (block_role_is_build(blockIdx.x, nb, nu, &j)) {
+    j = xcd_remap(j, nb);
+    const int nt = (ka.N + kKnnRows - 1) / kKnnRows;
+    const int b = j / nt, tile = j - b * nt;
+    knn_tile<DT, R>(smem, static_cast<const char*>(ka.x) + (size_t)b * ka.N * ka.C * ES,
+                    static_cast<const char*>(ka.keys) + (size_t)b * ka.M * ka.C * ES, ka.N, ka.C,
+                    ka.M, ka.k, ka.dil, ka.KK, ka.ib, ka.qscale, ka.qmax, tile * kKnnRows,
+                    ka.idx + (size_t)b * ka.N * ka.k);
+  } else {
+    j = xcd_remap(j, nu);
+    mrconv_tile<DT, RT, KB>(smem, ma, j * 16 * RT);
+  }
+}
+
+template <int DT, int R, int RT>
+const void* block_fn_kb(int KB) {
+  switch (KB) {
+    case 9: return (const void*)&block_kernel<DT, R, RT, 9>;
+    case 16: return (const void*)&block_kernel<DT, R, RT, 16>;
+    case 32: return (const void*)&block_kernel<DT, R, RT, 32>;
+    default: return (const void*)&block_kernel<DT, R, RT, 64>;
+  }
+}
+
+template <int DT, int R>
+const void* block_fn_rt(int RT, int KB) {
+  return RT == 2 ? block_fn_kb<DT, R, 2>(KB) : block_fn_kb<DT, R, 1>(KB);
+}
+
+template <int DT>
+const void* block_fn(int R, int RT, int KB) {
+  return R == 1 ? block_fn_rt<DT, 1>(RT, KB)
+                : R == 2 ? block_fn_rt<DT, 2>(RT, KB) : block_fn_rt<DT, 4>(RT, KB);
+}
+
+hipError_t launch_block(const KnnArgs& ka, const MrArgs& ma, int dt_bf16, int rt,
+                        hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  const int nb = ka.B * ((ka.N + kKnnRows - 1) / kKnnRows);
+  const int TM = 16 * rt;
+  const int nu = (ma.R + TM - 1) / TM;
+  const size_t smem = std::max(knn_smem_bytes(ka.C, dt_bf16),
+                               mrconv_smem_bytes(ma.C, ma.k, dt_bf16, rt));
+  const int R = knn_list_regs(ka.KK), KB = mrconv_k_bucket(ma.k);
+  const void* fn = dt_bf16 ? block_fn<1>(R, rt, KB) : block_fn<0>(R, rt, KB);
+  const dim3 grid(nb + nu), block(256);
+  struct {
+    KnnArgs ka;
+    MrArgs ma;
+    int nb, nu;
+  } args{ka, ma, nb, nu};
+  void* argv[] = {&args.ka, &args.ma, &args.nb, &args.nu};
+  if (smem > 65536) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+  }
+  if (ev0 || ev1) return hipExtLaunchKernel(fn, grid, block, argv, smem, stream, ev0, ev1, 0);
+  return hipLaunchKernel(fn, grid, block, argv, smem, stream);
+}
+
+MrArgs make_mr_args(const void* x, const void* keys, const int32_t* idx, const void* W,
+                    const void* bias, void* out, int B, int N, int M, int C, int Cout, int k) {
+  MrArgs a;
+  a.x = x;
+  a.keys = keys;
+  a.idx = idx;
+  a.W = W;
+  a.bias = bias;
+  a.out = out;
+  a.R = B * N;
+  a.N = N;
+  a.M = M;
+  a.C = C;
+  a.Cout = Cout;
+  a.k = k;
+  return a;
+}
+
+}  // namespace gl

@@ -61,6 +61,52 @@ __device__ __forceinline__ f32x4 mfma_f32(float a, float b, f32x4 acc) {
 }
 
 // ---------------------------------------------------------------------------
+// cross-lane moves inside each row of 16 lanes, as DPP modifiers (no LDS trip)
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, false);
+}
+
+// value of lane t ^ j (j = 1, 2, 4 or 8) within the lane's row of 16
+__device__ __forceinline__ uint32_t lane_xor16(uint32_t v, int j) {
+  switch (j) {
+    case 1: return dpp_mov<0xB1>(v);                     // quad_perm [1,0,3,2]
+    case 2: return dpp_mov<0x4E>(v);                     // quad_perm [2,3,0,1]
+    case 4: return dpp_mov<0x1B>(dpp_mov<0x141>(v));     // half-row mirror, then quad reverse
+    default: return dpp_mov<0x128>(v);                   // row rotate by 8
+  }
+}
+
+// value of lane 15 - t within the lane's row of 16
+__device__ __forceinline__ uint32_t lane_reverse16(uint32_t v) { return dpp_mov<0x140>(v); }
+
+// value of lane (16*(lane/16) + src) for a wave-uniform src in [0, 16)
+__device__ __forceinline__ uint32_t row_broadcast16(uint32_t v, int src, int lane) {
+  const uint32_t r0 = __builtin_amdgcn_readlane(v, src);
+  const uint32_t r1 = __builtin_amdgcn_readlane(v, 16 + src);
+  const uint32_t r2 = __builtin_amdgcn_readlane(v, 32 + src);
+  const uint32_t r3 = __builtin_amdgcn_readlane(v, 48 + src);
+  const int g = lane >> 4;
+  return g == 0 ? r0 : g == 1 ? r1 : g == 2 ? r2 : r3;
+}
+
+// sum of squares of the 8 bf16 values in v, added to acc (packed dot products)
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float sumsq_bf16x8(const uint4& v, float acc) {
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, v.x), __builtin_bit_cast(bf16x2, v.x), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, v.y), __builtin_bit_cast(bf16x2, v.y), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, v.z), __builtin_bit_cast(bf16x2, v.z), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, v.w), __builtin_bit_cast(bf16x2, v.w), acc, false);
+  return acc;
+}
+
+__device__ __forceinline__ float sumsq_f32x4(const uint4& v, float acc) {
+  const float4 f = __builtin_bit_cast(float4, v);
+  return fmaf(f.x, f.x, fmaf(f.y, f.y, fmaf(f.z, f.z, fmaf(f.w, f.w, acc))));
+}
+
+// ---------------------------------------------------------------------------
 // compare-exchange helpers on packed unsigned keys
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void cas_asc(uint32_t& a, uint32_t& b) {

@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 namespace gl {
 
 struct KnnArgs {
@@ -68,6 +70,12 @@ hipError_t launch_mrconv(const void* x, const void* keys, const int32_t* idx, co
                          const void* bias, void* out, int B, int N, int M, int C, int Cout, int k,
                          int dt_bf16, int rt, hipStream_t stream, hipEvent_t ev0 = nullptr,
                          hipEvent_t ev1 = nullptr);
+
+MrArgs make_mr_args(const void* x, const void* keys, const int32_t* idx, const void* W,
+                    const void* bias, void* out, int B, int N, int M, int C, int Cout, int k);
+// One block: the build tiles of ka and the update tiles of ma in one grid.
+hipError_t launch_block(const KnnArgs& ka, const MrArgs& ma, int dt_bf16, int rt,
+                        hipStream_t stream, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 hipError_t launch_pool(const void* x, void* keys, int B, int H, int W, int C, int r, int dt_bf16,
                        hipStream_t stream);

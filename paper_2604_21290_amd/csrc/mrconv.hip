@@ -1,45 +1,8 @@
-// Fused max-relative graph convolution for gfx950 (Sec. II-A Eq. 2-3; the
-// W_x / W_m split of Sec. IV-C2), and r x r key pooling for pyramid stages.
-//
-// One MRConv workgroup = 4 waves = TM = 16*RT consecutive nodes of the
-// flattened [B*N] node axis.
-//   1. gather: for each node and each 16-byte channel vector, the neighbour
-//      key rows are read with all loads of the vector in flight at once
-//      (the neighbour loop is unrolled to a compile-time bucket KB >= k; the
-//      slots past k repeat the first neighbour, which leaves the maximum
-//      unchanged).  Consecutive lanes read consecutive vectors of the same
-//      row, so every neighbour row is one coalesced burst.  The maximum is
-//      exact in the storage type; x_i is subtracted in fp32 and the result
-//      rounded once.  [x_i | m_i] goes straight into the LDS A-tile: no edge
-//      tensor and no [B,N,2C] concatenation is ever written to memory.
-//   2. FC on MFMA: out[TM, Cout] = A[TM, 2C] W^T + b.  The contraction runs
-//      over the concatenated axis, so columns 0..C-1 of W meet x_i and columns
-//      C..2C-1 meet m_i in one accumulation.  Each wave owns every 4th
-//      16-column output tile; W rows stream from L2 as MFMA B operands, a
-//      batch of k-steps at a time.
-#include "gl_device.h"
-#include "gl_kernels.h"
+// Standalone MRConv and key-pooling kernels and their launchers (the MRConv
+// tile itself is in mrconv_tile.h).
+#include "mrconv_tile.h"
 
 namespace gl {
-
-constexpr int kMrThreads = 256;
-constexpr int kMrKU = 2;  // k-steps of W operands loaded as one batch
-
-template <int DT>
-__device__ __forceinline__ void load_vec(const char* p, float* f) {
-  if (DT) {
-    unpack_bf16x8(*reinterpret_cast<const uint4*>(p), f);
-  } else {
-    const float4 v = *reinterpret_cast<const float4*>(p);
-    f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w;
-  }
-}
-
-template <int DT>
-__device__ __forceinline__ void store_vec(char* p, const float* f) {
-  if (DT) *reinterpret_cast<uint4*>(p) = pack_bf16x8(f);
-  else *reinterpret_cast<float4*>(p) = make_float4(f[0], f[1], f[2], f[3]);
-}
 
 int mrconv_lds_row_bytes(int C, int dt_bf16) { return 2 * C * (dt_bf16 ? 2 : 4) + 16; }
 
@@ -56,157 +19,8 @@ int mrconv_row_tiles(int C, int k, int dt_bf16, size_t lds_limit) {
 
 int mrconv_k_bucket(int k) { return k <= 9 ? 9 : k <= 16 ? 16 : k <= 32 ? 32 : 64; }
 
-// TM = 16*RT nodes starting at flattened node row0.  smem holds
-// mrconv_smem_bytes(C, k, RT) bytes.  Called by all 256 threads.
 template <int DT, int RT, int KB>
-__device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row0) {
-  constexpr int TM = 16 * RT;
-  constexpr int ES = DT ? 2 : 4;
-  constexpr int VEC = 16 / ES;
-  const int C = a.C, k = a.k, M = a.M, N = a.N, R = a.R, Cout = a.Cout;
-  const int lds_row = 2 * C * ES + 16;
-  char* sA = smem;
-  int32_t* sIdx = reinterpret_cast<int32_t*>(smem + TM * lds_row);
-
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int g = lane >> 4, t = lane & 15;
-  const int CG = C / VEC;
-
-  // -- neighbour lists of the tile ---------------------------------------------
-  for (int e = tid; e < TM * k; e += kMrThreads) {
-    const int r = e / k, tt = e - r * k, row = row0 + r;
-    const int j = row < R ? a.idx[(size_t)row * k + tt] : 0;
-    sIdx[e] = min(max(j, 0), M - 1);
-  }
-  __syncthreads();
-
-  // -- gather-max into the LDS A-tile ------------------------------------------
-  for (int e = tid; e < TM * CG; e += kMrThreads) {
-    const int r = e / CG, cg = e - r * CG;
-    const int row = min(row0 + r, R - 1);
-    const int b = row / N;
-    const char* xrow = static_cast<const char*>(a.x) + ((size_t)row * C + cg * VEC) * ES;
-    const char* kbase = static_cast<const char*>(a.keys) + ((size_t)b * M * C + cg * VEC) * ES;
-    const int32_t* nb = sIdx + r * k;
-    const uint4 xraw = *reinterpret_cast<const uint4*>(xrow);
-    float xf[VEC], mx[VEC];
-    if (DT) unpack_bf16x8(xraw, xf);
-    else { const float4 v = __builtin_bit_cast(float4, xraw); xf[0] = v.x; xf[1] = v.y; xf[2] = v.z; xf[3] = v.w; }
-#pragma unroll
-    for (int i = 0; i < VEC; ++i) mx[i] = -INFINITY;
-    constexpr int KG = KB < 16 ? KB : 16;  // neighbour loads in flight per group
-#pragma unroll 1
-    for (int t0 = 0; t0 < KB; t0 += KG) {
-      uint4 raw[KG];
-#pragma unroll
-      for (int u = 0; u < KG; ++u) {
-        const int tt = t0 + u;
-        const int j = nb[tt < k ? tt : 0];
-        raw[u] = *reinterpret_cast<const uint4*>(kbase + (size_t)j * C * ES);
-      }
-#pragma unroll
-      for (int u = 0; u < KG; ++u) {
-        float kf[VEC];
-        if (DT) unpack_bf16x8(raw[u], kf);
-        else { const float4 v = __builtin_bit_cast(float4, raw[u]); kf[0] = v.x; kf[1] = v.y; kf[2] = v.z; kf[3] = v.w; }
-#pragma unroll
-        for (int i = 0; i < VEC; ++i) mx[i] = fmaxf(mx[i], kf[i]);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < VEC; ++i) mx[i] -= xf[i];
-    char* dst = sA + r * lds_row + cg * 16;
-    *reinterpret_cast<uint4*>(dst) = xraw;
-    store_vec<DT>(dst + C * ES, mx);
-  }
-  __syncthreads();
-
-  // -- FC on MFMA -----------------------------------------------------------------
-  const int K2 = 2 * C;
-  const int KSTEP = DT ? 32 : 16;
-  const int ksteps = (K2 + KSTEP - 1) / KSTEP;
-  const int NCT = (Cout + 15) >> 4;
-  const char* Wb = static_cast<const char*>(a.W);
-  for (int p = 0; w + 16 * p < NCT; ++p) {
-    f32x4 acc[RT][4];
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4) acc[rt][c4] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const char* wrow[4];
-    bool nvalid[4];
-#pragma unroll
-    for (int c4 = 0; c4 < 4; ++c4) {
-      const int n = (w + 4 * (4 * p + c4)) * 16 + t;
-      nvalid[c4] = n < Cout;
-      wrow[c4] = Wb + (size_t)min(n, Cout - 1) * K2 * ES;
-    }
-    for (int s0 = 0; s0 < ksteps; s0 += kMrKU) {
-      uint4 bw[kMrKU][4];
-      bool kin[kMrKU];
-#pragma unroll
-      for (int u = 0; u < kMrKU; ++u) {
-        const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
-        kin[u] = kk < K2;
-        const int kl = kin[u] ? kk : 0;
-#pragma unroll
-        for (int c4 = 0; c4 < 4; ++c4)
-          bw[u][c4] = *reinterpret_cast<const uint4*>(wrow[c4] + (size_t)kl * ES);
-      }
-#pragma unroll
-      for (int u = 0; u < kMrKU; ++u) {
-        const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
-        uint4 af[RT];
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-          af[rt] = kin[u] ? *reinterpret_cast<const uint4*>(sA + (rt * 16 + t) * lds_row + kk * ES)
-                          : make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int c4 = 0; c4 < 4; ++c4) {
-          const uint4 bv = (kin[u] && nvalid[c4]) ? bw[u][c4] : make_uint4(0, 0, 0, 0);
-#pragma unroll
-          for (int rt = 0; rt < RT; ++rt) {
-            if (DT) {
-              acc[rt][c4] = mfma_bf16(af[rt], bv, acc[rt][c4]);
-            } else {
-              const float4 x4 = __builtin_bit_cast(float4, af[rt]);
-              const float4 w4 = __builtin_bit_cast(float4, bv);
-              acc[rt][c4] = mfma_f32(x4.x, w4.x, acc[rt][c4]);
-              acc[rt][c4] = mfma_f32(x4.y, w4.y, acc[rt][c4]);
-              acc[rt][c4] = mfma_f32(x4.z, w4.z, acc[rt][c4]);
-              acc[rt][c4] = mfma_f32(x4.w, w4.w, acc[rt][c4]);
-            }
-          }
-        }
-      }
-    }
-    // -- epilogue: + bias, round once, store ------------------------------------
-#pragma unroll
-    for (int c4 = 0; c4 < 4; ++c4) {
-      if (!nvalid[c4]) continue;
-      const int n = (w + 4 * (4 * p + c4)) * 16 + t;
-      float bn = 0.f;
-      if (a.bias) {
-        bn = DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(a.bias)[n])
-                : static_cast<const float*>(a.bias)[n];
-      }
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int row = row0 + rt * 16 + 4 * g + v;
-          if (row >= R) continue;
-          const float y = acc[rt][c4][v] + bn;
-          if (DT) static_cast<uint16_t*>(a.out)[(size_t)row * Cout + n] = (uint16_t)f32_to_bf16_bits(y);
-          else static_cast<float*>(a.out)[(size_t)row * Cout + n] = y;
-        }
-      }
-    }
-  }
-}
-
-template <int DT, int RT, int KB>
-__global__ __launch_bounds__(kMrThreads) void mrconv_kernel(MrArgs a) {
+__global__ __launch_bounds__(kMrThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void mrconv_kernel(MrArgs a) {
   extern __shared__ __align__(16) char smem[];
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
   mrconv_tile<DT, RT, KB>(smem, a, blk * 16 * RT);

@@ -62,7 +62,6 @@ def test_knn_validation():
     assert _knn(keys=P(10), M=5000)[0] == "GL_ERR_BAD_SHAPE"
     assert _knn(C=12)[0] == "GL_ERR_UNSUPPORTED"           # bf16 needs C % 8 == 0
     assert _knn(C=10, dt=0)[0] == "GL_ERR_UNSUPPORTED"     # fp32 needs C % 4 == 0
-    assert _knn(C=8192)[0] == "GL_ERR_UNSUPPORTED"         # query tile exceeds LDS
     assert _knn(k=0)[0] == "GL_ERR_BAD_K"
     assert _knn(d=0)[0] == "GL_ERR_BAD_K"
     assert _knn(k=33, d=2)[0] == "GL_ERR_BAD_K"             # k*d > 64

@@ -110,7 +110,7 @@ def test_lookahead_blocks_teacher_forced(case):
     teacher_forced_checks(w, xs, graphs, Wst, bst, n_img=n_img, rows=rows)
 
 
-@pytest.mark.parametrize("name", ["vig_ti", "vig_b", "pyr_s1", "hires"])
+@pytest.mark.parametrize("name", ["single", "vig_ti", "vig_b", "pyr_s1", "pyr_s2", "hires"])
 def test_stack_entry_matches_blocks_and_serial(name):
     """gl_graphleap_stack at the full workload size (the launch configuration
     the benchmark times) equals the block-by-block run bit for bit, and the
@@ -132,6 +132,13 @@ def test_stack_entry_matches_blocks_and_serial(name):
     assert torch.equal(out, xs[-1]), "stack entry differs from block-by-block"
     xs1, _ = run_blocks(w, x0d, Wd, bd, same_stream=True)
     assert torch.equal(xs1[-1], xs[-1]), "one-stream run differs from overlapped run"
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    ws = api.make_stack_workspace(x0d, w.H, w.W, w.k, w.pool_r)
+    fused = la.stack(x0d, w.H, w.W, Wd, bd, list(w.dilations), w.k, w.pool_r,
+                     schedule=api.GL_SCHED_LOOKAHEAD_FUSED, ws=ws)
+    torch.cuda.synchronize()
+    la.close()
+    assert torch.equal(fused, out), "one-launch blocks differ from the two-stream schedule"
 
 
 @pytest.mark.parametrize("name", ["vig_ti", "pyr_s2"])
@@ -170,9 +177,11 @@ def test_identity_weights_schedules_agree():
     la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
     a = la.stack(x0d, w.H, w.W, Wd, None, list(w.dilations), w.k)
     b = la.stack(x0d, w.H, w.W, Wd, None, list(w.dilations), w.k, schedule=api.GL_SCHED_STANDARD)
+    c = la.stack(x0d, w.H, w.W, Wd, None, list(w.dilations), w.k,
+                 schedule=api.GL_SCHED_LOOKAHEAD_FUSED)
     torch.cuda.synchronize()
     la.close()
-    assert torch.equal(a, x0d) and torch.equal(b, x0d)
+    assert torch.equal(a, x0d) and torch.equal(b, x0d) and torch.equal(c, x0d)
 
 
 def test_profiling_records_builds():
@@ -191,3 +200,14 @@ def test_profiling_records_builds():
     assert len(times) == w.L - 1          # bootstrap + L-2 lookahead builds (d_1 == d_0)
     assert len(upd) == w.L
     assert all(t > 0 for t in times) and all(t > 0 for t in upd)
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    la.set_profiling(64)
+    la.stack(to_dev(x0), w.H, w.W, to_dev(Wst), to_dev(bst), list(w.dilations), w.k,
+             schedule=api.GL_SCHED_LOOKAHEAD_FUSED)
+    torch.cuda.synchronize()
+    b = la.kernel_times_ms(api.GL_TIME_BUILD)
+    u = la.kernel_times_ms(api.GL_TIME_UPDATE)
+    f = la.kernel_times_ms(api.GL_TIME_FUSED)
+    la.close()
+    # bootstrap build; blocks 0 and L-1 are plain updates; blocks 1..L-2 one launch each
+    assert (len(b), len(u), len(f)) == (1, 2, w.L - 2)
