@@ -528,12 +528,24 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
       const bool build = l + 1 < L && !(l == 0 && dilations[1] == dilations[0]);
       const gl::MrArgs ma = gl::make_mr_args(a.x_in, keys, iw[cur], a.Wt, a.bias, a.x_out, B, N, M,
                                              C, C, k);
-      if (build) {
+      if (build && !gl::knn_use_stream(M, C, dtb)) {
         next = 1 - cur;
         const gl::KnnArgs ka = gl::make_knn_args(a.x_in, keys, B, N, C, M, k, dilations[l + 1],
                                                  iw[next]);
         s = timed_launch(h, GL_TIME_FUSED, "block launch", [&](hipEvent_t e0, hipEvent_t e1) {
           return gl::launch_block(ka, ma, dtb, rts[l], h->su, e0, e1);
+        });
+      } else if (build) {
+        // large key sets: the streamed kNN kernel, then the update, in stream order
+        next = 1 - cur;
+        s = timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
+          return gl::launch_knn(a.x_in, keys, B, N, C, M, k, dilations[l + 1], dtb, iw[next], h->su,
+                                e0, e1);
+        });
+        if (s != GL_OK) return s;
+        s = timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {
+          return gl::launch_mrconv(a.x_in, keys, iw[cur], a.Wt, a.bias, a.x_out, B, N, M, C, C, k,
+                                   dtb, rts[l], h->su, e0, e1);
         });
       } else {
         s = timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {

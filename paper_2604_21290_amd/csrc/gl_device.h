@@ -8,6 +8,7 @@ namespace gl {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // register-friendly 16-byte vector
 
 constexpr int kWave = 64;
 

@@ -61,6 +61,11 @@ hipError_t launch_knn(const void* x, const void* keys, int B, int N, int C, int 
                       int dil, int dt_bf16, int32_t* idx_out, hipStream_t stream,
                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
+// Large key sets (M > 256) use the kernel that streams key chunks through LDS.
+bool knn_use_stream(int M, int C, int dt_bf16);
+hipError_t launch_knn_stream(const KnnArgs& a, int dt_bf16, hipStream_t stream, hipEvent_t ev0,
+                             hipEvent_t ev1);
+
 int mrconv_lds_row_bytes(int C, int dt_bf16);
 size_t mrconv_smem_bytes(int C, int k, int dt_bf16, int rt);
 // Row tiles of 16 nodes per workgroup (2 or 1) whose LDS need fits lds_limit; 0 if none.

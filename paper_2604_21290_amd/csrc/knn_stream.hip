@@ -1,0 +1,386 @@
+// Dilated kNN graph build with keys streamed through LDS, for large key sets
+// (Sec. II-B Eq. 4; Sec. IV-B; Alg. 2).
+//
+// One workgroup = 4 waves = 64 query rows of one image; wave w owns rows
+// 16w .. 16w+15 and keeps their MFMA A operands (all contraction steps) and
+// inverse norms in registers for the whole kernel.
+//   1. Keys arrive in chunks of KC rows, loaded cooperatively (16-byte vectors,
+//      fully coalesced) into registers while the previous chunk is used, then
+//      stored to LDS; each key's distance scale factors are computed once per
+//      chunk (two threads per key).
+//   2. Four 16-key tiles at a time, the Gram tiles come from four independent
+//      MFMA chains with B operands read from LDS.  The epilogue costs two operations per candidate,
+//        d1s = qscale * ((1 + n_j) - 2 r_i r_j G_ij)
+//      (the fixed-point distance of the in-register kernel, before the
+//      floor), followed by a compare against the row's threshold: the
+//      K'-th packed key's distance bucket plus one, so no candidate that
+//      could enter the list is dropped.
+//   3. Every lane owns kStSlots LDS slots per row of its 4 rows and appends
+//      without branching: it always stores (passing key, or the empty marker
+//      0xffffffff) at its next free slot and advances the slot count by the
+//      pass bit.  When some lane's slots could overflow in the next group of
+//      tiles, and at the end, the wave merges its 16 rows' slots into their
+//      sorted register lists (4 rows at a time, 16 lanes per row, the same
+//      bitonic merge as the in-register kernel), empties the slots and
+//      refreshes the thresholds.
+// Results are identical to the in-register kernel: the same packed keys are
+// ranked, and the threshold only skips keys that cannot enter the list.
+#include "knn_tile.h"
+
+namespace gl {
+
+constexpr int kStRows = 64;      // query rows per workgroup
+constexpr int kStCap = 128;      // candidate slots per row
+constexpr int kStSlots = kStCap / 16;  // slots per (lane, row)
+constexpr int kStGroup = 4;      // key tiles computed together (independent MFMA chains)
+constexpr int kStThreads = 256;
+constexpr int kStMaxVec = 8;     // 16-byte loads per thread per chunk (keys <= 32 KB)
+constexpr size_t kStKeyBytes = 32 * 1024;  // one key chunk
+
+struct StreamGeom {
+  int KC, kstride;
+  size_t keys, scales, cand, tau, total;
+};
+
+__host__ __device__ inline StreamGeom stream_geom(int C, int dt_bf16) {
+  StreamGeom s;
+  s.kstride = C * (dt_bf16 ? 2 : 4) + 16;
+  int kc = (int)(kStKeyBytes / s.kstride) / 64 * 64;  // whole groups of 4 tiles
+  s.KC = kc > 256 ? 256 : kc < 64 ? 64 : kc;          // wide rows: 64 keys (<= 97 KB)
+  s.keys = 0;
+  s.scales = s.keys + (size_t)s.KC * s.kstride;
+  s.cand = s.scales + (size_t)s.KC * 8;
+  s.tau = s.cand + (size_t)kStRows * kStCap * 4;
+  s.total = s.tau + kStRows * 4;
+  return s;
+}
+
+template <int DT>
+__device__ __forceinline__ void st_load_chunk(u32x4 (&regs)[kStMaxVec], const char* kb, int k0,
+                                              int M, int C, int CG, int nvec, int e0, int tid) {
+  constexpr int ES = DT ? 2 : 4;
+  constexpr int VEC = 16 / ES;
+#pragma unroll
+  for (int i = 0; i < kStMaxVec; ++i) {
+    const int e = min(e0 + tid + i * kStThreads, nvec - 1);
+    const int r = e / CG, cg = e - r * CG;
+    regs[i] = *reinterpret_cast<const u32x4*>(kb + ((size_t)min(k0 + r, M - 1) * C + cg * VEC) * ES);
+  }
+}
+
+__device__ __forceinline__ void st_store_chunk(const u32x4 (&regs)[kStMaxVec], char* kbuf,
+                                               int kstride, int CG, int nvec, int e0, int tid) {
+#pragma unroll
+  for (int i = 0; i < kStMaxVec; ++i) {
+    const int e = e0 + tid + i * kStThreads;
+    const int ec = min(e, nvec - 1);
+    const int r = ec / CG, cg = ec - r * CG;
+    if (e < nvec) *reinterpret_cast<u32x4*>(kbuf + r * kstride + cg * 16) = regs[i];
+  }
+}
+
+// Distance scale factors of the keys of one chunk, two threads per key.  Norms
+// are summed in the order of the in-register kernel (per 4-lane-group channel
+// slice over the contraction steps, then (s0 + s1) + (s2 + s3)), so both
+// kernels rank identical packed keys.
+template <int DT>
+__device__ __forceinline__ void st_chunk_scales(const char* kbuf, float2* ksc, int KC, int kstride,
+                                                int k0, int M, int C, int ksteps, float qscale,
+                                                int tid) {
+  constexpr int ES = DT ? 2 : 4;
+  constexpr int KSTEP = DT ? 32 : 16;
+  const int half = tid & 1;
+  for (int r0 = 0; r0 < KC; r0 += kStThreads / 2) {
+    const int r = r0 + (tid >> 1);
+    const int rr = min(r, KC - 1);
+    float pair = 0.f;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int gg = 2 * half + q;
+      float ss = 0.f;
+      for (int s = 0; s < ksteps; ++s) {
+        const int c = s * KSTEP + gg * (KSTEP / 4);
+        if (c < C) {
+          const uint4 v = *reinterpret_cast<const uint4*>(kbuf + rr * kstride + (size_t)c * ES);
+          ss = DT ? sumsq_bf16x8(v, ss) : sumsq_f32x4(v, ss);
+        }
+      }
+      pair = q ? pair + ss : ss;
+    }
+    const float other = __shfl_xor(pair, 1);
+    const float ss = half ? other + pair : pair + other;  // (s0 + s1) + (s2 + s3)
+    const float m2rj = -2.f / fmaxf(sqrtf(ss), 1e-12f);
+    const float base = ss > 0.f ? 2.f : 1.f;  // 1 + n_j
+    if (half == 0 && r < KC)
+      ksc[r] = k0 + r < M ? make_float2(m2rj * qscale, base * qscale) : make_float2(0.f, INFINITY);
+  }
+}
+
+// Merge the wave's buffered candidates of its 16 rows into their sorted lists,
+// empty the slots and refresh the filter thresholds.  L[p] holds row 4p + g
+// (16 lanes per row); tS[v] belongs to row 4g + v.
+template <int R>
+__device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], uint32_t* cand,
+                                         uint32_t* tauL, int KK, int ib, int lane, int g, int t) {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int row = 4 * p + g;
+    uint32_t tk = list_element<R>(L[p], KK - 1, lane);
+    uint32_t v4[kStSlots];
+#pragma unroll
+    for (int m = 0; m < kStSlots; ++m) {
+      uint32_t* slot = cand + row * kStCap + t + 16 * m;
+      const uint32_t c = *slot;
+      *slot = 0xffffffffu;
+      v4[m] = c < tk ? c : 0xffffffffu;
+    }
+    bool pass = false;
+#pragma unroll
+    for (int m = 0; m < kStSlots; ++m) pass |= v4[m] != 0xffffffffu;
+    if (__any(pass)) {
+      sort_regs_asc<kStSlots>(v4);
+#pragma unroll
+      for (int m = 0; m < kStSlots; ++m) {
+        if (!__any(v4[m] < tk)) break;
+        merge16_into_list<R>(L[p], sort16_lanes(v4[m], t), t);
+        tk = list_element<R>(L[p], KK - 1, lane);
+      }
+    }
+    if (t == 0) tauL[row] = tk;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const uint32_t tk = tauL[4 * g + v];
+    tS[v] = tk == 0xffffffffu ? INFINITY : (float)((tk >> ib) + 1u);
+  }
+}
+
+template <int DT, int R, int KS>
+__global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int KC, int kstride) {
+  extern __shared__ __align__(16) char smem[];
+  constexpr int ES = DT ? 2 : 4;
+  constexpr int VEC = 16 / ES;
+  constexpr int KSTEP = DT ? 32 : 16;
+  const int N = a.N, C = a.C, M = a.M, k = a.k, dil = a.dil, KK = a.KK, ib = a.ib;
+  const float qscale = a.qscale;
+  const float qmaxf = (float)a.qmax;
+  const int ksteps = (C + KSTEP - 1) / KSTEP;
+  const int nqb = (N + kStRows - 1) / kStRows;
+  const int blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int b = blk / nqb, q0 = (blk - b * nqb) * kStRows;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int g = lane >> 4, t = lane & 15;
+
+  const StreamGeom geo = stream_geom(C, DT);
+  char* kbuf0 = smem + geo.keys;
+  float2* ksc0 = reinterpret_cast<float2*>(smem + geo.scales);
+  uint32_t* cand = reinterpret_cast<uint32_t*>(smem + geo.cand) + w * 16 * kStCap;
+  uint32_t* tauL = reinterpret_cast<uint32_t*>(smem + geo.tau) + w * 16;
+
+  const char* xb = static_cast<const char*>(a.x) + (size_t)b * N * C * ES;
+  const char* kb = static_cast<const char*>(a.keys) + (size_t)b * M * C * ES;
+
+  // -- query operands and inverse norms (rows q0 + 16w + t) ----------------------
+  uint4 af[KS];
+  float qss = 0.f;
+  {
+    const char* qg = xb + (size_t)min(q0 + 16 * w + t, N - 1) * C * ES;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int c = s * KSTEP + g * (KSTEP / 4);
+      const bool in = s < ksteps && c < C;
+      af[s] = *reinterpret_cast<const uint4*>(qg + (size_t)(in ? c : 0) * ES);
+      if (!in) af[s] = make_uint4(0, 0, 0, 0);
+      qss = DT ? sumsq_bf16x8(af[s], qss) : sumsq_f32x4(af[s], qss);
+    }
+  }
+  qss += __shfl_xor(qss, 16);
+  qss += __shfl_xor(qss, 32);
+  float qr[4];
+  {
+    const float rq = 1.f / fmaxf(sqrtf(qss), 1e-12f);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) qr[v] = __shfl(rq, 4 * g + v);
+  }
+
+  // -- key chunks ---------------------------------------------------------------------
+  const int CG = C / VEC;
+  const int nvec = KC * CG;
+  u32x4 regs[kStMaxVec];
+
+  // -- selection state ------------------------------------------------------------
+  // L[p]: sorted list of row 4p + g (element e = t + 16*a);  tS[v]: filter
+  // threshold of row 4g + v;  nS[v]: this lane's used slots of that row, which
+  // are cand[(4g + v) * kStCap + t * kStSlots + s], s < nS[v].
+  uint32_t L[4][R];
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+#pragma unroll
+    for (int q = 0; q < R; ++q) L[p][q] = 0xffffffffu;
+  float tS[4] = {INFINITY, INFINITY, INFINITY, INFINITY};
+  int nS[4] = {0, 0, 0, 0};
+#pragma unroll
+  for (int m = 0; m < kStSlots; ++m)
+#pragma unroll
+    for (int p = 0; p < 4; ++p) cand[(4 * p + g) * kStCap + t + 16 * m] = 0xffffffffu;
+  uint32_t* mySlots = cand + 4 * g * kStCap + t * kStSlots;
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+
+  // -- main loop --------------------------------------------------------------------
+  // One LDS key buffer; the next chunk waits in registers while this one is used.
+  char* kbuf = kbuf0;
+  const int nchunks = (M + KC - 1) / KC;
+  // A chunk of at most kStMaxVec vectors per thread is prefetched into
+  // registers while the previous one is used; wider chunks (rows of more than
+  // 32 KB / 64) are copied piecewise when their turn comes.
+  const bool prefetch = nvec <= kStMaxVec * kStThreads;
+  if (prefetch) st_load_chunk<DT>(regs, kb, 0, M, C, CG, nvec, 0, tid);
+  for (int ch = 0; ch < nchunks; ++ch) {
+    const int k0 = ch * KC;
+    const int ntl = (min(KC, M - k0) + 15) >> 4;
+    if (prefetch) {
+      st_store_chunk(regs, kbuf, kstride, CG, nvec, 0, tid);
+    } else {
+      for (int e0 = 0; e0 < nvec; e0 += kStMaxVec * kStThreads) {
+        st_load_chunk<DT>(regs, kb, k0, M, C, CG, nvec, e0, tid);
+        st_store_chunk(regs, kbuf, kstride, CG, nvec, e0, tid);
+      }
+    }
+    __syncthreads();
+    st_chunk_scales<DT>(kbuf, ksc0, KC, kstride, k0, M, C, ksteps, qscale, tid);
+    __syncthreads();
+    if (prefetch && ch + 1 < nchunks) st_load_chunk<DT>(regs, kb, k0 + KC, M, C, CG, nvec, 0, tid);
+    for (int t0 = 0; t0 < ntl; t0 += kStGroup) {
+      bool full = false;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) full |= nS[v] > kStSlots - kStGroup;
+      if (__any(full)) {
+        st_flush<R>(L, tS, cand, tauL, KK, ib, lane, g, t);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) nS[v] = 0;
+      }
+      // Gram tiles t0 .. t0+3.  All KC rows of the key buffer hold finite
+      // values (the chunk loader repeats the last key), and the scales of
+      // rows past the key set make their distance +inf, so tiles and keys past
+      // the end need no test.  Contraction steps past C multiply a zero A
+      // operand.
+      f32x4 acc[kStGroup];
+#pragma unroll
+      for (int p = 0; p < kStGroup; ++p) acc[p] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const int c = min(s * KSTEP + g * (KSTEP / 4), C - VEC);
+        uint4 bv[kStGroup];
+#pragma unroll
+        for (int p = 0; p < kStGroup; ++p)
+          bv[p] = *reinterpret_cast<const uint4*>(kbuf + ((t0 + p) * 16 + t) * kstride + c * ES);
+#pragma unroll
+        for (int p = 0; p < kStGroup; ++p) {
+          if (DT) {
+            acc[p] = mfma_bf16(af[s], bv[p], acc[p]);
+          } else {
+            const float4 x4 = __builtin_bit_cast(float4, af[s]);
+            const float4 y4 = __builtin_bit_cast(float4, bv[p]);
+            acc[p] = mfma_f32(x4.x, y4.x, acc[p]);
+            acc[p] = mfma_f32(x4.y, y4.y, acc[p]);
+            acc[p] = mfma_f32(x4.z, y4.z, acc[p]);
+            acc[p] = mfma_f32(x4.w, y4.w, acc[p]);
+          }
+        }
+      }
+#pragma unroll
+      for (int p = 0; p < kStGroup; ++p) {
+        const int tt = t0 + p;
+        const float2 sc = ksc0[tt * 16 + t];
+        const uint32_t j = (uint32_t)(k0 + tt * 16 + t);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float d1s = fmaf(acc[p][v] * sc.x, qr[v], sc.y);
+          const bool pass = d1s < tS[v];
+          const uint32_t q = (uint32_t)__builtin_amdgcn_fmed3f(d1s, 0.f, qmaxf);
+          mySlots[v * kStCap + nS[v]] = pass ? (q << ib) | j : 0xffffffffu;
+          nS[v] += pass ? 1 : 0;
+        }
+      }
+    }
+    __syncthreads();  // every wave is done with this chunk before it is overwritten
+  }
+  st_flush<R>(L, tS, cand, tauL, KK, ib, lane, g, t);
+
+  // -- dilation and output ------------------------------------------------------------
+  const uint32_t mask = (1u << ib) - 1u;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int row = q0 + 16 * w + 4 * p + g;
+    if (row < N) {
+      int32_t* o = a.idx + ((size_t)b * N + row) * k;
+#pragma unroll
+      for (int q = 0; q < R; ++q) {
+        const int e = t + 16 * q;
+        if (e < KK && (e % dil) == 0) o[e / dil] = (int32_t)(L[p][q] & mask);
+      }
+    }
+  }
+}
+
+// Contraction steps compiled into the kernel: the next bucket at or above
+// ceil(C / step); steps past C run on a zero A operand.
+int knn_stream_ks(int C, int dt_bf16) {
+  const int KSTEP = dt_bf16 ? 32 : 16;
+  const int ks = (C + KSTEP - 1) / KSTEP;
+  for (int b : {2, 3, 4, 6, 8, 12, 16, 20, 24})
+    if (ks <= b) return b;
+  return 0;
+}
+
+bool knn_use_stream(int M, int C, int dt_bf16) {
+  return M > 256 && knn_stream_ks(C, dt_bf16) > 0;
+}
+
+template <int DT, int R>
+const void* stream_fn_ks(int KS) {
+  switch (KS) {
+    case 2: return (const void*)&knn_stream_kernel<DT, R, 2>;
+    case 3: return (const void*)&knn_stream_kernel<DT, R, 3>;
+    case 4: return (const void*)&knn_stream_kernel<DT, R, 4>;
+    case 6: return (const void*)&knn_stream_kernel<DT, R, 6>;
+    case 8: return (const void*)&knn_stream_kernel<DT, R, 8>;
+    case 12: return (const void*)&knn_stream_kernel<DT, R, 12>;
+    case 16: return (const void*)&knn_stream_kernel<DT, R, 16>;
+    case 20: return (const void*)&knn_stream_kernel<DT, R, 20>;
+    default: return (const void*)&knn_stream_kernel<DT, R, 24>;
+  }
+}
+
+hipError_t launch_knn_stream(const KnnArgs& a, int dt_bf16, hipStream_t stream, hipEvent_t ev0,
+                             hipEvent_t ev1) {
+  const StreamGeom geo = stream_geom(a.C, dt_bf16);
+  const int KS = knn_stream_ks(a.C, dt_bf16);
+  const int R = knn_list_regs(a.KK);
+  const void* fn;
+  if (dt_bf16) {
+    fn = R == 1 ? stream_fn_ks<1, 1>(KS) : R == 2 ? stream_fn_ks<1, 2>(KS) : stream_fn_ks<1, 4>(KS);
+  } else {
+    fn = R == 1 ? stream_fn_ks<0, 1>(KS) : R == 2 ? stream_fn_ks<0, 2>(KS) : stream_fn_ks<0, 4>(KS);
+  }
+  const dim3 grid(a.B * ((a.N + kStRows - 1) / kStRows)), block(kStThreads);
+  if (KS == 0 || geo.total > 160 * 1024) return hipErrorInvalidValue;
+  struct {
+    KnnArgs a;
+    int KC, kstride;
+  } args{a, geo.KC, geo.kstride};
+  void* argv[] = {&args.a, &args.KC, &args.kstride};
+  if (geo.total > 65536) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)geo.total);
+    if (e != hipSuccess) return e;
+  }
+  if (ev0 || ev1) return hipExtLaunchKernel(fn, grid, block, argv, geo.total, stream, ev0, ev1, 0);
+  return hipLaunchKernel(fn, grid, block, argv, geo.total, stream);
+}
+
+}  // namespace gl

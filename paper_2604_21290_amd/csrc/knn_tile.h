@@ -190,13 +190,13 @@ __device__ __forceinline__ void knn_tile(char* smem, const char* __restrict__ xb
         sj += __shfl_xor(sj, 16);
         sj += __shfl_xor(sj, 32);
         const int j = chunk0 + tt * 16 + t;
-        const float m2rj = -2.f / fmaxf(sqrtf(sj), 1e-12f);
-        const float base = sj > 0.f ? 2.f : 1.f;  // 1 + n_j
+        // qscale is a power of two, so scaling the factors scales d1 exactly
+        const float m2rjS = -2.f / fmaxf(sqrtf(sj), 1e-12f) * qscale;
+        const float baseS = (sj > 0.f ? 2.f : 1.f) * qscale;  // (1 + n_j) * qscale
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float d1 = fmaf(acc[p][v] * m2rj, qr[v], base);
-          uint32_t q = (uint32_t)(fmaxf(d1, 0.f) * qscale);
-          q = min(q, qmax);
+          const float d1s = fmaf(acc[p][v] * m2rjS, qr[v], baseS);
+          const uint32_t q = min((uint32_t)fmaxf(d1s, 0.f), qmax);
           sStrip[(4 * g + v) * kKnnChunk + tt * 16 + t] =
               (j < M) ? ((q << ib) | (uint32_t)j) : 0xffffffffu;
         }

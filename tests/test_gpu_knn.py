@@ -84,6 +84,12 @@ EDGE = [
     ("wide_C_bf16", 1, 40, None, 1024, 9, 4, I.BF16, "unit"),
     ("unnormalised_fp32", 3, 196, None, 192, 9, 2, I.F32, "normal"),
     ("KK_33_R4", 1, 196, None, 64, 11, 3, I.BF16, "normal"),
+    # streamed-key kernel (M > 256): ragged last chunk, widest rows, fp32
+    ("stream_ragged_M333", 2, 90, 333, 96, 16, 2, I.BF16, "normal"),
+    ("stream_wide_C768_bf16", 1, 70, 300, 768, 9, 1, I.BF16, "unit"),
+    ("stream_wide_C384_fp32", 1, 70, 300, 384, 9, 2, I.F32, "normal"),
+    ("stream_C160_R4", 2, 64, 784, 160, 16, 4, I.BF16, "unit"),
+    ("stream_fp32_C96", 1, 130, 3136, 96, 16, 2, I.F32, "normal"),
 ]
 
 
