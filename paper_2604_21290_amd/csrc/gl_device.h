@@ -107,6 +107,12 @@ __device__ __forceinline__ float sumsq_f32x4(const uint4& v, float acc) {
   return fmaf(f.x, f.x, fmaf(f.y, f.y, fmaf(f.z, f.z, fmaf(f.w, f.w, acc))));
 }
 
+// 1 / max(||k||, 1e-12) from the squared norm, with the hardware reciprocal
+// square root (about 1 ulp); both kNN kernels use it for their key rows.
+__device__ __forceinline__ float key_rnorm(float ss) {
+  return __builtin_amdgcn_rsqf(fmaxf(ss, 1e-24f));
+}
+
 // ---------------------------------------------------------------------------
 // compare-exchange helpers on packed unsigned keys
 // ---------------------------------------------------------------------------

@@ -32,25 +32,35 @@ namespace gl {
 constexpr int kStRows = 64;      // query rows per workgroup
 constexpr int kStCap = 128;      // candidate slots per row
 constexpr int kStSlots = kStCap / 16;  // slots per (lane, row)
+constexpr int kStRowStride = kStCap + 2;  // words per row of slots (rows 4 apart change bank)
 constexpr int kStGroup = 4;      // key tiles computed together (independent MFMA chains)
 constexpr int kStThreads = 256;
-constexpr int kStMaxVec = 8;     // 16-byte loads per thread per chunk (keys <= 32 KB)
-constexpr size_t kStKeyBytes = 32 * 1024;  // one key chunk
+constexpr int kStMaxVec = 10;    // 16-byte loads per thread for a prefetched chunk (<= 40 KB)
+constexpr int kStLdsBudget = 80 * 1024;  // two workgroups per CU
 
 struct StreamGeom {
   int KC, kstride;
   size_t keys, scales, cand, tau, total;
 };
 
-__host__ __device__ inline StreamGeom stream_geom(int C, int dt_bf16) {
+// LDS layout: key chunk (KC rows of kstride bytes), per-key scale pairs,
+// candidate slots, per-row thresholds.  A key row holds the KS contraction
+// steps the kernel runs (channels past C stay zero) plus 16 bytes that move
+// consecutive rows to other banks.  KC is a multiple of 64 (whole groups of 4
+// tiles), as large as the budget allows, at least 64.
+__host__ __device__ inline StreamGeom stream_geom(int C, int dt_bf16, int KS) {
   StreamGeom s;
-  s.kstride = C * (dt_bf16 ? 2 : 4) + 16;
-  int kc = (int)(kStKeyBytes / s.kstride) / 64 * 64;  // whole groups of 4 tiles
-  s.KC = kc > 256 ? 256 : kc < 64 ? 64 : kc;          // wide rows: 64 keys (<= 97 KB)
+  const int rowb = C * (dt_bf16 ? 2 : 4);
+  s.kstride = KS * 64 + 16;  // a contraction step is 64 bytes in either type
+  const int fixed = kStRows * kStRowStride * 4 + kStRows * 4;
+  int kc = (kStLdsBudget - fixed) / (s.kstride + 8);
+  const int kv = kStMaxVec * kStThreads * 16 / rowb;  // prefetchable rows
+  kc = (kc < kv ? kc : kv) / 64 * 64;
+  s.KC = kc > 256 ? 256 : kc < 64 ? 64 : kc;
   s.keys = 0;
   s.scales = s.keys + (size_t)s.KC * s.kstride;
   s.cand = s.scales + (size_t)s.KC * 8;
-  s.tau = s.cand + (size_t)kStRows * kStCap * 4;
+  s.tau = s.cand + (size_t)kStRows * kStRowStride * 4;
   s.total = s.tau + kStRows * 4;
   return s;
 }
@@ -83,42 +93,75 @@ __device__ __forceinline__ void st_store_chunk(const u32x4 (&regs)[kStMaxVec], c
 // are summed in the order of the in-register kernel (per 4-lane-group channel
 // slice over the contraction steps, then (s0 + s1) + (s2 + s3)), so both
 // kernels rank identical packed keys.
-template <int DT>
+template <int DT, int KS>
 __device__ __forceinline__ void st_chunk_scales(const char* kbuf, float2* ksc, int KC, int kstride,
-                                                int k0, int M, int C, int ksteps, float qscale,
-                                                int tid) {
+                                                int k0, int M, int C, float qscale, int tid) {
   constexpr int ES = DT ? 2 : 4;
   constexpr int KSTEP = DT ? 32 : 16;
   const int half = tid & 1;
   for (int r0 = 0; r0 < KC; r0 += kStThreads / 2) {
     const int r = r0 + (tid >> 1);
     const int rr = min(r, KC - 1);
+    uint4 v[2][KS];
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const int c = s * KSTEP + (2 * half + q) * (KSTEP / 4);
+        v[q][s] = *reinterpret_cast<const uint4*>(kbuf + rr * kstride + c * ES);
+      }
     float pair = 0.f;
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int gg = 2 * half + q;
       float ss = 0.f;
-      for (int s = 0; s < ksteps; ++s) {
-        const int c = s * KSTEP + gg * (KSTEP / 4);
-        if (c < C) {
-          const uint4 v = *reinterpret_cast<const uint4*>(kbuf + rr * kstride + (size_t)c * ES);
-          ss = DT ? sumsq_bf16x8(v, ss) : sumsq_f32x4(v, ss);
-        }
-      }
+#pragma unroll
+      for (int s = 0; s < KS; ++s) ss = DT ? sumsq_bf16x8(v[q][s], ss) : sumsq_f32x4(v[q][s], ss);
       pair = q ? pair + ss : ss;
     }
     const float other = __shfl_xor(pair, 1);
     const float ss = half ? other + pair : pair + other;  // (s0 + s1) + (s2 + s3)
-    const float m2rj = -2.f / fmaxf(sqrtf(ss), 1e-12f);
+    const float m2rj = -2.f * key_rnorm(ss);
     const float base = ss > 0.f ? 2.f : 1.f;  // 1 + n_j
     if (half == 0 && r < KC)
       ksc[r] = k0 + r < M ? make_float2(m2rj * qscale, base * qscale) : make_float2(0.f, INFINITY);
   }
 }
 
+// Gram tiles t0 .. t0+3 of the chunk in LDS against the wave's 16 query rows.
+template <int DT, int KS>
+__device__ __forceinline__ void st_gram(f32x4 (&acc)[kStGroup], const uint4 (&af)[KS],
+                                        const char* kbuf, int t0, int kstride, int C, int g, int t) {
+  constexpr int ES = DT ? 2 : 4;
+  constexpr int KSTEP = DT ? 32 : 16;
+#pragma unroll
+  for (int p = 0; p < kStGroup; ++p) acc[p] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const int c = s * KSTEP + g * (KSTEP / 4);  // channels past C read the zero pad
+    uint4 bv[kStGroup];
+#pragma unroll
+    for (int p = 0; p < kStGroup; ++p)
+      bv[p] = *reinterpret_cast<const uint4*>(kbuf + ((t0 + p) * 16 + t) * kstride + c * ES);
+#pragma unroll
+    for (int p = 0; p < kStGroup; ++p) {
+      if (DT) {
+        acc[p] = mfma_bf16(af[s], bv[p], acc[p]);
+      } else {
+        const float4 x4 = __builtin_bit_cast(float4, af[s]);
+        const float4 y4 = __builtin_bit_cast(float4, bv[p]);
+        acc[p] = mfma_f32(x4.x, y4.x, acc[p]);
+        acc[p] = mfma_f32(x4.y, y4.y, acc[p]);
+        acc[p] = mfma_f32(x4.z, y4.z, acc[p]);
+        acc[p] = mfma_f32(x4.w, y4.w, acc[p]);
+      }
+    }
+  }
+}
+
 // Merge the wave's buffered candidates of its 16 rows into their sorted lists,
 // empty the slots and refresh the filter thresholds.  L[p] holds row 4p + g
-// (16 lanes per row); tS[v] belongs to row 4g + v.
+// (16 lanes per row); tS[v] belongs to row 4g + v.  Slot s of lane t in row r
+// is cand[r * kStRowStride + 16 s + t].
 template <int R>
 __device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], uint32_t* cand,
                                          uint32_t* tauL, int KK, int ib, int lane, int g, int t) {
@@ -128,10 +171,13 @@ __device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], ui
   for (int p = 0; p < 4; ++p) {
     const int row = 4 * p + g;
     uint32_t tk = list_element<R>(L[p], KK - 1, lane);
+    int tr = t;
+    asm volatile("" : "+v"(tr));  // keeps the 8 slot addresses out of the caller's loops
     uint32_t v4[kStSlots];
+    // slot m of lane (t + m) mod 16: a lane's used slots spread over 16 readers
 #pragma unroll
     for (int m = 0; m < kStSlots; ++m) {
-      uint32_t* slot = cand + row * kStCap + t + 16 * m;
+      uint32_t* slot = cand + row * kStRowStride + 16 * m + ((tr + m) & 15);
       const uint32_t c = *slot;
       *slot = 0xffffffffu;
       v4[m] = c < tk ? c : 0xffffffffu;
@@ -159,9 +205,12 @@ __device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], ui
   }
 }
 
+// Narrow rows (KS <= 4) overlap the next group's Gram tiles with the current
+// epilogue and are held to two waves per SIMD; wider rows need their registers
+// for the A operands and run one group at a time.
 template <int DT, int R, int KS>
-__global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int KC, int kstride) {
-  extern __shared__ __align__(16) char smem[];
+__device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int kstride, char* smem) {
+  constexpr bool PIPE = KS <= 4;
   constexpr int ES = DT ? 2 : 4;
   constexpr int VEC = 16 / ES;
   constexpr int KSTEP = DT ? 32 : 16;
@@ -175,10 +224,10 @@ __global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int K
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, t = lane & 15;
 
-  const StreamGeom geo = stream_geom(C, DT);
+  const StreamGeom geo = stream_geom(C, DT, KS);
   char* kbuf0 = smem + geo.keys;
   float2* ksc0 = reinterpret_cast<float2*>(smem + geo.scales);
-  uint32_t* cand = reinterpret_cast<uint32_t*>(smem + geo.cand) + w * 16 * kStCap;
+  uint32_t* cand = reinterpret_cast<uint32_t*>(smem + geo.cand) + w * 16 * kStRowStride;
   uint32_t* tauL = reinterpret_cast<uint32_t*>(smem + geo.tau) + w * 16;
 
   const char* xb = static_cast<const char*>(a.x) + (size_t)b * N * C * ES;
@@ -215,7 +264,7 @@ __global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int K
   // -- selection state ------------------------------------------------------------
   // L[p]: sorted list of row 4p + g (element e = t + 16*a);  tS[v]: filter
   // threshold of row 4g + v;  nS[v]: this lane's used slots of that row, which
-  // are cand[(4g + v) * kStCap + t * kStSlots + s], s < nS[v].
+  // are cand[(4g + v) * kStRowStride + 16 s + t], s < nS[v].
   uint32_t L[4][R];
 #pragma unroll
   for (int p = 0; p < 4; ++p)
@@ -226,10 +275,19 @@ __global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int K
 #pragma unroll
   for (int m = 0; m < kStSlots; ++m)
 #pragma unroll
-    for (int p = 0; p < 4; ++p) cand[(4 * p + g) * kStCap + t + 16 * m] = 0xffffffffu;
-  uint32_t* mySlots = cand + 4 * g * kStCap + t * kStSlots;
+    for (int p = 0; p < 4; ++p) cand[(4 * p + g) * kStRowStride + 16 * m + t] = 0xffffffffu;
+  uint32_t* mySlots = cand + 4 * g * kStRowStride + t;
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   __builtin_amdgcn_wave_barrier();
+
+  // -- zero pad of the key rows (channels C .. 32 KS); chunk stores leave it alone ----
+  {
+    const int padv = (kstride - 16 - C * ES) / 16;
+    for (int i = tid; i < KC * padv; i += kStThreads) {
+      const int r = i / padv;
+      *reinterpret_cast<u32x4*>(kbuf0 + r * kstride + C * ES + (i - r * padv) * 16) = u32x4{0, 0, 0, 0};
+    }
+  }
 
   // -- main loop --------------------------------------------------------------------
   // One LDS key buffer; the next chunk waits in registers while this one is used.
@@ -237,7 +295,7 @@ __global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int K
   const int nchunks = (M + KC - 1) / KC;
   // A chunk of at most kStMaxVec vectors per thread is prefetched into
   // registers while the previous one is used; wider chunks (rows of more than
-  // 32 KB / 64) are copied piecewise when their turn comes.
+  // 40 KB / 64) are copied piecewise when their turn comes.
   const bool prefetch = nvec <= kStMaxVec * kStThreads;
   if (prefetch) st_load_chunk<DT>(regs, kb, 0, M, C, CG, nvec, 0, tid);
   for (int ch = 0; ch < nchunks; ++ch) {
@@ -252,9 +310,17 @@ __global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int K
       }
     }
     __syncthreads();
-    st_chunk_scales<DT>(kbuf, ksc0, KC, kstride, k0, M, C, ksteps, qscale, tid);
+    st_chunk_scales<DT, KS>(kbuf, ksc0, KC, kstride, k0, M, C, qscale, tid);
     __syncthreads();
     if (prefetch && ch + 1 < nchunks) st_load_chunk<DT>(regs, kb, k0 + KC, M, C, CG, nvec, 0, tid);
+    // Gram tiles of group t0 + 4 are issued before the epilogue of group t0
+    // (independent MFMA chains run while the VALU filters).  All KC rows of the
+    // key buffer hold finite values (the chunk loader repeats the last key),
+    // and the scales of rows past the key set make their distance +inf, so
+    // tiles and keys past the end need no test.  Contraction steps past C
+    // multiply a zero A operand.
+    f32x4 acc[kStGroup];
+    if (PIPE) st_gram<DT, KS>(acc, af, kbuf, 0, kstride, C, g, t);
     for (int t0 = 0; t0 < ntl; t0 += kStGroup) {
       bool full = false;
 #pragma unroll
@@ -264,34 +330,11 @@ __global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int K
 #pragma unroll
         for (int v = 0; v < 4; ++v) nS[v] = 0;
       }
-      // Gram tiles t0 .. t0+3.  All KC rows of the key buffer hold finite
-      // values (the chunk loader repeats the last key), and the scales of
-      // rows past the key set make their distance +inf, so tiles and keys past
-      // the end need no test.  Contraction steps past C multiply a zero A
-      // operand.
-      f32x4 acc[kStGroup];
-#pragma unroll
-      for (int p = 0; p < kStGroup; ++p) acc[p] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const int c = min(s * KSTEP + g * (KSTEP / 4), C - VEC);
-        uint4 bv[kStGroup];
-#pragma unroll
-        for (int p = 0; p < kStGroup; ++p)
-          bv[p] = *reinterpret_cast<const uint4*>(kbuf + ((t0 + p) * 16 + t) * kstride + c * ES);
-#pragma unroll
-        for (int p = 0; p < kStGroup; ++p) {
-          if (DT) {
-            acc[p] = mfma_bf16(af[s], bv[p], acc[p]);
-          } else {
-            const float4 x4 = __builtin_bit_cast(float4, af[s]);
-            const float4 y4 = __builtin_bit_cast(float4, bv[p]);
-            acc[p] = mfma_f32(x4.x, y4.x, acc[p]);
-            acc[p] = mfma_f32(x4.y, y4.y, acc[p]);
-            acc[p] = mfma_f32(x4.z, y4.z, acc[p]);
-            acc[p] = mfma_f32(x4.w, y4.w, acc[p]);
-          }
-        }
+      f32x4 nxt[kStGroup];
+      if (PIPE) {
+        if (t0 + kStGroup < ntl) st_gram<DT, KS>(nxt, af, kbuf, t0 + kStGroup, kstride, C, g, t);
+      } else {
+        st_gram<DT, KS>(acc, af, kbuf, t0, kstride, C, g, t);
       }
 #pragma unroll
       for (int p = 0; p < kStGroup; ++p) {
@@ -303,9 +346,13 @@ __global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int K
           const float d1s = fmaf(acc[p][v] * sc.x, qr[v], sc.y);
           const bool pass = d1s < tS[v];
           const uint32_t q = (uint32_t)__builtin_amdgcn_fmed3f(d1s, 0.f, qmaxf);
-          mySlots[v * kStCap + nS[v]] = pass ? (q << ib) | j : 0xffffffffu;
+          mySlots[v * kStRowStride + 16 * nS[v]] = pass ? (q << ib) | j : 0xffffffffu;
           nS[v] += pass ? 1 : 0;
         }
+      }
+      if (PIPE) {
+#pragma unroll
+        for (int p = 0; p < kStGroup; ++p) acc[p] = nxt[p];
       }
     }
     __syncthreads();  // every wave is done with this chunk before it is overwritten
@@ -328,6 +375,18 @@ __global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int K
   }
 }
 
+template <int DT, int R, int KS>
+__global__ __launch_bounds__(kStThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void knn_stream_kernel_narrow(KnnArgs a, int KC, int kstride) {
+  extern __shared__ __align__(16) char smem[];
+  knn_stream_body<DT, R, KS>(a, KC, kstride, smem);
+}
+
+template <int DT, int R, int KS>
+__global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int KC, int kstride) {
+  extern __shared__ __align__(16) char smem[];
+  knn_stream_body<DT, R, KS>(a, KC, kstride, smem);
+}
+
 // Contraction steps compiled into the kernel: the next bucket at or above
 // ceil(C / step); steps past C run on a zero A operand.
 int knn_stream_ks(int C, int dt_bf16) {
@@ -345,9 +404,9 @@ bool knn_use_stream(int M, int C, int dt_bf16) {
 template <int DT, int R>
 const void* stream_fn_ks(int KS) {
   switch (KS) {
-    case 2: return (const void*)&knn_stream_kernel<DT, R, 2>;
-    case 3: return (const void*)&knn_stream_kernel<DT, R, 3>;
-    case 4: return (const void*)&knn_stream_kernel<DT, R, 4>;
+    case 2: return (const void*)&knn_stream_kernel_narrow<DT, R, 2>;
+    case 3: return (const void*)&knn_stream_kernel_narrow<DT, R, 3>;
+    case 4: return (const void*)&knn_stream_kernel_narrow<DT, R, 4>;
     case 6: return (const void*)&knn_stream_kernel<DT, R, 6>;
     case 8: return (const void*)&knn_stream_kernel<DT, R, 8>;
     case 12: return (const void*)&knn_stream_kernel<DT, R, 12>;
@@ -359,8 +418,8 @@ const void* stream_fn_ks(int KS) {
 
 hipError_t launch_knn_stream(const KnnArgs& a, int dt_bf16, hipStream_t stream, hipEvent_t ev0,
                              hipEvent_t ev1) {
-  const StreamGeom geo = stream_geom(a.C, dt_bf16);
   const int KS = knn_stream_ks(a.C, dt_bf16);
+  const StreamGeom geo = stream_geom(a.C, dt_bf16, KS);
   const int R = knn_list_regs(a.KK);
   const void* fn;
   if (dt_bf16) {

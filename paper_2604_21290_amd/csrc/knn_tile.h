@@ -77,10 +77,11 @@ __device__ __forceinline__ void merge16_into_list(uint32_t* L, uint32_t c, int t
 // List element e (wave-uniform) of each row, broadcast to the row's 16 lanes.
 template <int R>
 __device__ __forceinline__ uint32_t list_element(const uint32_t* L, int e, int lane) {
-  uint32_t v = L[0];
+  // register select by masks (a select chain can be lowered to an indexed
+  // private-memory load)
+  uint32_t v = 0;
 #pragma unroll
-  for (int a = 1; a < R; ++a)
-    if ((e >> 4) == a) v = L[a];
+  for (int a = 0; a < R; ++a) v |= L[a] & (0u - (uint32_t)((e >> 4) == a));
   return row_broadcast16(v, e & 15, lane);
 }
 
@@ -191,7 +192,7 @@ __device__ __forceinline__ void knn_tile(char* smem, const char* __restrict__ xb
         sj += __shfl_xor(sj, 32);
         const int j = chunk0 + tt * 16 + t;
         // qscale is a power of two, so scaling the factors scales d1 exactly
-        const float m2rjS = -2.f / fmaxf(sqrtf(sj), 1e-12f) * qscale;
+        const float m2rjS = -2.f * key_rnorm(sj) * qscale;
         const float baseS = (sj > 0.f ? 2.f : 1.f) * qscale;  // (1 + n_j) * qscale
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
