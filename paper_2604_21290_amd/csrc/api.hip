@@ -100,9 +100,9 @@ gl_status check_mrconv(const void* x, int B, int N, int C, const void* keys, int
   if (C % vec_width(dt))
     return fail(GL_ERR_UNSUPPORTED, "mrconv: C=%d must be a multiple of %d", C, vec_width(dt));
   const int dtb = dt == GL_BF16;
+  // rt = 0: the fused LDS tile does not fit; the two-pass form is used
   int rt = gl::mrconv_row_tiles(C, k, dtb, 65536);
   if (!rt) rt = gl::mrconv_row_tiles(C, k, dtb, 160 * 1024);
-  if (!rt) return fail(GL_ERR_UNSUPPORTED, "mrconv: C=%d too wide for one LDS tile", C);
   if (!aligned(x, 16) || (keys && !aligned(keys, 16)) || !aligned(W, 16) || !aligned(out, 16) ||
       !aligned(idx, 4) || (bias && !aligned(bias, esize(dt))))
     return fail(GL_ERR_ALIGNMENT, "mrconv: x/keys/W/out need 16-byte alignment");
@@ -124,6 +124,8 @@ constexpr uint32_t kHandleMagic = 0x474c4c41u;  // "GLLA"
 struct gl_lookahead {
   uint32_t magic;
   hipStream_t su, sb;
+  void* ws;          // [x | m] rows of the two-pass MRConv (grown on demand, update stream)
+  size_t ws_bytes;
   hipEvent_t ev_ready, ev_built;
   bool pending;
   int prof_max;
@@ -134,6 +136,30 @@ struct gl_lookahead {
 namespace {
 
 bool handle_ok(gl_lookahead_t h) { return h && h->magic == kHandleMagic; }
+
+// The handle's MRConv workspace, at least `bytes` long.  Growing it waits for
+// the update stream, whose kernels are the only users of the old buffer.
+gl_status ensure_ws(gl_lookahead_t h, size_t bytes) {
+  if (bytes <= h->ws_bytes) return GL_OK;
+  hipError_t e = hipStreamSynchronize(h->su);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  if (h->ws) (void)hipFree(h->ws);
+  h->ws = nullptr;
+  h->ws_bytes = 0;
+  if ((e = hipMalloc(&h->ws, bytes)) != hipSuccess) return hip_fail(e, "hipMalloc (MRConv workspace)");
+  h->ws_bytes = bytes;
+  return GL_OK;
+}
+
+// Workspace the MRConv of one block needs on this handle (null if none).
+gl_status block_ws(gl_lookahead_t h, int B, int N, int C, gl_dtype dt, int rt, void** ws) {
+  *ws = nullptr;
+  const int dtb = dt == GL_BF16;
+  if (!gl::mrconv_use_split(C, C, dtb, rt)) return GL_OK;
+  gl_status s = ensure_ws(h, gl::mrconv_split_ws_bytes(B * N, C, dtb));
+  if (s == GL_OK) *ws = h->ws;
+  return s;
+}
 
 void free_profiling(gl_lookahead_t h) {
   for (int w = 0; w < 3; ++w) {
@@ -258,9 +284,11 @@ gl_status enqueue_block(gl_lookahead_t h, const BlockArgs& a, int rt, bool do_po
       return s;
     if ((s = mark_built(h)) != GL_OK) return s;
   }
+  void* ws;
+  if ((s = block_ws(h, a.B, N, a.C, a.dt, rt, &ws)) != GL_OK) return s;
   return timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {
     return gl::launch_mrconv(a.x_in, keys, a.idx_use, a.Wt, a.bias, a.x_out, a.B, N, M, a.C, a.C,
-                             a.k, a.dt == GL_BF16, rt, h->su, e0, e1);
+                             a.k, a.dt == GL_BF16, rt, ws, h->su, e0, e1);
   });
 }
 
@@ -310,8 +338,20 @@ gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
   int rt = 0;
   gl_status s = check_mrconv(x, B, N, C, keys, M, idx, k, W, bias, Cout, dt, out, &rt);
   if (s != GL_OK) return s;
-  hipError_t e = gl::launch_mrconv(x, keys ? keys : x, idx, W, bias, out, B, N, M, C, Cout, k,
-                                   dt == GL_BF16, rt, stream);
+  const int dtb = dt == GL_BF16;
+  void* ws = nullptr;
+  hipError_t e;
+  if (gl::mrconv_use_split(C, Cout, dtb, rt)) {
+    // stream-ordered workspace for the [x | m] rows of the two-pass form
+    if ((e = hipMallocAsync(&ws, gl::mrconv_split_ws_bytes(B * N, C, dtb), stream)) != hipSuccess)
+      return hip_fail(e, "hipMallocAsync (MRConv workspace)");
+  }
+  e = gl::launch_mrconv(x, keys ? keys : x, idx, W, bias, out, B, N, M, C, Cout, k, dtb, rt, ws,
+                        stream);
+  if (ws) {
+    hipError_t f = hipFreeAsync(ws, stream);
+    if (e == hipSuccess) e = f;
+  }
   return e == hipSuccess ? GL_OK : hip_fail(e, "mrconv launch");
 }
 
@@ -322,6 +362,8 @@ gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_look
   h->magic = kHandleMagic;
   h->su = s_update;
   h->sb = s_build;
+  h->ws = nullptr;
+  h->ws_bytes = 0;
   h->pending = false;
   h->prof_max = 0;
   h->prof_n[0] = h->prof_n[1] = h->prof_n[2] = 0;
@@ -343,6 +385,10 @@ gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_look
 gl_status gl_lookahead_destroy(gl_lookahead_t h) {
   if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "lookahead_destroy: bad handle");
   free_profiling(h);
+  if (h->ws) {
+    (void)hipStreamSynchronize(h->su);
+    (void)hipFree(h->ws);
+  }
   (void)hipEventDestroy(h->ev_ready);
   (void)hipEventDestroy(h->ev_built);
   h->magic = 0;
@@ -497,8 +543,10 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
       e = gl::launch_knn(a.x_in, pooled ? keys_ws : a.x_in, B, N, C, M, k, dilations[l],
                          dt == GL_BF16, iw[0], h->su);
       if (e != hipSuccess) return hip_fail(e, "knn launch");
+      void* ws;
+      if ((s = block_ws(h, B, N, C, dt, rts[l], &ws)) != GL_OK) return s;
       e = gl::launch_mrconv(a.x_in, pooled ? keys_ws : a.x_in, iw[0], a.Wt, a.bias, a.x_out, B, N,
-                            M, C, C, k, dt == GL_BF16, rts[l], h->su);
+                            M, C, C, k, dt == GL_BF16, rts[l], ws, h->su);
       if (e != hipSuccess) return hip_fail(e, "mrconv launch");
     }
     return GL_OK;
@@ -528,7 +576,9 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
       const bool build = l + 1 < L && !(l == 0 && dilations[1] == dilations[0]);
       const gl::MrArgs ma = gl::make_mr_args(a.x_in, keys, iw[cur], a.Wt, a.bias, a.x_out, B, N, M,
                                              C, C, k);
-      if (build && !gl::knn_use_stream(M, C, dtb)) {
+      void* ws;
+      if ((s = block_ws(h, B, N, C, dt, rts[l], &ws)) != GL_OK) return s;
+      if (build && !gl::knn_use_stream(M, C, dtb) && !ws) {
         next = 1 - cur;
         const gl::KnnArgs ka = gl::make_knn_args(a.x_in, keys, B, N, C, M, k, dilations[l + 1],
                                                  iw[next]);
@@ -536,7 +586,8 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
           return gl::launch_block(ka, ma, dtb, rts[l], h->su, e0, e1);
         });
       } else if (build) {
-        // large key sets: the streamed kNN kernel, then the update, in stream order
+        // large key sets or wide channels: the build kernel, then the update, in
+        // stream order
         next = 1 - cur;
         s = timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
           return gl::launch_knn(a.x_in, keys, B, N, C, M, k, dilations[l + 1], dtb, iw[next], h->su,
@@ -545,12 +596,12 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
         if (s != GL_OK) return s;
         s = timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {
           return gl::launch_mrconv(a.x_in, keys, iw[cur], a.Wt, a.bias, a.x_out, B, N, M, C, C, k,
-                                   dtb, rts[l], h->su, e0, e1);
+                                   dtb, rts[l], ws, h->su, e0, e1);
         });
       } else {
         s = timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {
           return gl::launch_mrconv(a.x_in, keys, iw[cur], a.Wt, a.bias, a.x_out, B, N, M, C, C, k,
-                                   dtb, rts[l], h->su, e0, e1);
+                                   dtb, rts[l], ws, h->su, e0, e1);
         });
       }
       if (s != GL_OK) return s;

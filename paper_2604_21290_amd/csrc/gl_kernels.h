@@ -30,6 +30,14 @@ struct MrArgs {
   int R, N, M, C, Cout, k;
 };
 
+struct GemmArgs {
+  const void* A;      // [R, K], K contiguous
+  const void* W;      // [Cout, K], K contiguous
+  const void* bias;   // [Cout] or null
+  void* out;          // [R, Cout]
+  int R, K, Cout;
+};
+
 // Workgroups are dispatched round-robin over the 8 XCDs (workgroup id mod 8).
 // Map dispatch ids so that consecutive logical ids (neighbouring tiles of the
 // same image, which share key rows) land on the same XCD and its L2.
@@ -71,10 +79,18 @@ size_t mrconv_smem_bytes(int C, int k, int dt_bf16, int rt);
 // Row tiles of 16 nodes per workgroup (2 or 1) whose LDS need fits lds_limit; 0 if none.
 int mrconv_row_tiles(int C, int k, int dt_bf16, size_t lds_limit);
 int mrconv_k_bucket(int k);
+// MRConv.  Narrow channels: one fused kernel (gather into the LDS A-tile,
+// FC from it).  Wide channels (mrconv_use_split): a gather kernel writes
+// [x | m] to split_ws (mrconv_split_ws_bytes), then the tiled GEMM.
 hipError_t launch_mrconv(const void* x, const void* keys, const int32_t* idx, const void* W,
                          const void* bias, void* out, int B, int N, int M, int C, int Cout, int k,
-                         int dt_bf16, int rt, hipStream_t stream, hipEvent_t ev0 = nullptr,
-                         hipEvent_t ev1 = nullptr);
+                         int dt_bf16, int rt, void* split_ws, hipStream_t stream,
+                         hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+bool mrconv_use_split(int C, int Cout, int dt_bf16, int rt);
+size_t mrconv_split_ws_bytes(int R, int C, int dt_bf16);
+size_t gemm_smem_bytes();
+hipError_t launch_gemm_nt(const GemmArgs& a, int dt_bf16, hipStream_t stream, hipEvent_t ev0,
+                          hipEvent_t ev1);
 
 MrArgs make_mr_args(const void* x, const void* keys, const int32_t* idx, const void* W,
                     const void* bias, void* out, int B, int N, int M, int C, int Cout, int k);

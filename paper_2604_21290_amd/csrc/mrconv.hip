@@ -36,26 +36,75 @@ const void* mrconv_fn_kb(int KB) {
   }
 }
 
+// Gather-only workgroup of the two-pass MRConv: kMrGatherRows nodes.
+constexpr int kMrGatherRows = 16;
+
+template <int DT, int KB>
+__global__ __launch_bounds__(kMrThreads) void mr_gather_kernel(MrArgs a, void* xcat) {
+  __shared__ int32_t sIdx[kMrGatherRows * 64];
+  constexpr int ES = DT ? 2 : 4;
+  const int row0 = xcd_remap(blockIdx.x, gridDim.x) * kMrGatherRows;
+  for (int e = threadIdx.x; e < kMrGatherRows * a.k; e += kMrThreads) {
+    const int r = e / a.k, tt = e - r * a.k, row = row0 + r;
+    const int j = row < a.R ? a.idx[(size_t)row * a.k + tt] : 0;
+    sIdx[e] = min(max(j, 0), a.M - 1);
+  }
+  __syncthreads();
+  const size_t stride = (size_t)2 * a.C * ES;
+  mr_gather_rows<DT, KB>(a, row0, kMrGatherRows, sIdx, static_cast<char*>(xcat) + row0 * stride,
+                         stride);
+}
+
+template <int DT>
+const void* gather_fn_kb(int KB) {
+  switch (KB) {
+    case 9: return (const void*)&mr_gather_kernel<DT, 9>;
+    case 16: return (const void*)&mr_gather_kernel<DT, 16>;
+    case 32: return (const void*)&mr_gather_kernel<DT, 32>;
+    default: return (const void*)&mr_gather_kernel<DT, 64>;
+  }
+}
+
+// The fused tile streams all of W through every workgroup of 16*rt nodes;
+// beyond 16 KB of W per node (or when the tile does not fit LDS) the two-pass
+// form, which reads W once per 128 nodes, is used.
+bool mrconv_use_split(int C, int Cout, int dt_bf16, int rt) {
+  if (rt < 1) return true;
+  const size_t wbytes = (size_t)Cout * 2 * C * (dt_bf16 ? 2 : 4);
+  return wbytes / (size_t)(16 * rt) > 16384;
+}
+
+size_t mrconv_split_ws_bytes(int R, int C, int dt_bf16) {
+  return (size_t)R * 2 * C * (dt_bf16 ? 2 : 4);
+}
+
 hipError_t launch_mrconv(const void* x, const void* keys, const int32_t* idx, const void* W,
                          const void* bias, void* out, int B, int N, int M, int C, int Cout, int k,
-                         int dt_bf16, int rt, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
-  MrArgs a;
-  a.x = x;
-  a.keys = keys;
-  a.idx = idx;
-  a.W = W;
-  a.bias = bias;
-  a.out = out;
-  a.R = B * N;
-  a.N = N;
-  a.M = M;
-  a.C = C;
-  a.Cout = Cout;
-  a.k = k;
+                         int dt_bf16, int rt, void* split_ws, hipStream_t stream, hipEvent_t ev0,
+                         hipEvent_t ev1) {
+  MrArgs a = make_mr_args(x, keys, idx, W, bias, out, B, N, M, C, Cout, k);
+  const int KB = mrconv_k_bucket(k);
+  if (mrconv_use_split(C, Cout, dt_bf16, rt)) {
+    if (!split_ws) return hipErrorInvalidValue;
+    const dim3 g1((a.R + kMrGatherRows - 1) / kMrGatherRows), blk(kMrThreads);
+    const void* fg = dt_bf16 ? gather_fn_kb<1>(KB) : gather_fn_kb<0>(KB);
+    void* argv[] = {&a, &split_ws};
+    hipError_t e = ev0 ? hipExtLaunchKernel(fg, g1, blk, argv, 0, stream, ev0, nullptr, 0)
+                       : hipLaunchKernel(fg, g1, blk, argv, 0, stream);
+    if (e != hipSuccess) return e;
+    GemmArgs ga;
+    ga.A = split_ws;
+    ga.W = W;
+    ga.bias = bias;
+    ga.out = out;
+    ga.R = a.R;
+    ga.K = 2 * C;
+    ga.Cout = Cout;
+    return launch_gemm_nt(ga, dt_bf16, stream, nullptr, ev1);
+  }
   const int TM = 16 * rt;
   const size_t smem = mrconv_smem_bytes(C, k, dt_bf16, rt);
   const dim3 grid((a.R + TM - 1) / TM), block(kMrThreads);
-  const int KB = mrconv_k_bucket(k);
   const void* fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2>(KB) : mrconv_fn_kb<1, 1>(KB))
                            : (rt == 2 ? mrconv_fn_kb<0, 2>(KB) : mrconv_fn_kb<0, 1>(KB));
   return launch_with_smem(fn, grid, block, smem, stream, ev0, ev1, a);

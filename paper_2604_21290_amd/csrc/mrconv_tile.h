@@ -43,31 +43,39 @@ __device__ __forceinline__ void store_vec(char* p, const float* f) {
   else *reinterpret_cast<float4*>(p) = make_float4(f[0], f[1], f[2], f[3]);
 }
 
-// TM = 16*RT nodes starting at flattened node row0.  smem holds
-// mrconv_smem_bytes(C, k, RT) bytes.  Called by all 256 threads.
-template <int DT, int RT, int KB>
-__device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row0) {
-  constexpr int TM = 16 * RT;
+// W operands of k-steps s0 .. s0+kMrKU-1 for the wave's output tiles
+// w + 4*(4p + c4), c4 < 4 (16 columns each).  Tiles past Cout are not loaded;
+// k past 2C reads column 0 (the MFMA gets a zero operand there).
+template <int DT>
+__device__ __forceinline__ void mr_load_w(uint4 (&bw)[kMrKU][4], const char* Wb, int w, int p,
+                                          int s0, int K2, int Cout, int g, int t) {
+  constexpr int ES = DT ? 2 : 4;
+  constexpr int KSTEP = DT ? 32 : 16;
+#pragma unroll
+  for (int c4 = 0; c4 < 4; ++c4) {
+    const int n0 = (w + 4 * (4 * p + c4)) * 16;
+    if (n0 >= Cout) continue;  // wave-uniform
+    const char* wrow = Wb + (size_t)min(n0 + t, Cout - 1) * K2 * ES;
+#pragma unroll
+    for (int u = 0; u < kMrKU; ++u) {
+      const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
+      bw[u][c4] = *reinterpret_cast<const uint4*>(wrow + (size_t)(kk < K2 ? kk : 0) * ES);
+    }
+  }
+}
+
+// Gather-max of TM nodes from flattened node row0 (Eq. 2): row r of dst
+// (dst + r * dst_stride, LDS or global memory) receives [x_i | m_i] with
+// m_i = max_t keys[idx[i, t]] - x_i.  sIdx holds the TM x k neighbour lists
+// (clamped to [0, M)).  Rows past R are not written.  Called by all 256 threads.
+template <int DT, int KB>
+__device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM,
+                                               const int32_t* sIdx, char* dst, size_t dst_stride) {
   constexpr int ES = DT ? 2 : 4;
   constexpr int VEC = 16 / ES;
-  const int C = a.C, k = a.k, M = a.M, N = a.N, R = a.R, Cout = a.Cout;
-  const int lds_row = 2 * C * ES + 16;
-  char* sA = smem;
-  int32_t* sIdx = reinterpret_cast<int32_t*>(smem + TM * lds_row);
-
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int g = lane >> 4, t = lane & 15;
+  const int C = a.C, k = a.k, M = a.M, N = a.N, R = a.R;
+  const int tid = threadIdx.x;
   const int CG = C / VEC;
-
-  // -- neighbour lists of the tile ---------------------------------------------
-  for (int e = tid; e < TM * k; e += kMrThreads) {
-    const int r = e / k, tt = e - r * k, row = row0 + r;
-    const int j = row < R ? a.idx[(size_t)row * k + tt] : 0;
-    sIdx[e] = min(max(j, 0), M - 1);
-  }
-  __syncthreads();
-
-  // -- gather-max into the LDS A-tile ------------------------------------------
   // Each task is one (node, 16-byte channel vector); with a small neighbour
   // bucket two tasks keep their loads in flight together.
   constexpr int KG = KB < 16 ? KB : 16;    // neighbour loads in flight per group
@@ -123,45 +131,65 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
       else { const float4 v = __builtin_bit_cast(float4, xraw[q]); xf[0] = v.x; xf[1] = v.y; xf[2] = v.z; xf[3] = v.w; }
 #pragma unroll
       for (int i = 0; i < VEC; ++i) mx[q][i] -= xf[i];
-      char* dst = sA + r * lds_row + cg * 16;
-      *reinterpret_cast<uint4*>(dst) = xraw[q];
-      store_vec<DT>(dst + C * ES, mx[q]);
+      if (row0 + r >= R) continue;
+      char* d = dst + (size_t)r * dst_stride + cg * 16;
+      *reinterpret_cast<uint4*>(d) = xraw[q];
+      store_vec<DT>(d + C * ES, mx[q]);
     }
   }
-  __syncthreads();
+}
 
-  // -- FC on MFMA -----------------------------------------------------------------
+// TM = 16*RT nodes starting at flattened node row0.  smem holds
+// mrconv_smem_bytes(C, k, RT) bytes.  Called by all 256 threads.
+template <int DT, int RT, int KB>
+__device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row0) {
+  constexpr int TM = 16 * RT;
+  constexpr int ES = DT ? 2 : 4;
+  const int C = a.C, k = a.k, M = a.M, R = a.R, Cout = a.Cout;
+  const int lds_row = 2 * C * ES + 16;
+  char* sA = smem;
+  int32_t* sIdx = reinterpret_cast<int32_t*>(smem + TM * lds_row);
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int g = lane >> 4, t = lane & 15;
+
+  // -- neighbour lists of the tile ---------------------------------------------
+  for (int e = tid; e < TM * k; e += kMrThreads) {
+    const int r = e / k, tt = e - r * k, row = row0 + r;
+    const int j = row < R ? a.idx[(size_t)row * k + tt] : 0;
+    sIdx[e] = min(max(j, 0), M - 1);
+  }
+
+  // -- FC geometry; the first batch of W operands is requested here, after the
+  //    lists (loads return in order) and ahead of the gather, so its latency
+  //    overlaps the gather's ------------------------------------------------------
   const int K2 = 2 * C;
   const int KSTEP = DT ? 32 : 16;
   const int ksteps = (K2 + KSTEP - 1) / KSTEP;
   const int NCT = (Cout + 15) >> 4;
   const char* Wb = static_cast<const char*>(a.W);
+  uint4 bw[kMrKU][4];
+  if (w < NCT) mr_load_w<DT>(bw, Wb, w, 0, 0, K2, Cout, g, t);
+  __syncthreads();
+
+  mr_gather_rows<DT, KB>(a, row0, TM, sIdx, sA, lds_row);
+  __syncthreads();
+
+  // -- FC on MFMA -----------------------------------------------------------------
   for (int p = 0; w + 16 * p < NCT; ++p) {
     f32x4 acc[RT][4];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int c4 = 0; c4 < 4; ++c4) acc[rt][c4] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const char* wrow[4];
     bool nvalid[4];
 #pragma unroll
-    for (int c4 = 0; c4 < 4; ++c4) {
-      const int n = (w + 4 * (4 * p + c4)) * 16 + t;
-      nvalid[c4] = n < Cout;
-      wrow[c4] = Wb + (size_t)min(n, Cout - 1) * K2 * ES;
-    }
+    for (int c4 = 0; c4 < 4; ++c4) nvalid[c4] = (w + 4 * (4 * p + c4)) * 16 < Cout;
     for (int s0 = 0; s0 < ksteps; s0 += kMrKU) {
-      uint4 bw[kMrKU][4];
+      if (p != 0 || s0 != 0) mr_load_w<DT>(bw, Wb, w, p, s0, K2, Cout, g, t);
       bool kin[kMrKU];
 #pragma unroll
-      for (int u = 0; u < kMrKU; ++u) {
-        const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
-        kin[u] = kk < K2;
-        const int kl = kin[u] ? kk : 0;
-#pragma unroll
-        for (int c4 = 0; c4 < 4; ++c4)
-          bw[u][c4] = *reinterpret_cast<const uint4*>(wrow[c4] + (size_t)kl * ES);
-      }
+      for (int u = 0; u < kMrKU; ++u) kin[u] = (s0 + u) * KSTEP + g * (KSTEP / 4) < K2;
 #pragma unroll
       for (int u = 0; u < kMrKU; ++u) {
         const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
@@ -192,8 +220,8 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
     // -- epilogue: + bias, round once, store ------------------------------------
 #pragma unroll
     for (int c4 = 0; c4 < 4; ++c4) {
-      if (!nvalid[c4]) continue;
       const int n = (w + 4 * (4 * p + c4)) * 16 + t;
+      if (!nvalid[c4] || n >= Cout) continue;
       float bn = 0.f;
       if (a.bias) {
         bn = DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(a.bias)[n])

@@ -57,6 +57,13 @@ EDGE = [
     ("fp32_vig", 1, 196, None, 192, 192, 9, I.F32, False),
     ("k_max_64", 1, 70, None, 16, 16, 64, I.BF16, True),
     ("wide_C_1024", 1, 40, None, 1024, 64, 9, I.BF16, True),
+    # two-pass form (gather to [x | m], then the tiled GEMM): ragged node and
+    # output tiles, a half contraction step at the end, fp32, pooled keys, k > 16
+    ("split_ragged_R_Cout", 3, 70, None, 512, 300, 9, I.BF16, True),
+    ("split_K_tail", 2, 45, None, 520, 264, 9, I.BF16, False),
+    ("split_fp32", 2, 77, None, 320, 136, 7, I.F32, True),
+    ("split_pooled", 2, 196, 49, 576, 576, 9, I.BF16, True),
+    ("split_k20", 1, 150, None, 512, 512, 20, I.BF16, False),
 ]
 
 
