@@ -118,8 +118,14 @@ gl_status gl_pool_keys(const void* x, int B, int H, int W, int C, int r, gl_dtyp
  *   m[b,i,c]   = max_t keys[b, idx[b,i,t], c] - x[b,i,c]
  *   out[b,i,o] = sum_c x[b,i,c] W[o,c] + sum_c m[b,i,c] W[o,C+c] + bias[o]
  * i.e. [x_i, max_j(x_j - x_i)] W^T + b with W = [W_x | W_m] (Sec. IV-C2).
- * The neighbour rows are gathered on the fly; no [B,N,k,C] edge tensor and
- * no [B,N,2C] concatenation is ever written to memory.
+ * The neighbour rows are gathered on the fly; no [B,N,k,C] edge tensor is
+ * ever written.  Narrow layers gather straight into an on-chip tile and never
+ * write the [B,N,2C] concatenation either.  When W is large per node (more
+ * than 16 KB of W per node of the fused tile, e.g. C = Cout = 640) the call
+ * runs two passes instead: the gather writes [x_i, m_i] rows to a workspace
+ * of B*N*2C*s bytes, then a tiled GEMM reads them.  This call allocates that
+ * workspace stream-ordered on `stream` (hipMallocAsync / hipFreeAsync); a
+ * failed allocation returns GL_ERR_HIP.
  *
  *   x    [B, N, C] (dt); keys [B, M, C] (dt) or NULL for keys = x (M == N).
  *   idx  [B, N, k] int32 in [0, M).  Out-of-range values are clamped into
@@ -136,7 +142,10 @@ gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
  * Lookahead handle (Sec. IV-A, IV-F; the look-ahead buffer of Sec. IV-G).
  * Holds two HIP events that order the build stream against the update
  * stream; the caller owns both streams and every tensor.  Streams must be
- * distinct for the build to overlap the update; they may be equal.
+ * distinct for the build to overlap the update; they may be equal.  For
+ * layers that take the two-pass MRConv (see gl_mrconv) the handle also owns
+ * the workspace, allocated on first need and grown when a larger layer needs
+ * it (growing waits for the update stream); gl_lookahead_destroy frees it.
  * -------------------------------------------------------------------------*/
 typedef struct gl_lookahead* gl_lookahead_t;
 

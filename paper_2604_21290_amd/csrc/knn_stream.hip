@@ -35,8 +35,11 @@ constexpr int kStSlots = kStCap / 16;  // slots per (lane, row)
 constexpr int kStRowStride = kStCap + 2;  // words per row of slots (rows 4 apart change bank)
 constexpr int kStGroup = 4;      // key tiles computed together (independent MFMA chains)
 constexpr int kStThreads = 256;
-constexpr int kStMaxVec = 10;    // 16-byte loads per thread for a prefetched chunk (<= 40 KB)
-constexpr int kStLdsBudget = 80 * 1024;  // two workgroups per CU
+// Narrow rows (<= 4 contraction steps) run two workgroups per CU; wider rows
+// are register-bound to one, which then gets more LDS and a deeper prefetch.
+constexpr int kStWideKS = 12;
+__host__ __device__ constexpr int st_max_vec(int KS) { return KS >= kStWideKS ? 20 : 10; }
+__host__ __device__ constexpr int st_lds_budget(int KS) { return KS >= kStWideKS ? 150 * 1024 : 80 * 1024; }
 
 struct StreamGeom {
   int KC, kstride;
@@ -53,8 +56,8 @@ __host__ __device__ inline StreamGeom stream_geom(int C, int dt_bf16, int KS) {
   const int rowb = C * (dt_bf16 ? 2 : 4);
   s.kstride = KS * 64 + 16;  // a contraction step is 64 bytes in either type
   const int fixed = kStRows * kStRowStride * 4 + kStRows * 4;
-  int kc = (kStLdsBudget - fixed) / (s.kstride + 8);
-  const int kv = kStMaxVec * kStThreads * 16 / rowb;  // prefetchable rows
+  int kc = (st_lds_budget(KS) - fixed) / (s.kstride + 8);
+  const int kv = st_max_vec(KS) * kStThreads * 16 / rowb;  // prefetchable rows
   kc = (kc < kv ? kc : kv) / 64 * 64;
   s.KC = kc > 256 ? 256 : kc < 64 ? 64 : kc;
   s.keys = 0;
@@ -65,23 +68,24 @@ __host__ __device__ inline StreamGeom stream_geom(int C, int dt_bf16, int KS) {
   return s;
 }
 
-template <int DT>
-__device__ __forceinline__ void st_load_chunk(u32x4 (&regs)[kStMaxVec], const char* kb, int k0,
+template <int DT, int MV>
+__device__ __forceinline__ void st_load_chunk(u32x4 (&regs)[MV], const char* kb, int k0,
                                               int M, int C, int CG, int nvec, int e0, int tid) {
   constexpr int ES = DT ? 2 : 4;
   constexpr int VEC = 16 / ES;
 #pragma unroll
-  for (int i = 0; i < kStMaxVec; ++i) {
+  for (int i = 0; i < MV; ++i) {
     const int e = min(e0 + tid + i * kStThreads, nvec - 1);
     const int r = e / CG, cg = e - r * CG;
     regs[i] = *reinterpret_cast<const u32x4*>(kb + ((size_t)min(k0 + r, M - 1) * C + cg * VEC) * ES);
   }
 }
 
-__device__ __forceinline__ void st_store_chunk(const u32x4 (&regs)[kStMaxVec], char* kbuf,
+template <int MV>
+__device__ __forceinline__ void st_store_chunk(const u32x4 (&regs)[MV], char* kbuf,
                                                int kstride, int CG, int nvec, int e0, int tid) {
 #pragma unroll
-  for (int i = 0; i < kStMaxVec; ++i) {
+  for (int i = 0; i < MV; ++i) {
     const int e = e0 + tid + i * kStThreads;
     const int ec = min(e, nvec - 1);
     const int r = ec / CG, cg = ec - r * CG;
@@ -102,22 +106,18 @@ __device__ __forceinline__ void st_chunk_scales(const char* kbuf, float2* ksc, i
   for (int r0 = 0; r0 < KC; r0 += kStThreads / 2) {
     const int r = r0 + (tid >> 1);
     const int rr = min(r, KC - 1);
-    uint4 v[2][KS];
+    float sq[2] = {0.f, 0.f};
 #pragma unroll
-    for (int q = 0; q < 2; ++q)
+    for (int s = 0; s < KS; ++s) {
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
+      for (int q = 0; q < 2; ++q) {
         const int c = s * KSTEP + (2 * half + q) * (KSTEP / 4);
-        v[q][s] = *reinterpret_cast<const uint4*>(kbuf + rr * kstride + c * ES);
+        const uint4 v = *reinterpret_cast<const uint4*>(kbuf + rr * kstride + c * ES);
+        sq[q] = DT ? sumsq_bf16x8(v, sq[q]) : sumsq_f32x4(v, sq[q]);
       }
-    float pair = 0.f;
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      float ss = 0.f;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) ss = DT ? sumsq_bf16x8(v[q][s], ss) : sumsq_f32x4(v[q][s], ss);
-      pair = q ? pair + ss : ss;
+      if (KS > 4 && (s & 3) == 3) __builtin_amdgcn_sched_barrier(0);
     }
+    const float pair = sq[0] + sq[1];
     const float other = __shfl_xor(pair, 1);
     const float ss = half ? other + pair : pair + other;  // (s0 + s1) + (s2 + s3)
     const float m2rj = -2.f * key_rnorm(ss);
@@ -155,6 +155,9 @@ __device__ __forceinline__ void st_gram(f32x4 (&acc)[kStGroup], const uint4 (&af
         acc[p] = mfma_f32(x4.w, y4.w, acc[p]);
       }
     }
+    // long contractions: keep the scheduler from hoisting every step's B loads
+    // (4 registers per tile and step) above the first MFMAs
+    if (KS > 4 && (s & 3) == 3) __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -206,11 +209,13 @@ __device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], ui
 }
 
 // Narrow rows (KS <= 4) overlap the next group's Gram tiles with the current
-// epilogue and are held to two waves per SIMD; wider rows need their registers
-// for the A operands and run one group at a time.
+// epilogue and are held to two waves per SIMD.  Medium rows need those
+// registers for their A operands and run one group at a time.  Wide rows
+// (KS >= kStWideKS) are at one wave per SIMD anyway and overlap again.
 template <int DT, int R, int KS>
 __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int kstride, char* smem) {
-  constexpr bool PIPE = KS <= 4;
+  constexpr bool PIPE = KS <= 4 || KS >= kStWideKS;
+  constexpr int MV = st_max_vec(KS);
   constexpr int ES = DT ? 2 : 4;
   constexpr int VEC = 16 / ES;
   constexpr int KSTEP = DT ? 32 : 16;
@@ -259,7 +264,7 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
   // -- key chunks ---------------------------------------------------------------------
   const int CG = C / VEC;
   const int nvec = KC * CG;
-  u32x4 regs[kStMaxVec];
+  u32x4 regs[MV];
 
   // -- selection state ------------------------------------------------------------
   // L[p]: sorted list of row 4p + g (element e = t + 16*a);  tS[v]: filter
@@ -293,10 +298,10 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
   // One LDS key buffer; the next chunk waits in registers while this one is used.
   char* kbuf = kbuf0;
   const int nchunks = (M + KC - 1) / KC;
-  // A chunk of at most kStMaxVec vectors per thread is prefetched into
-  // registers while the previous one is used; wider chunks (rows of more than
-  // 40 KB / 64) are copied piecewise when their turn comes.
-  const bool prefetch = nvec <= kStMaxVec * kStThreads;
+  // A chunk of at most MV vectors per thread is prefetched into registers
+  // while the previous one is used; larger chunks are copied piecewise when
+  // their turn comes.
+  const bool prefetch = nvec <= MV * kStThreads;
   if (prefetch) st_load_chunk<DT>(regs, kb, 0, M, C, CG, nvec, 0, tid);
   for (int ch = 0; ch < nchunks; ++ch) {
     const int k0 = ch * KC;
@@ -304,7 +309,7 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
     if (prefetch) {
       st_store_chunk(regs, kbuf, kstride, CG, nvec, 0, tid);
     } else {
-      for (int e0 = 0; e0 < nvec; e0 += kStMaxVec * kStThreads) {
+      for (int e0 = 0; e0 < nvec; e0 += MV * kStThreads) {
         st_load_chunk<DT>(regs, kb, k0, M, C, CG, nvec, e0, tid);
         st_store_chunk(regs, kbuf, kstride, CG, nvec, e0, tid);
       }
