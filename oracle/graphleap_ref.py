@@ -28,10 +28,18 @@ notes):
     key nodes and MRConv gathers the pooled (unnormalised) key rows.
   * The lookahead stack uses G(X^0) for blocks 0 and 1 and G(X^(l-1)) for
     block l >= 2; each graph gets the dilation of the block that consumes it.
+  * The full ViG block (Eq. 11-15, Alg. 1): sigma is the exact GELU
+    x Phi(x); fully connected layers are x W^T + b with W[out, in] and an
+    optional bias; there is no normalisation layer (the equations have none);
+    MRConv is single-head; the FFN is C -> 4C -> C.  Its lookahead graph comes
+    from the projected features U^(l-1) (U^0 for blocks 0 and 1).
 """
 from __future__ import annotations
 
+import math
+
 import numpy as np
+from scipy.special import erf
 
 EPS = 1e-12
 
@@ -193,4 +201,64 @@ def stack_ref(x0: np.ndarray, Ws: list, bs: list, dilations, k: int, H: int, W: 
         xs.append(mrconv_ref(xs[l], idx, Ws[l], bs[l] if bs is not None else None, keys=ku))
     if return_all:
         return xs, graphs
+    return xs[-1]
+
+
+# ----------------------------------------------------------------------------
+# the full GraphLeap ViG block (Sec. III Eq. 11-15; Alg. 1): FC1, the
+# leap-ahead graph, MRConv, FC2 + residual, FFN + residual
+# ----------------------------------------------------------------------------
+VIG_PARAMS = ("W_in", "b_in", "W_upd", "b_upd", "W_out", "b_out", "W_1", "b_1", "W_2", "b_2")
+
+
+def gelu_ref(x: np.ndarray) -> np.ndarray:
+    """sigma(x) = x Phi(x) = x/2 (1 + erf(x / sqrt 2)), the exact GELU."""
+    x = np.asarray(x, dtype=np.float64)
+    return 0.5 * x * (1.0 + erf(x / math.sqrt(2.0)))
+
+
+def linear_ref(x: np.ndarray, W: np.ndarray, b: np.ndarray | None = None) -> np.ndarray:
+    """A fully connected layer over the channel axis: x W^T + b, W[out, in]."""
+    out = np.asarray(x, dtype=np.float64) @ np.asarray(W, dtype=np.float64).T
+    if b is not None:
+        out = out + np.asarray(b, dtype=np.float64)
+    return out
+
+
+def vig_block_ref(x: np.ndarray, idx: np.ndarray, p: dict, return_all: bool = False):
+    """Block l of Alg. 1 given the graph it uses (idx into U's rows):
+        U  = X W_in^T + b_in                        (FC1, Eq. 11)
+        Ut = MRConv(U; idx)  with W_upd [C, 2C]     (Eq. 13)
+        Y  = sigma(Ut) W_out^T + b_out + X          (FC2 + residual, Eq. 14)
+        X' = sigma(Y W_1^T + b_1) W_2^T + b_2 + Y   (FFN + residual, Eq. 15)
+    Missing biases are zero.  Returns X' (or X', U, Ut, Y)."""
+    x = np.asarray(x, dtype=np.float64)
+    u = linear_ref(x, p["W_in"], p.get("b_in"))
+    ut = mrconv_ref(u, idx, p["W_upd"], p.get("b_upd"))
+    y = linear_ref(gelu_ref(ut), p["W_out"], p.get("b_out")) + x
+    h = gelu_ref(linear_ref(y, p["W_1"], p.get("b_1")))
+    xn = linear_ref(h, p["W_2"], p.get("b_2")) + y
+    return (xn, u, ut, y) if return_all else xn
+
+
+def vig_stack_ref(x0: np.ndarray, params: list, dilations, k: int,
+                  schedule: str = "lookahead", return_all: bool = False):
+    """L full blocks.  Lookahead (Eq. 12 and the bootstrap of Alg. 1): block 0
+    uses G(U^0) and block l >= 1 uses G(U^(l-1)); standard (Eq. 6): block l
+    uses G(U^l).  Each graph gets the dilation of the block that consumes it.
+    Returns X^L, or (xs, us, graphs) with return_all."""
+    if schedule not in ("lookahead", "standard"):
+        raise ValueError(schedule)
+    L = len(dilations)
+    xs = [np.asarray(x0, dtype=np.float64)]
+    us, graphs = [], []
+    for l in range(L):
+        u = linear_ref(xs[l], params[l]["W_in"], params[l].get("b_in"))
+        us.append(u)
+        src = u if (schedule == "standard" or l == 0) else us[l - 1]
+        idx = knn_ref(src, k, dilations[l])
+        graphs.append(idx)
+        xs.append(vig_block_ref(xs[l], idx, params[l]))
+    if return_all:
+        return xs, us, graphs
     return xs[-1]

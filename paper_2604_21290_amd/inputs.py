@@ -186,6 +186,28 @@ def make_bias(w: Workload, layer: int, Cout: int | None = None, zero: bool = Tru
     return store(g.uniform(-0.1, 0.1, Cout), w.dtype)
 
 
+def make_vig_params(w: Workload, layer: int, bias: bool = True) -> dict:
+    """Weights of one full ViG block (FC1, MRConv, FC2, FFN 4C), Kaiming-uniform
+    per fan-in, as Stored tensors keyed like the oracle's VIG_PARAMS.  W_upd is
+    make_weight(w, layer); the others draw from their own seeded streams.  The
+    two layers that end a residual branch (W_out, W_2) are scaled by 0.2 so a
+    12-block stack without normalisation layers keeps O(1) activations.
+    Biases are uniform(-0.1, 0.1) when `bias`, else omitted."""
+    C = w.C
+    shapes = {"W_in": (C, C), "W_out": (C, C), "W_1": (4 * C, C), "W_2": (C, 4 * C)}
+    p = {"W_upd": make_weight(w, layer)}
+    for m, (name, shp) in enumerate(sorted(shapes.items())):
+        g = np.random.default_rng([w.seed, layer, m, 17])
+        bound = math.sqrt(6.0 / shp[1]) * (0.2 if name in ("W_out", "W_2") else 1.0)
+        p[name] = store(g.uniform(-bound, bound, shp), w.dtype)
+    if bias:
+        outs = {"b_in": C, "b_upd": C, "b_out": C, "b_1": 4 * C, "b_2": C}
+        for m, (name, n) in enumerate(sorted(outs.items())):
+            g = np.random.default_rng([w.seed, layer, m, 29])
+            p[name] = store(g.uniform(-0.1, 0.1, n), w.dtype)
+    return p
+
+
 def random_features(seed: int, B: int, N: int, C: int, dtype: str,
                     unit: bool = True) -> Stored:
     """Generic seeded features for edge-case tests."""

@@ -2,7 +2,8 @@
 invariants and independent pure-Python brute force.
 
 Each pin takes an oracle-like namespace `ref` (with knn_ref, max_relative_ref,
-mrconv_ref, pool_keys_ref, stack_ref) and raises AssertionError on failure, so
+mrconv_ref, pool_keys_ref, stack_ref, gelu_ref, linear_ref, vig_block_ref,
+vig_stack_ref) and raises AssertionError on failure, so
 the same pins run against the oracle (test_oracle_pins.py) and against copies
 of it with planted mistakes (test_oracle_mutants.py), which every mistake must
 fail at least one pin.
@@ -358,6 +359,137 @@ def pin_stack_pooled_graph_source(ref):
                                              keys=ref.pool_keys_ref(xs[1], H, W, 2)))
 
 
+# ---------------------------------------------------------------------------
+# full ViG block pins (Eq. 11-15, Alg. 1)
+# ---------------------------------------------------------------------------
+PHI1 = 0.8413447460685429   # standard normal CDF at 1 (printed tables)
+PHI2 = 0.9772498680518208   # standard normal CDF at 2
+
+
+def _bf_gelu(v):
+    return 0.5 * v * (1.0 + math.erf(v / math.sqrt(2.0)))
+
+
+def bf_linear(x, W, b=None):
+    """Pure-Python x W^T + b over the last axis (W[out, in])."""
+    x = np.asarray(x).tolist()
+    W = np.asarray(W).tolist()
+    B, N = len(x), len(x[0])
+    out = np.zeros((B, N, len(W)))
+    for bb in range(B):
+        for i in range(N):
+            for o, wrow in enumerate(W):
+                s = math.fsum(a * w for a, w in zip(x[bb][i], wrow))
+                out[bb, i, o] = s + (0.0 if b is None else float(b[o]))
+    return out
+
+
+def bf_vig_block(x, idx, p):
+    gel = np.vectorize(_bf_gelu)
+    u = bf_linear(x, p["W_in"], p.get("b_in"))
+    ut = bf_mrconv(u, idx, p["W_upd"], p.get("b_upd"))
+    y = bf_linear(gel(ut), p["W_out"], p.get("b_out")) + np.asarray(x)
+    h = gel(bf_linear(y, p["W_1"], p.get("b_1")))
+    return bf_linear(h, p["W_2"], p.get("b_2")) + y
+
+
+def _vig_params(rng, C, bias=True):
+    p = {"W_in": rng.standard_normal((C, C)), "W_upd": rng.standard_normal((C, 2 * C)),
+         "W_out": rng.standard_normal((C, C)), "W_1": rng.standard_normal((4 * C, C)),
+         "W_2": rng.standard_normal((C, 4 * C)) * 0.5}
+    if bias:
+        for n, o in (("b_in", C), ("b_upd", C), ("b_out", C), ("b_1", 4 * C), ("b_2", C)):
+            p[n] = rng.standard_normal(o)
+    return p
+
+
+def pin_gelu_closed_form(ref):
+    """sigma(x) = x Phi(x): table values of Phi, and sigma(x) - sigma(-x) = x."""
+    x = np.array([0.0, 1.0, -1.0, 2.0, -2.0, 30.0, -30.0])
+    want = np.array([0.0, PHI1, -(1.0 - PHI1), 2 * PHI2, -2 * (1.0 - PHI2), 30.0, 0.0])
+    assert np.allclose(ref.gelu_ref(x), want, rtol=0, atol=1e-15), ref.gelu_ref(x)
+    z = np.linspace(-5, 5, 41)
+    assert np.allclose(ref.gelu_ref(z) - ref.gelu_ref(-z), z, rtol=0, atol=1e-14)
+
+
+def pin_linear_bruteforce(ref):
+    rng = np.random.default_rng(41)
+    x = rng.standard_normal((2, 5, 3))
+    W = rng.standard_normal((4, 3))
+    b = rng.standard_normal(4)
+    assert np.allclose(ref.linear_ref(x, W, b), bf_linear(x, W, b), atol=1e-12)
+    assert np.allclose(ref.linear_ref(x, W), bf_linear(x, W), atol=1e-12)
+
+
+def pin_vig_block_bruteforce(ref):
+    rng = np.random.default_rng(42)
+    x = rng.standard_normal((1, 6, 3))
+    idx = rng.integers(0, 6, (1, 6, 2))
+    p = _vig_params(rng, 3)
+    assert np.allclose(ref.vig_block_ref(x, idx, p), bf_vig_block(x, idx, p), atol=1e-10)
+
+
+def pin_vig_block_residual_identity(ref):
+    """W_out = 0 and W_2 = 0 (no biases): both residual paths return X exactly."""
+    rng = np.random.default_rng(43)
+    x = rng.standard_normal((2, 7, 4))
+    p = _vig_params(rng, 4, bias=False)
+    p["W_out"] = np.zeros((4, 4))
+    p["W_2"] = np.zeros((4, 16))
+    idx = rng.integers(0, 7, (2, 7, 3))
+    assert np.array_equal(ref.vig_block_ref(x, idx, p), x)
+
+
+def pin_vig_block_hand(ref):
+    """Worked by hand, self-only graph (m = 0):
+    (a) W_in = I, W_upd = [I | 0], W_out = I, W_1 = 0: U = Ut = X,
+        Y = sigma(X) + X, FFN = sigma(0) W_2 = 0, so X' = X + sigma(X);
+    (b) W_out = 0 (Y = X), W_1 = [I; 0], b_1 = (1, -1, 0, ...), W_2 = [I | 0]:
+        X' = sigma(X + b_1[:2]) + X, at X = 0 that is (Phi(1), -(1 - Phi(1)))."""
+    C = 2
+    idx = np.arange(2)[None, :, None]
+    I2 = np.eye(C)
+    x = np.array([[[1.0, -1.0], [2.0, 0.0]]])
+    pa = {"W_in": I2, "W_upd": np.hstack([I2, np.zeros((C, C))]), "W_out": I2,
+          "W_1": np.zeros((4 * C, C)), "W_2": np.ones((C, 4 * C))}
+    want = np.array([[[1 + PHI1, -1 - (1 - PHI1)], [2 + 2 * PHI2, 0.0]]])
+    assert np.allclose(ref.vig_block_ref(x, idx, pa), want, rtol=0, atol=1e-14)
+    W1 = np.zeros((4 * C, C))
+    W1[:C] = I2
+    W2 = np.zeros((C, 4 * C))
+    W2[:, :C] = I2
+    b1 = np.zeros(4 * C)
+    b1[:2] = (1.0, -1.0)
+    pb = {"W_in": I2, "W_upd": np.hstack([I2, np.zeros((C, C))]), "W_out": np.zeros((C, C)),
+          "W_1": W1, "b_1": b1, "W_2": W2}
+    x0 = np.zeros((1, 2, C))
+    want = np.array([[[PHI1, -(1 - PHI1)], [PHI1, -(1 - PHI1)]]])
+    assert np.allclose(ref.vig_block_ref(x0, idx, pb), want, rtol=0, atol=1e-14)
+
+
+def pin_vig_stack_graph_source(ref):
+    """Lookahead: blocks 0 and 1 use G(U^0), block 2 uses G(U^1); standard:
+    block l uses G(U^l), with U^l = X^l W_in^l^T computed here."""
+    rng = np.random.default_rng(44)
+    x = rng.standard_normal((1, 12, 3))
+    ps = [_vig_params(rng, 3) for _ in range(3)]
+    for p in ps:
+        p["W_2"] = p["W_2"] * 0.1
+    dil = (1, 2, 1)
+    xs, us, graphs = ref.vig_stack_ref(x, ps, dil, 3, schedule="lookahead", return_all=True)
+    u = [xs[l] @ ps[l]["W_in"].T + ps[l]["b_in"] for l in range(3)]
+    for l in range(3):
+        assert np.allclose(us[l], u[l], atol=1e-12)
+    assert np.array_equal(graphs[0], ref.knn_ref(u[0], 3, 1))
+    assert np.array_equal(graphs[1], ref.knn_ref(u[0], 3, 2))
+    assert np.array_equal(graphs[2], ref.knn_ref(u[1], 3, 1))
+    assert np.allclose(xs[3], ref.vig_block_ref(xs[2], graphs[2], ps[2]), atol=1e-12)
+    xs, us, graphs = ref.vig_stack_ref(x, ps, dil, 3, schedule="standard", return_all=True)
+    for l in range(3):
+        ul = xs[l] @ ps[l]["W_in"].T + ps[l]["b_in"]
+        assert np.array_equal(graphs[l], ref.knn_ref(ul, 3, dil[l]))
+
+
 PINS = [
     pin_circle_closed_form_fixture, pin_circle_knn, pin_knn_bruteforce, pin_knn_self_first,
     pin_knn_duplicates_lower_index, pin_knn_permutation_equivariant, pin_knn_scale_invariant,
@@ -365,7 +497,9 @@ PINS = [
     pin_knn_sorted_by_distance, pin_circle_mrconv, pin_mrconv_bruteforce, pin_mrconv_self_only,
     pin_mrconv_translation, pin_mrconv_max_minus, pin_mrconv_bias_only, pin_pool_closed_form,
     pin_stack_single_layer, pin_stack_identity_weights, pin_stack_circle_two_blocks,
-    pin_stack_pooled_graph_source,
+    pin_stack_pooled_graph_source, pin_gelu_closed_form, pin_linear_bruteforce,
+    pin_vig_block_bruteforce, pin_vig_block_residual_identity, pin_vig_block_hand,
+    pin_vig_stack_graph_source,
 ]
 
 

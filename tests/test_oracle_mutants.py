@@ -116,6 +116,56 @@ def _stack_factory(schedule_override=None, knn=None, mrconv=None, pool=None):
     return stack
 
 
+def _gelu_tanh(x):
+    x = np.asarray(x, dtype=np.float64)
+    return 0.5 * x * (1 + np.tanh(np.sqrt(2 / np.pi) * (x + 0.044715 * x ** 3)))
+
+
+def _linear_untransposed(x, W, b=None):
+    out = np.asarray(x, dtype=np.float64) @ np.asarray(W, dtype=np.float64).reshape(
+        np.asarray(W).shape[1], np.asarray(W).shape[0])
+    return out if b is None else out + b
+
+
+def _block_factory(fc2_residual=True, ffn_residual="y", gelu_after_wout=False,
+                   drop_b1=False, linear=None):
+    lin = linear or R.linear_ref
+
+    def block(x, idx, p, return_all=False):
+        x = np.asarray(x, dtype=np.float64)
+        u = lin(x, p["W_in"], p.get("b_in"))
+        ut = R.mrconv_ref(u, idx, p["W_upd"], p.get("b_upd"))
+        if gelu_after_wout:
+            y = R.gelu_ref(lin(ut, p["W_out"], p.get("b_out")))
+        else:
+            y = lin(R.gelu_ref(ut), p["W_out"], p.get("b_out"))
+        if fc2_residual:
+            y = y + x
+        h = R.gelu_ref(lin(y, p["W_1"], None if drop_b1 else p.get("b_1")))
+        xn = lin(h, p["W_2"], p.get("b_2")) + (y if ffn_residual == "y" else x)
+        return (xn, u, ut, y) if return_all else xn
+    return block
+
+
+def _vig_stack_factory(graph_from="u", lag=1, block=None):
+    blk = block or R.vig_block_ref
+
+    def stack(x0, params, dilations, k, schedule="lookahead", return_all=False):
+        L = len(dilations)
+        xs = [np.asarray(x0, dtype=np.float64)]
+        us, graphs = [], []
+        for l in range(L):
+            u = R.linear_ref(xs[l], params[l]["W_in"], params[l].get("b_in"))
+            us.append(u)
+            feats = us if graph_from == "u" else xs
+            j = l if (schedule == "standard" or l == 0) else max(l - lag, 0)
+            idx = R.knn_ref(feats[j], k, dilations[l])
+            graphs.append(idx)
+            xs.append(blk(xs[l], idx, params[l]))
+        return (xs, us, graphs) if return_all else xs[-1]
+    return stack
+
+
 MUTANTS = {
     "knn_no_normalisation": dict(knn_ref=_knn_factory(normalize=False)),
     "knn_descending": dict(knn_ref=_knn_factory(descending=True)),
@@ -132,6 +182,14 @@ MUTANTS = {
     "pool_transposed": dict(pool_keys_ref=_pool_transposed),
     "stack_standard_not_lookahead": dict(stack_ref=_stack_factory(schedule_override="standard")),
     "stack_pool_transposed": dict(stack_ref=_stack_factory(pool=_pool_transposed)),
+    "gelu_tanh_approximation": dict(gelu_ref=_gelu_tanh),
+    "linear_weight_not_transposed": dict(linear_ref=_linear_untransposed),
+    "block_no_fc2_residual": dict(vig_block_ref=_block_factory(fc2_residual=False)),
+    "block_ffn_residual_from_x": dict(vig_block_ref=_block_factory(ffn_residual="x")),
+    "block_gelu_after_wout": dict(vig_block_ref=_block_factory(gelu_after_wout=True)),
+    "block_ffn_bias_dropped": dict(vig_block_ref=_block_factory(drop_b1=True)),
+    "vig_stack_graph_from_x": dict(vig_stack_ref=_vig_stack_factory(graph_from="x")),
+    "vig_stack_no_lookahead": dict(vig_stack_ref=_vig_stack_factory(lag=0)),
 }
 
 
