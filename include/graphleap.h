@@ -157,12 +157,14 @@ gl_status gl_lookahead_destroy(gl_lookahead_t h);
  * dispatch with a start and an end HIP event (at most max_records pairs of
  * each kind are kept; later launches are not timed).
  * gl_lookahead_kernel_times() synchronises the recorded events of one kind
- * (which = GL_TIME_BUILD, GL_TIME_UPDATE or GL_TIME_FUSED), writes their
+ * (which = GL_TIME_BUILD, GL_TIME_UPDATE, GL_TIME_FUSED or GL_TIME_LINEAR),
+ * writes their
  * durations in milliseconds (at most cap of them) and clears that kind's
  * records.  max_records == 0 disables it. */
 #define GL_TIME_BUILD 0
 #define GL_TIME_UPDATE 1
 #define GL_TIME_FUSED 2   /* one-launch blocks of GL_SCHED_LOOKAHEAD_FUSED */
+#define GL_TIME_LINEAR 3  /* fully connected layers of the full ViG block */
 gl_status gl_lookahead_set_profiling(gl_lookahead_t h, int max_records);
 gl_status gl_lookahead_kernel_times(gl_lookahead_t h, int which, float* ms_out, int cap,
                                     int* n_out);
@@ -239,6 +241,82 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
 const char* gl_status_string(gl_status s);
 const char* gl_last_error(void);   /* thread-local detail of the last non-OK status */
 int gl_version(void);
+
+/* ===========================================================================
+ * The full GraphLeap ViG block (Sec. III Eq. 11-15, Alg. 1): FC1, the
+ * leap-ahead graph, MRConv, FC2 + residual and the FFN + residual.
+ * ========================================================================= */
+
+typedef enum { GL_ACT_NONE = 0, GL_ACT_GELU = 1 } gl_act;
+
+/* ---------------------------------------------------------------------------
+ * gl_linear -- one fully connected layer over the channel axis (FC1, FC2 and
+ * the FFN of Eq. 11, 14, 15):
+ *   out[r, o] = act_out( sum_c act_in(x[r, c]) W[o, c] + bias[o] ) + residual[r, o]
+ * act = GL_ACT_GELU is the exact GELU x Phi(x); act_in is applied to x's
+ * stored values and rounded back to dt (as if sigma(x) had been stored),
+ * everything after the contraction is fp32, rounded once to dt.
+ *   x [R, K] (dt); W [Cout, K] (dt); bias [Cout] (dt) or NULL;
+ *   residual [R, Cout] (dt) or NULL, and may be `out` itself (in place);
+ *   out [R, Cout] (dt), must not overlap x, W or bias.
+ * Limits: R, K, Cout >= 1; K % 8 == 0 (bf16) or K % 4 == 0 (fp32).
+ * -------------------------------------------------------------------------*/
+gl_status gl_linear(const void* x, int R, int K, const void* W, const void* bias, int Cout,
+                    gl_act act_in, gl_act act_out, const void* residual, gl_dtype dt,
+                    void* out, hipStream_t stream);
+
+/* Weights of one full block (dt, row-major [out, in]; biases may be NULL). */
+typedef struct {
+  const void* W_in;   /* [C, C]   FC1 */
+  const void* b_in;   /* [C] */
+  const void* W_upd;  /* [C, 2C]  MRConv update, [W_x | W_m] */
+  const void* b_upd;  /* [C] */
+  const void* W_out;  /* [C, C]   FC2 */
+  const void* b_out;  /* [C] */
+  const void* W_1;    /* [4C, C]  FFN hidden layer */
+  const void* b_1;    /* [4C] */
+  const void* W_2;    /* [C, 4C]  FFN output layer */
+  const void* b_2;    /* [C] */
+} gl_vig_params;
+
+/* Bytes of the workspace gl_vig_block and gl_vig_stack need (they carve
+ * sigma-input, Y and the FFN's hidden rows out of it; the stack also U, two
+ * feature buffers and two graphs). */
+size_t gl_vig_workspace_bytes(int B, int N, int C, int k, gl_dtype dt);
+
+/* ---------------------------------------------------------------------------
+ * gl_vig_block -- one full block on the lookahead handle's streams, given the
+ * graph it uses (Alg. 1):
+ *   U = x_in W_in^T + b_in -> u_out           (cached for the next graph)
+ *   [build idx_next = G(U, dilation_next) on the build stream, overlapping
+ *    everything below; skipped when idx_next is NULL]
+ *   Ut = MRConv(U; idx_use)  (W_upd, b_upd)
+ *   Y = GELU(Ut) W_out^T + b_out + x_in
+ *   x_out = GELU(Y W_1^T + b_1) W_2^T + b_2 + Y
+ * Enqueues on the update stream after waiting for the handle's previous
+ * build.  x_in, x_out, u_out [B, N, C]; idx_use, idx_next [B, N, k] int32;
+ * ws of at least gl_vig_workspace_bytes().  x_out must not overlap x_in,
+ * u_out, ws or the graphs.
+ * -------------------------------------------------------------------------*/
+gl_status gl_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, int C, int k,
+                       const int32_t* idx_use, const gl_vig_params* p, gl_dtype dt, void* ws,
+                       size_t ws_bytes, void* u_out, int32_t* idx_next, int dilation_next,
+                       void* x_out);
+
+/* ---------------------------------------------------------------------------
+ * gl_vig_stack -- L full blocks, natively enqueued.
+ *   GL_SCHED_LOOKAHEAD: Ghat^0 = G(U^0, d_0), Ghat^l = G(U^(l-1), d_l)
+ *     (Eq. 12 and Alg. 1's bootstrap); each build runs on the build stream
+ *     while the rest of its block runs on the update stream.
+ *   GL_SCHED_LOOKAHEAD_FUSED: the same graphs; one stream, each build in one
+ *     launch with its block's MRConv (both read only U^l).
+ *   GL_SCHED_STANDARD: Ghat^l = G(U^l, d_l) (Eq. 6), serial.
+ * params: L blocks' weights.  x0, x_out [B, N, C]; ws of at least
+ * gl_vig_workspace_bytes(); x_out must not overlap x0 or ws.
+ * -------------------------------------------------------------------------*/
+gl_status gl_vig_stack(gl_lookahead_t h, const void* x0, int B, int N, int C, int L, int k,
+                       const int* dilations, const gl_vig_params* params, gl_dtype dt,
+                       gl_schedule schedule, void* ws, size_t ws_bytes, void* x_out);
 
 #ifdef __cplusplus
 }

@@ -20,14 +20,22 @@ LIB_PATH = os.path.join(_HERE, "libgraphleap.so")
 
 GL_F32, GL_BF16 = 0, 1
 GL_SCHED_LOOKAHEAD, GL_SCHED_STANDARD, GL_SCHED_LOOKAHEAD_FUSED = 0, 1, 2
-GL_TIME_BUILD, GL_TIME_UPDATE, GL_TIME_FUSED = 0, 1, 2
+GL_TIME_BUILD, GL_TIME_UPDATE, GL_TIME_FUSED, GL_TIME_LINEAR = 0, 1, 2, 3
+GL_ACT_NONE, GL_ACT_GELU = 0, 1
 GL_MAX_KD, GL_MAX_M, GL_MAX_K = 64, 4096, 64
 
 STATUS = {0: "GL_OK", 1: "GL_ERR_NULL_PTR", 2: "GL_ERR_BAD_SHAPE", 3: "GL_ERR_BAD_K",
           4: "GL_ERR_UNSUPPORTED", 5: "GL_ERR_ALIGNMENT", 6: "GL_ERR_ALIAS", 7: "GL_ERR_HIP",
           8: "GL_ERR_BAD_HANDLE"}
 
-_vp, _i, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+_vp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+
+VIG_PARAMS = ("W_in", "b_in", "W_upd", "b_upd", "W_out", "b_out", "W_1", "b_1", "W_2", "b_2")
+
+
+class VigParams(ctypes.Structure):
+    """gl_vig_params: device pointers of one full block's weights (NULL biases allowed)."""
+    _fields_ = [(n, ctypes.c_void_p) for n in VIG_PARAMS]
 
 # name -> argtypes (every entry point returns gl_status as int unless noted)
 SIGNATURES = {
@@ -42,11 +50,18 @@ SIGNATURES = {
     "gl_graphleap_block": [_vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _i, _vp, _vp, _i, _vp, _vp, _i],
     "gl_graphleap_stack": [_vp, _vp, _i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i), _vp, _vp, _i,
                            _i, _vp, _vp, _vp, _vp],
+    "gl_linear": [_vp, _i, _i, _vp, _vp, _i, _i, _i, _vp, _i, _vp, _vp],
+    "gl_vig_workspace_bytes": [_i, _i, _i, _i, _i],
+    "gl_vig_block": [_vp, _vp, _i, _i, _i, _i, _vp, ctypes.POINTER(VigParams), _i, _vp, _sz, _vp,
+                     _vp, _i, _vp],
+    "gl_vig_stack": [_vp, _vp, _i, _i, _i, _i, _i, ctypes.POINTER(_i), ctypes.POINTER(VigParams),
+                     _i, _i, _vp, _sz, _vp],
     "gl_status_string": [_i],
     "gl_last_error": [],
     "gl_version": [],
 }
-RESTYPES = {"gl_status_string": ctypes.c_char_p, "gl_last_error": ctypes.c_char_p}
+RESTYPES = {"gl_status_string": ctypes.c_char_p, "gl_last_error": ctypes.c_char_p,
+            "gl_vig_workspace_bytes": ctypes.c_size_t}
 
 _lib = None
 
@@ -139,6 +154,34 @@ def mrconv(x: torch.Tensor, idx: torch.Tensor, W: torch.Tensor, bias: torch.Tens
     return out
 
 
+def linear(x: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = None,
+           act_in: int = GL_ACT_NONE, act_out: int = GL_ACT_NONE,
+           residual: torch.Tensor | None = None, out: torch.Tensor | None = None,
+           stream=None) -> torch.Tensor:
+    """out[..., Cout] = act_out(act_in(x) W^T + bias) + residual over the last axis."""
+    K = x.shape[-1]
+    R = x.numel() // K
+    Cout = W.shape[0]
+    if out is None:
+        out = torch.empty(x.shape[:-1] + (Cout,), dtype=x.dtype, device=x.device)
+    _call("gl_linear", _p(x), R, K, _p(W), _p(bias), Cout, act_in, act_out, _p(residual), _dt(x),
+          _p(out), _s(stream))
+    return out
+
+
+def vig_params(p: dict) -> VigParams:
+    """gl_vig_params from a dict of device tensors keyed like VIG_PARAMS."""
+    return VigParams(*[(p[n].data_ptr() if p.get(n) is not None else None) for n in VIG_PARAMS])
+
+
+def vig_workspace(x0: torch.Tensor, k: int) -> torch.Tensor:
+    B, N, C = x0.shape
+    n = lib().gl_vig_workspace_bytes(B, N, C, k, _dt(x0))
+    if not n:
+        raise GraphLeapError("gl_vig_workspace_bytes", 2, "bad shape")
+    return torch.empty(n, dtype=torch.uint8, device=x0.device)
+
+
 # ---------------------------------------------------------------------------
 # lookahead
 # ---------------------------------------------------------------------------
@@ -198,6 +241,33 @@ class Lookahead:
         _call("gl_graphleap_block", self._h, _p(x_in), B, H, W, C, pool_r, _p(keys_ws),
               _p(idx_use), k, _p(Wt), _p(bias), _dt(x_in), _p(x_out), _p(idx_next),
               dilation_next)
+        return x_out
+
+    def vig_block(self, x_in, idx_use, params: dict, ws, u_out=None, x_out=None, idx_next=None,
+                  dilation_next=1):
+        """One full ViG block; returns (x_out, u_out)."""
+        B, N, C = x_in.shape
+        k = idx_use.shape[2]
+        x_out = torch.empty_like(x_in) if x_out is None else x_out
+        u_out = torch.empty_like(x_in) if u_out is None else u_out
+        self._keep(x_in, ws, u_out, idx_use, idx_next)
+        pp = vig_params(params)
+        _call("gl_vig_block", self._h, _p(x_in), B, N, C, k, _p(idx_use), ctypes.byref(pp),
+              _dt(x_in), _p(ws), ws.numel(), _p(u_out), _p(idx_next), dilation_next, _p(x_out))
+        return x_out, u_out
+
+    def vig_stack(self, x0, params: list, dilations, k, schedule=GL_SCHED_LOOKAHEAD_FUSED,
+                  ws=None, x_out=None):
+        """len(dilations) full ViG blocks; params: list of dicts of device tensors."""
+        B, N, C = x0.shape
+        L = len(dilations)
+        ws = vig_workspace(x0, k) if ws is None else ws
+        x_out = torch.empty_like(x0) if x_out is None else x_out
+        dil = (ctypes.c_int * L)(*dilations)
+        arr = (VigParams * L)(*[vig_params(p) for p in params])
+        self._keep(x0, ws)
+        _call("gl_vig_stack", self._h, _p(x0), B, N, C, L, k, dil, arr, _dt(x0), schedule, _p(ws),
+              ws.numel(), _p(x_out))
         return x_out
 
     def stack(self, x0, H, W, Ws, bs, dilations, k, pool_r=1, schedule=GL_SCHED_LOOKAHEAD,

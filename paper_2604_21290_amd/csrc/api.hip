@@ -129,8 +129,8 @@ struct gl_lookahead {
   hipEvent_t ev_ready, ev_built;
   bool pending;
   int prof_max;
-  int prof_n[3];                                           // builds, updates, fused
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> prof[3];
+  int prof_n[4];                                           // builds, updates, fused, linear
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> prof[4];
 };
 
 namespace {
@@ -162,7 +162,7 @@ gl_status block_ws(gl_lookahead_t h, int B, int N, int C, gl_dtype dt, int rt, v
 }
 
 void free_profiling(gl_lookahead_t h) {
-  for (int w = 0; w < 3; ++w) {
+  for (int w = 0; w < 4; ++w) {
     for (auto& p : h->prof[w]) {
       (void)hipEventDestroy(p.first);
       (void)hipEventDestroy(p.second);
@@ -366,7 +366,7 @@ gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_look
   h->ws_bytes = 0;
   h->pending = false;
   h->prof_max = 0;
-  h->prof_n[0] = h->prof_n[1] = h->prof_n[2] = 0;
+  h->prof_n[0] = h->prof_n[1] = h->prof_n[2] = h->prof_n[3] = 0;
   hipError_t e = hipEventCreateWithFlags(&h->ev_ready, hipEventDisableTiming);
   if (e != hipSuccess) {
     delete h;
@@ -401,7 +401,7 @@ gl_status gl_lookahead_set_profiling(gl_lookahead_t h, int max_records) {
   if (max_records < 0 || max_records > 1 << 20)
     return fail(GL_ERR_BAD_SHAPE, "set_profiling: max_records=%d", max_records);
   free_profiling(h);
-  for (int w = 0; w < 3; ++w) {
+  for (int w = 0; w < 4; ++w) {
     for (int i = 0; i < max_records; ++i) {
       hipEvent_t a, b;
       hipError_t e = hipEventCreate(&a);
@@ -424,7 +424,7 @@ gl_status gl_lookahead_set_profiling(gl_lookahead_t h, int max_records) {
 gl_status gl_lookahead_kernel_times(gl_lookahead_t h, int which, float* ms_out, int cap,
                                     int* n_out) {
   if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "kernel_times: bad handle");
-  if (which != GL_TIME_BUILD && which != GL_TIME_UPDATE && which != GL_TIME_FUSED)
+  if (which < GL_TIME_BUILD || which > GL_TIME_LINEAR)
     return fail(GL_ERR_UNSUPPORTED, "kernel_times: which=%d", which);
   if (!n_out || (cap > 0 && !ms_out)) return fail(GL_ERR_NULL_PTR, "kernel_times: null output");
   const int n = h->prof_n[which] < cap ? h->prof_n[which] : cap;
@@ -633,6 +633,289 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
     cur = next;
   }
   return GL_OK;
+}
+
+}  // extern "C"
+
+// ===========================================================================
+// The full ViG block (Sec. III Eq. 11-15, Alg. 1)
+// ===========================================================================
+namespace {
+
+gl_status check_linear(const void* x, int R, int K, const void* W, const void* bias, int Cout,
+                       gl_act act_in, gl_act act_out, const void* residual, gl_dtype dt,
+                       const void* out) {
+  if (!x || !W || !out) return fail(GL_ERR_NULL_PTR, "linear: x, W and out are required");
+  if (!dtype_ok(dt)) return fail(GL_ERR_UNSUPPORTED, "linear: unknown dtype %d", (int)dt);
+  if ((act_in != GL_ACT_NONE && act_in != GL_ACT_GELU) ||
+      (act_out != GL_ACT_NONE && act_out != GL_ACT_GELU))
+    return fail(GL_ERR_UNSUPPORTED, "linear: unknown activation");
+  if (R < 1 || K < 1 || Cout < 1 || !size_ok(R, 1, K) || !size_ok(R, 1, Cout) ||
+      !size_ok(Cout, 1, K))
+    return fail(GL_ERR_BAD_SHAPE, "linear: bad shape R=%d K=%d Cout=%d", R, K, Cout);
+  if (K % vec_width(dt))
+    return fail(GL_ERR_UNSUPPORTED, "linear: K=%d must be a multiple of %d", K, vec_width(dt));
+  const size_t es = esize(dt);
+  if (!aligned(x, 16) || !aligned(W, 16) || !aligned(out, es) || (bias && !aligned(bias, es)) ||
+      (residual && !aligned(residual, es)))
+    return fail(GL_ERR_ALIGNMENT, "linear: x and W need 16-byte alignment");
+  const size_t ob = (size_t)R * Cout * es;
+  if (overlap(out, ob, x, (size_t)R * K * es) || overlap(out, ob, W, (size_t)Cout * K * es) ||
+      overlap(out, ob, bias, bias ? (size_t)Cout * es : 0) ||
+      (residual && residual != out && overlap(out, ob, residual, ob)))
+    return fail(GL_ERR_ALIAS, "linear: out overlaps an input");
+  return GL_OK;
+}
+
+hipError_t run_linear(const void* x, int R, int K, const void* W, const void* bias, int Cout,
+                      int act_in, int act_out, const void* residual, gl_dtype dt, void* out,
+                      hipStream_t stream, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
+  gl::GemmArgs a;
+  a.A = x;
+  a.W = W;
+  a.bias = bias;
+  a.residual = residual;
+  a.out = out;
+  a.R = R;
+  a.K = K;
+  a.Cout = Cout;
+  a.act_in = act_in;
+  a.act_out = act_out;
+  return gl::launch_gemm_nt(a, dt == GL_BF16, stream, e0, e1);
+}
+
+size_t round256(size_t v) { return (v + 255) & ~size_t(255); }
+
+// Workspace carve-up: sigma-input Ut, Y, FFN hidden H (block and stack), then
+// U, two feature buffers and two graphs (stack only).
+struct VigWs {
+  char* ut;
+  char* y;
+  char* hid;
+  char* u;
+  char* x[2];
+  int32_t* idx[2];
+  size_t bytes;
+};
+
+size_t vig_ws_bytes(int B, int N, int C, int k, gl_dtype dt) {
+  const size_t fb = round256((size_t)B * N * C * esize(dt));
+  return 10 * fb + 2 * round256((size_t)B * N * k * 4);
+}
+
+VigWs vig_ws(void* base, int B, int N, int C, int k, gl_dtype dt) {
+  const size_t fb = round256((size_t)B * N * C * esize(dt));
+  const size_t ib = round256((size_t)B * N * k * 4);
+  char* p = static_cast<char*>(base);
+  VigWs w;
+  w.ut = p;
+  w.y = p + fb;
+  w.hid = p + 2 * fb;     // 4 feature buffers: [B, N, 4C]
+  w.u = p + 6 * fb;
+  w.x[0] = p + 7 * fb;
+  w.x[1] = p + 8 * fb;
+  w.idx[0] = reinterpret_cast<int32_t*>(p + 10 * fb);
+  w.idx[1] = reinterpret_cast<int32_t*>(p + 10 * fb + ib);
+  w.bytes = vig_ws_bytes(B, N, C, k, dt);
+  return w;
+}
+
+gl_status check_vig_params(const gl_vig_params* p, int C, gl_dtype dt) {
+  if (!p) return fail(GL_ERR_NULL_PTR, "vig: params is NULL");
+  if (!p->W_in || !p->W_upd || !p->W_out || !p->W_1 || !p->W_2)
+    return fail(GL_ERR_NULL_PTR, "vig: every weight matrix is required");
+  const size_t es = esize(dt);
+  const void* mats[5] = {p->W_in, p->W_upd, p->W_out, p->W_1, p->W_2};
+  const void* bs[5] = {p->b_in, p->b_upd, p->b_out, p->b_1, p->b_2};
+  for (int i = 0; i < 5; ++i) {
+    if (!aligned(mats[i], 16) || (bs[i] && !aligned(bs[i], es)))
+      return fail(GL_ERR_ALIGNMENT, "vig: weights need 16-byte alignment");
+  }
+  (void)C;
+  return GL_OK;
+}
+
+// One full block on the handle's streams.  u holds U^l (computed here unless
+// u_ready); idx_next (if any) receives G(U^l, dil_next).
+gl_status enqueue_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, int C, int k,
+                            const int32_t* idx_use, const gl_vig_params& p, gl_dtype dt,
+                            const VigWs& w, void* u, bool u_ready, int32_t* idx_next,
+                            int dil_next, gl_schedule schedule, int rt, void* x_out) {
+  const int R = B * N, dtb = dt == GL_BF16;
+  gl_status s;
+  auto lin = [&](const char* what, const void* xi, int K, const void* W, const void* b, int Co,
+                 int ai, int ao, const void* res, void* o) {
+    return timed_launch(h, GL_TIME_LINEAR, what, [&](hipEvent_t e0, hipEvent_t e1) {
+      return run_linear(xi, R, K, W, b, Co, ai, ao, res, dt, o, h->su, e0, e1);
+    });
+  };
+  if (schedule == GL_SCHED_LOOKAHEAD && (s = join_build(h)) != GL_OK) return s;
+  if (!u_ready && (s = lin("linear launch (FC1)", x_in, C, p.W_in, p.b_in, C, 0, 0, nullptr, u)) != GL_OK)
+    return s;
+  void* mws;
+  if ((s = block_ws(h, B, N, C, dt, rt, &mws)) != GL_OK) return s;
+  const bool fused = schedule == GL_SCHED_LOOKAHEAD_FUSED && idx_next &&
+                     !gl::knn_use_stream(N, C, dtb) && !mws;
+  if (fused) {
+    const gl::KnnArgs ka = gl::make_knn_args(u, u, B, N, C, N, k, dil_next, idx_next);
+    const gl::MrArgs ma = gl::make_mr_args(u, u, idx_use, p.W_upd, p.b_upd, w.ut, B, N, N, C, C, k);
+    s = timed_launch(h, GL_TIME_FUSED, "block launch", [&](hipEvent_t e0, hipEvent_t e1) {
+      return gl::launch_block(ka, ma, dtb, rt, h->su, e0, e1);
+    });
+    if (s != GL_OK) return s;
+  } else {
+    if (idx_next) {
+      if (schedule == GL_SCHED_LOOKAHEAD) {
+        if ((s = fork_build(h)) != GL_OK) return s;
+        if ((s = enqueue_build(h, u, B, N, C, nullptr, N, k, dil_next, dt, idx_next)) != GL_OK)
+          return s;
+        if ((s = mark_built(h)) != GL_OK) return s;
+      } else {
+        s = timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
+          return gl::launch_knn(u, u, B, N, C, N, k, dil_next, dtb, idx_next, h->su, e0, e1);
+        });
+        if (s != GL_OK) return s;
+      }
+    }
+    s = timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {
+      return gl::launch_mrconv(u, u, idx_use, p.W_upd, p.b_upd, w.ut, B, N, N, C, C, k, dtb, rt,
+                               mws, h->su, e0, e1);
+    });
+    if (s != GL_OK) return s;
+  }
+  if ((s = lin("linear launch (FC2)", w.ut, C, p.W_out, p.b_out, C, 1, 0, x_in, w.y)) != GL_OK)
+    return s;
+  if ((s = lin("linear launch (FFN1)", w.y, C, p.W_1, p.b_1, 4 * C, 0, 1, nullptr, w.hid)) != GL_OK)
+    return s;
+  return lin("linear launch (FFN2)", w.hid, 4 * C, p.W_2, p.b_2, C, 0, 0, w.y, x_out);
+}
+
+}  // namespace
+
+extern "C" {
+
+gl_status gl_linear(const void* x, int R, int K, const void* W, const void* bias, int Cout,
+                    gl_act act_in, gl_act act_out, const void* residual, gl_dtype dt,
+                    void* out, hipStream_t stream) {
+  gl_status s = check_linear(x, R, K, W, bias, Cout, act_in, act_out, residual, dt, out);
+  if (s != GL_OK) return s;
+  hipError_t e = run_linear(x, R, K, W, bias, Cout, act_in, act_out, residual, dt, out, stream);
+  return e == hipSuccess ? GL_OK : hip_fail(e, "linear launch");
+}
+
+size_t gl_vig_workspace_bytes(int B, int N, int C, int k, gl_dtype dt) {
+  if (B < 1 || N < 1 || C < 1 || k < 1 || !dtype_ok(dt)) return 0;
+  return vig_ws_bytes(B, N, C, k, dt);
+}
+
+gl_status gl_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, int C, int k,
+                       const int32_t* idx_use, const gl_vig_params* p, gl_dtype dt, void* ws,
+                       size_t ws_bytes, void* u_out, int32_t* idx_next, int dilation_next,
+                       void* x_out) {
+  if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "vig_block: bad handle");
+  gl_status s;
+  if ((s = check_vig_params(p, C, dt)) != GL_OK) return s;
+  if (!x_in || !idx_use || !ws || !u_out || !x_out)
+    return fail(GL_ERR_NULL_PTR, "vig_block: x_in, idx_use, ws, u_out and x_out are required");
+  int rt = 0;
+  // shapes of every layer: FC1 [C->C], MRConv [2C->C], FC2 [C->C], FFN [C->4C->C]
+  if ((s = check_mrconv(u_out, B, N, C, nullptr, N, idx_use, k, p->W_upd, p->b_upd, C, dt, x_out,
+                        &rt)) != GL_OK)
+    return s;
+  if (idx_next && (s = check_knn(u_out, B, N, C, nullptr, N, k, dilation_next, dt, idx_next)) != GL_OK)
+    return s;
+  const VigWs w = vig_ws(ws, B, N, C, k, dt);
+  if (ws_bytes < w.bytes)
+    return fail(GL_ERR_BAD_SHAPE, "vig_block: ws_bytes=%zu < %zu", ws_bytes, w.bytes);
+  const size_t xb = (size_t)B * N * C * esize(dt), ib = (size_t)B * N * k * 4;
+  if (!aligned(x_in, 16) || !aligned(u_out, 16) || !aligned(ws, 256) || !aligned(x_out, 16))
+    return fail(GL_ERR_ALIGNMENT, "vig_block: x_in, u_out, x_out need 16 bytes, ws 256");
+  if (overlap(x_out, xb, x_in, xb) || overlap(x_out, xb, u_out, xb) ||
+      overlap(x_out, xb, ws, ws_bytes) || overlap(x_out, xb, idx_use, ib) ||
+      overlap(x_out, xb, idx_next, idx_next ? ib : 0) || overlap(u_out, xb, x_in, xb) ||
+      overlap(u_out, xb, ws, ws_bytes) || overlap(x_in, xb, ws, ws_bytes) ||
+      overlap(idx_use, ib, ws, ws_bytes) || overlap(idx_next, idx_next ? ib : 0, ws, ws_bytes) ||
+      overlap(idx_next, idx_next ? ib : 0, idx_use, ib))
+    return fail(GL_ERR_ALIAS, "vig_block: buffers overlap");
+  return enqueue_vig_block(h, x_in, B, N, C, k, idx_use, *p, dt, w, u_out, false, idx_next,
+                           dilation_next, GL_SCHED_LOOKAHEAD, rt, x_out);
+}
+
+gl_status gl_vig_stack(gl_lookahead_t h, const void* x0, int B, int N, int C, int L, int k,
+                       const int* dilations, const gl_vig_params* params, gl_dtype dt,
+                       gl_schedule schedule, void* ws, size_t ws_bytes, void* x_out) {
+  if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "vig_stack: bad handle");
+  if (!x0 || !dilations || !params || !ws || !x_out)
+    return fail(GL_ERR_NULL_PTR, "vig_stack: x0, dilations, params, ws and x_out are required");
+  if (L < 1) return fail(GL_ERR_BAD_SHAPE, "vig_stack: L=%d", L);
+  if (schedule != GL_SCHED_LOOKAHEAD && schedule != GL_SCHED_STANDARD &&
+      schedule != GL_SCHED_LOOKAHEAD_FUSED)
+    return fail(GL_ERR_UNSUPPORTED, "vig_stack: schedule=%d", (int)schedule);
+  const VigWs w = vig_ws(ws, B, N, C, k, dt);
+  if (ws_bytes < w.bytes)
+    return fail(GL_ERR_BAD_SHAPE, "vig_stack: ws_bytes=%zu < %zu", ws_bytes, w.bytes);
+  if (!aligned(x0, 16) || !aligned(x_out, 16) || !aligned(ws, 256))
+    return fail(GL_ERR_ALIGNMENT, "vig_stack: x0, x_out need 16 bytes, ws 256");
+  const size_t xb = (size_t)B * N * C * esize(dt);
+  if (overlap(x_out, xb, x0, xb) || overlap(x_out, xb, ws, ws_bytes) || overlap(x0, xb, ws, ws_bytes))
+    return fail(GL_ERR_ALIAS, "vig_stack: x_out, x0 and ws must not overlap");
+  gl_status s;
+  int rt = 0;
+  for (int l = 0; l < L; ++l) {
+    if ((s = check_vig_params(&params[l], C, dt)) != GL_OK) return s;
+    if ((s = check_knn(w.u, B, N, C, nullptr, N, k, dilations[l], dt, w.idx[0])) != GL_OK) return s;
+    if ((s = check_mrconv(w.u, B, N, C, nullptr, N, w.idx[0], k, params[l].W_upd, params[l].b_upd,
+                          C, dt, w.ut, &rt)) != GL_OK)
+      return s;
+  }
+  const int dtb = dt == GL_BF16;
+  if ((s = join_build(h)) != GL_OK) return s;
+  if (schedule == GL_SCHED_STANDARD) {
+    for (int l = 0; l < L; ++l) {
+      const void* xi = l == 0 ? x0 : w.x[(l - 1) & 1];
+      void* xo = l == L - 1 ? x_out : w.x[l & 1];
+      if ((s = timed_launch(h, GL_TIME_LINEAR, "linear launch (FC1)", [&](hipEvent_t e0, hipEvent_t e1) {
+             return run_linear(xi, B * N, C, params[l].W_in, params[l].b_in, C, 0, 0, nullptr, dt,
+                               w.u, h->su, e0, e1);
+           })) != GL_OK)
+        return s;
+      if ((s = timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
+             return gl::launch_knn(w.u, w.u, B, N, C, N, k, dilations[l], dtb, w.idx[0], h->su, e0,
+                                   e1);
+           })) != GL_OK)
+        return s;
+      if ((s = enqueue_vig_block(h, xi, B, N, C, k, w.idx[0], params[l], dt, w, w.u, true, nullptr,
+                                 0, schedule, rt, xo)) != GL_OK)
+        return s;
+    }
+    return GL_OK;
+  }
+  // lookahead: U^0, then Ghat^0 = G(U^0, d_0)
+  if ((s = timed_launch(h, GL_TIME_LINEAR, "linear launch (FC1)", [&](hipEvent_t e0, hipEvent_t e1) {
+         return run_linear(x0, B * N, C, params[0].W_in, params[0].b_in, C, 0, 0, nullptr, dt, w.u,
+                           h->su, e0, e1);
+       })) != GL_OK)
+    return s;
+  if ((s = timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
+         return gl::launch_knn(w.u, w.u, B, N, C, N, k, dilations[0], dtb, w.idx[0], h->su, e0, e1);
+       })) != GL_OK)
+    return s;
+  int cur = 0;
+  for (int l = 0; l < L; ++l) {
+    const void* xi = l == 0 ? x0 : w.x[(l - 1) & 1];
+    void* xo = l == L - 1 ? x_out : w.x[l & 1];
+    int next = cur;
+    int32_t* idx_next = nullptr;
+    if (l + 1 < L && !(l == 0 && dilations[1] == dilations[0])) {
+      next = 1 - cur;
+      idx_next = w.idx[next];
+    }
+    if ((s = enqueue_vig_block(h, xi, B, N, C, k, w.idx[cur], params[l], dt, w, w.u, l == 0,
+                               idx_next, idx_next ? dilations[l + 1] : 0, schedule, rt, xo)) != GL_OK)
+      return s;
+    cur = next;
+  }
+  return join_build(h);
 }
 
 }  // extern "C"

@@ -1,12 +1,14 @@
-// FC update as a tiled MFMA GEMM over materialised node features, for wide
-// channels (Sec. II-A Eq. 3; the W_x / W_m split of Sec. IV-C2 is the two
-// halves of the contraction axis).
-//
-//   out[R, Cout] = A[R, K] W[Cout, K]^T + b,   A = [x | m] (K = 2C)
-//
-// When 2C is wide, the fused MRConv tile would stream all of W through every
-// 16- or 32-node workgroup.  Here a workgroup owns a 128 x 128 output tile, so
-// W is read once per 128 nodes and A once per 128 output channels.
+// Tiled MFMA GEMM for the fully connected layers of the path:
+//   out[R, Cout] = act_out(act_in(A)[R, K] W[Cout, K]^T + b) + residual
+//   * the MRConv update over materialised [x | m] rows for wide channels
+//     (Sec. II-A Eq. 3; the W_x / W_m split of Sec. IV-C2 is the two halves of
+//     the contraction axis), where the fused MRConv tile would stream all of W
+//     through every 16- or 32-node workgroup;
+//   * FC1, FC2 + residual and the FFN of the full ViG block (Eq. 11, 14, 15):
+//     act_in = GELU gives sigma(U~) W_out^T, act_out = GELU the FFN's hidden
+//     layer, residual the two skip connections.
+// A workgroup owns a 128 x 128 output tile, so W is read once per 128 rows
+// and A once per 128 output channels.
 //   - 4 waves in a 2 x 2 layout; each wave holds a 64 x 64 accumulator block
 //     (4 x 4 MFMA tiles of 16 x 16) in registers.
 //   - The contraction runs in steps of 64 bytes per row (32 bf16 or 16 fp32
@@ -15,7 +17,9 @@
 //     (128 rows x 64 bytes each) pass through LDS, double-buffered: the
 //     global loads of step s+1 are in flight while step s is multiplied, and
 //     one barrier per step separates the buffers.
-//   - Epilogue: + bias in fp32, rounded once to the storage type.
+//   - act_in is applied to A's elements as they are staged (fp32, rounded back
+//     to the storage type, as if the caller had stored sigma(A)).
+//   - Epilogue in fp32: + bias, act_out, + residual, rounded once.
 #include "gl_device.h"
 #include "gl_kernels.h"
 
@@ -28,7 +32,25 @@ constexpr int kGmTile = kGmBM * kGmRow;    // one operand tile: 10 KB
 
 size_t gemm_smem_bytes() { return (size_t)4 * kGmTile; }
 
+// GELU of the 16-byte vector's elements, rounded back to the storage type.
 template <int DT>
+__device__ __forceinline__ u32x4 gelu_vec(u32x4 v) {
+  if (DT) {
+    float f[8];
+    unpack_bf16x8(__builtin_bit_cast(uint4, v), f);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) f[i] = gelu_f32(f[i]);
+    return __builtin_bit_cast(u32x4, pack_bf16x8(f));
+  }
+  float4 f = __builtin_bit_cast(float4, v);
+  f.x = gelu_f32(f.x);
+  f.y = gelu_f32(f.y);
+  f.z = gelu_f32(f.z);
+  f.w = gelu_f32(f.w);
+  return __builtin_bit_cast(u32x4, f);
+}
+
+template <int DT, int ACT_IN, int ACT_OUT>
 __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
   extern __shared__ __align__(16) char smem[];
   constexpr int ES = DT ? 2 : 4;
@@ -68,6 +90,12 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
       if (!in) ra[i] = rb[i] = u32x4{0, 0, 0, 0};
     }
   };
+  auto act = [&]() {
+    if (ACT_IN) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) ra[i] = gelu_vec<DT>(ra[i]);
+    }
+  };
   auto sstore = [&](int buf) {
     char* sa = smem + buf * 2 * kGmTile;
 #pragma unroll
@@ -84,6 +112,7 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   gload(0);
+  act();
   sstore(0);
   __syncthreads();
   for (int s = 0; s < nsteps; ++s) {
@@ -110,7 +139,10 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
           acc[i][j] = mfma_f32(x4.w, y4.w, acc[i][j]);
         }
       }
-    if (s + 1 < nsteps) sstore((s + 1) & 1);
+    if (s + 1 < nsteps) {
+      act();
+      sstore((s + 1) & 1);
+    }
     __syncthreads();
   }
 
@@ -130,9 +162,15 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
       for (int v = 0; v < 4; ++v) {
         const int row = m0 + wm * 64 + i * 16 + 4 * g + v;
         if (row >= R) continue;
-        const float y = acc[i][j][v] + bn;
-        if (DT) static_cast<uint16_t*>(a.out)[(size_t)row * Cout + n] = (uint16_t)f32_to_bf16_bits(y);
-        else static_cast<float*>(a.out)[(size_t)row * Cout + n] = y;
+        float y = acc[i][j][v] + bn;
+        if (ACT_OUT) y = gelu_f32(y);
+        const size_t o = (size_t)row * Cout + n;
+        if (a.residual) {
+          y += DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(a.residual)[o])
+                  : static_cast<const float*>(a.residual)[o];
+        }
+        if (DT) static_cast<uint16_t*>(a.out)[o] = (uint16_t)f32_to_bf16_bits(y);
+        else static_cast<float*>(a.out)[o] = y;
       }
   }
 }
@@ -141,7 +179,13 @@ hipError_t launch_gemm_nt(const GemmArgs& a, int dt_bf16, hipStream_t stream, hi
                           hipEvent_t ev1) {
   const int nm = (a.R + kGmBM - 1) / kGmBM, nn = (a.Cout + kGmBN - 1) / kGmBN;
   const dim3 grid(nm * nn), block(kGmThreads);
-  const void* fn = dt_bf16 ? (const void*)&gemm_nt_kernel<1> : (const void*)&gemm_nt_kernel<0>;
+  const int v = (dt_bf16 ? 4 : 0) + (a.act_in ? 2 : 0) + (a.act_out ? 1 : 0);
+  static const void* const fns[8] = {
+      (const void*)&gemm_nt_kernel<0, 0, 0>, (const void*)&gemm_nt_kernel<0, 0, 1>,
+      (const void*)&gemm_nt_kernel<0, 1, 0>, (const void*)&gemm_nt_kernel<0, 1, 1>,
+      (const void*)&gemm_nt_kernel<1, 0, 0>, (const void*)&gemm_nt_kernel<1, 0, 1>,
+      (const void*)&gemm_nt_kernel<1, 1, 0>, (const void*)&gemm_nt_kernel<1, 1, 1>};
+  const void* fn = fns[v];
   return launch_with_smem(fn, grid, block, gemm_smem_bytes(), stream, ev0, ev1, a);
 }
 

@@ -107,6 +107,11 @@ __device__ __forceinline__ float sumsq_f32x4(const uint4& v, float acc) {
   return fmaf(f.x, f.x, fmaf(f.y, f.y, fmaf(f.z, f.z, fmaf(f.w, f.w, acc))));
 }
 
+// Exact GELU x * Phi(x) = x/2 (1 + erf(x / sqrt 2)), with the device erff.
+__device__ __forceinline__ float gelu_f32(float x) {
+  return 0.5f * x * (1.f + erff(x * 0.70710678118654752f));
+}
+
 // 1 / max(||k||, 1e-12) from the squared norm, with the hardware reciprocal
 // square root (about 1 ulp); both kNN kernels use it for their key rows.
 __device__ __forceinline__ float key_rnorm(float ss) {

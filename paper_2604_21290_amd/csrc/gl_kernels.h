@@ -31,11 +31,13 @@ struct MrArgs {
 };
 
 struct GemmArgs {
-  const void* A;      // [R, K], K contiguous
-  const void* W;      // [Cout, K], K contiguous
-  const void* bias;   // [Cout] or null
-  void* out;          // [R, Cout]
+  const void* A;         // [R, K], K contiguous
+  const void* W;         // [Cout, K], K contiguous
+  const void* bias;      // [Cout] or null
+  const void* residual;  // [R, Cout] or null (may be `out` itself)
+  void* out;             // [R, Cout]
   int R, K, Cout;
+  int act_in, act_out;   // 0 none, 1 GELU (on A's elements / on the pre-residual output)
 };
 
 // Workgroups are dispatched round-robin over the 8 XCDs (workgroup id mod 8).

@@ -96,10 +96,12 @@ hipError_t launch_mrconv(const void* x, const void* keys, const int32_t* idx, co
     ga.A = split_ws;
     ga.W = W;
     ga.bias = bias;
+    ga.residual = nullptr;
     ga.out = out;
     ga.R = a.R;
     ga.K = 2 * C;
     ga.Cout = Cout;
+    ga.act_in = ga.act_out = 0;
     return launch_gemm_nt(ga, dt_bf16, stream, nullptr, ev1);
   }
   const int TM = 16 * rt;

@@ -27,7 +27,8 @@ P = lambda i: ctypes.c_void_p(A * (i + 1))  # noqa: E731
 
 def header_functions():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:gl_status|const char\*|int)\s+(gl_\w+)\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:gl_status|const char\*|int|size_t)\s+(gl_\w+)\(", text,
+                                 re.M)))
 
 
 def test_exports_every_declared_symbol():
@@ -128,3 +129,32 @@ def test_status_strings():
     for code, name in api.STATUS.items():
         assert L.gl_status_string(code).decode() == name
     assert L.gl_status_string(99).decode() == "GL_ERR_UNKNOWN"
+
+
+def _lin(x=P(0), R=64, K=64, W=P(10), b=None, Co=64, ai=0, ao=0, res=None, dt=1, out=P(20)):
+    st = api.lib().gl_linear(x, R, K, W, b, Co, ai, ao, res, dt, out, None)
+    return api.STATUS[st]
+
+
+@host_only
+def test_linear_validation():
+    assert _lin(x=None) == "GL_ERR_NULL_PTR"
+    assert _lin(W=None) == "GL_ERR_NULL_PTR"
+    assert _lin(ai=2) == "GL_ERR_UNSUPPORTED"
+    assert _lin(dt=3) == "GL_ERR_UNSUPPORTED"
+    assert _lin(R=0) == "GL_ERR_BAD_SHAPE"
+    assert _lin(K=12) == "GL_ERR_UNSUPPORTED"               # bf16 rows need K % 8 == 0
+    assert _lin(x=ctypes.c_void_p(A + 8)) == "GL_ERR_ALIGNMENT"
+    assert _lin(out=P(0)) == "GL_ERR_ALIAS"                  # out on top of x
+    assert _lin(res=ctypes.c_void_p(A * 21 + 64)) == "GL_ERR_ALIAS"   # partial overlap with out
+
+
+@host_only
+def test_vig_validation():
+    L = api.lib()
+    assert L.gl_vig_workspace_bytes(2, 196, 192, 9, 1) > 0
+    assert L.gl_vig_workspace_bytes(0, 196, 192, 9, 1) == 0
+    pp = api.VigParams()
+    st = L.gl_vig_stack(None, P(0), 2, 196, 192, 2, 9, (ctypes.c_int * 2)(1, 1),
+                        ctypes.byref(pp), 1, 2, P(5), 1 << 30, P(9))
+    assert api.STATUS[st] == "GL_ERR_BAD_HANDLE"

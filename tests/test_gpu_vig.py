@@ -1,0 +1,211 @@
+"""GPU parity of the full GraphLeap ViG block (gl_linear, gl_vig_block,
+gl_vig_stack) against the CPU oracle (Eq. 11-15, Alg. 1).
+
+Blocks are teacher-forced: each block's projected features U, the graph built
+from them and its output are checked against the oracle evaluated on the exact
+stored tensors the GPU saw; the stack entry must then reproduce the
+block-by-block run bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from gpu_helpers import check_close, check_idx, from_dev, require_gpu, to_dev
+from paper_2604_21290_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[gpu-test]", *a, flush=True)
+
+
+def _dev_params(p: dict) -> dict:
+    return {n: to_dev(v) for n, v in p.items()}
+
+
+def _host_params(p: dict) -> dict:
+    return {n: v.value for n, v in p.items()}
+
+
+# -- gl_linear --------------------------------------------------------------------
+LIN = [
+    # label, R, K, Cout, act_in, act_out, residual, bias, dtype
+    ("fc1_vig_ti", 6272, 192, 192, 0, 0, False, True, I.BF16),
+    ("fc2_gelu_in_residual", 1000, 192, 192, 1, 0, True, True, I.BF16),
+    ("ffn1_gelu_out", 777, 192, 768, 0, 1, False, True, I.BF16),
+    ("ffn2_residual", 777, 768, 192, 0, 0, True, False, I.BF16),
+    ("ragged_k_tail", 131, 40, 70, 1, 1, True, True, I.BF16),
+    ("fp32_all", 257, 36, 130, 1, 1, True, True, I.F32),
+    ("one_row", 1, 8, 1, 0, 0, False, False, I.BF16),
+]
+
+
+@pytest.mark.parametrize("case", LIN, ids=[c[0] for c in LIN])
+def test_linear_parity(case):
+    require_gpu()
+    from paper_2604_21290_amd import api
+    label, R, K, Co, ai, ao, with_res, with_bias, dt = case
+    g = np.random.default_rng(R + 7 * K + Co)
+    x = I.store(g.standard_normal((R, K)), dt)
+    W = I.store(g.uniform(-1, 1, (Co, K)) / np.sqrt(K), dt)
+    b = I.store(g.uniform(-0.5, 0.5, Co), dt) if with_bias else None
+    r = I.store(g.standard_normal((R, Co)), dt) if with_res else None
+    _say("linear", label)
+    out = api.linear(to_dev(x), to_dev(W), None if b is None else to_dev(b), ai, ao,
+                     None if r is None else to_dev(r))
+    torch.cuda.synchronize()
+    xa = O.gelu_ref(x.value) if ai else x.value
+    ref = O.linear_ref(xa, W.value, None if b is None else b.value)
+    if ao:
+        ref = O.gelu_ref(ref)
+    if r is not None:
+        ref = ref + r.value
+    check_close(from_dev(out).value, ref, dt, label)
+
+
+def test_linear_residual_in_place():
+    require_gpu()
+    from paper_2604_21290_amd import api
+    g = np.random.default_rng(5)
+    x = I.store(g.standard_normal((300, 64)), I.BF16)
+    W = I.store(g.uniform(-0.2, 0.2, (64, 64)), I.BF16)
+    r = I.store(g.standard_normal((300, 64)), I.BF16)
+    rd = to_dev(r)
+    out = api.linear(to_dev(x), to_dev(W), residual=rd, out=rd)
+    torch.cuda.synchronize()
+    assert out.data_ptr() == rd.data_ptr()
+    check_close(from_dev(out).value, O.linear_ref(x.value, W.value) + r.value, I.BF16, "in place")
+
+
+# -- full blocks ------------------------------------------------------------------
+def _workload(name, B):
+    w = I.with_batch(I.WORKLOADS[name], B)
+    return w
+
+
+def _run_blocks(w, L, x0d, params_d, same_stream=False):
+    """Drive L full blocks through gl_vig_block; return xs, us, graphs used."""
+    from paper_2604_21290_amd import api
+    B, N, C = x0d.shape
+    dil = w.dilations
+    s_up = torch.cuda.current_stream()
+    la = api.Lookahead(s_up, s_up if same_stream else torch.cuda.Stream())
+    ws = api.vig_workspace(x0d, w.k)
+    bufs = [torch.empty((B, N, w.k), dtype=torch.int32, device="cuda") for _ in range(2)]
+    u0 = api.linear(x0d, params_d[0]["W_in"], params_d[0].get("b_in"))
+    api.knn_graph(u0, w.k, dil[0], out=bufs[0])
+    xs, us, graphs, cur = [x0d], [], [], 0
+    for l in range(L):
+        idx_next, nxt = None, cur
+        if l + 1 < L and not (l == 0 and dil[1] == dil[0]):
+            nxt = 1 - cur
+            idx_next = bufs[nxt]
+        torch.cuda.synchronize()
+        graphs.append(bufs[cur].clone())
+        x_out, u_out = la.vig_block(xs[-1], bufs[cur], params_d[l], ws, idx_next=idx_next,
+                                    dilation_next=dil[l + 1] if idx_next is not None else 1)
+        torch.cuda.synchronize()
+        us.append(u_out.clone())
+        xs.append(x_out)
+        cur = nxt
+    torch.cuda.synchronize()
+    la.close()
+    return xs, us, graphs
+
+
+@pytest.mark.parametrize("name,B,L", [("vig_ti", 4, 6), ("vig_b", 2, 5), ("single", 1, 1)])
+def test_vig_blocks_teacher_forced(name, B, L):
+    require_gpu()
+    w = _workload(name, B)
+    x0 = I.make_features(w)
+    ps = [I.make_vig_params(w, l) for l in range(L)]
+    pd = [_dev_params(p) for p in ps]
+    ph = [_host_params(p) for p in ps]
+    _say("vig blocks", name, "B", B, "L", L)
+    xs, us, graphs = _run_blocks(w, L, to_dev(x0), pd)
+    hx = [from_dev(x).value for x in xs]
+    hu = [from_dev(u).value for u in us]
+    for l in range(L):
+        # U^l = X^l W_in^T + b_in on the stored X^l
+        check_close(hu[l], O.linear_ref(hx[l], ph[l]["W_in"], ph[l]["b_in"]), w.dtype,
+                    f"{name} U^{l}")
+        # the graph used by block l: G(U^0) for l <= 1, else G(U^(l-1)), on stored U
+        src = hu[0] if l == 0 else hu[l - 1]
+        g = graphs[l].cpu().numpy()
+        check_idx(g, O.knn_distances(src), w.k, w.dilations[l], label=f"{name} graph {l}")
+        # X^(l+1) from the stored X^l and the GPU's graph
+        ref = O.vig_block_ref(hx[l], g, ph[l])
+        rel = check_close(hx[l + 1], ref, w.dtype, f"{name} block {l}")
+        _say(name, "block", l, "rel", rel)
+
+
+@pytest.mark.parametrize("name,B,L", [("vig_ti", 4, 6), ("vig_b", 2, 5)])
+def test_vig_stack_matches_blocks(name, B, L):
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = _workload(name, B)
+    x0d = to_dev(I.make_features(w))
+    pd = [_dev_params(I.make_vig_params(w, l)) for l in range(L)]
+    dil = list(w.dilations[:L])
+    xs, _, _ = _run_blocks(w, L, x0d, pd)
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    outs = {}
+    for name_s, sc in (("fused", api.GL_SCHED_LOOKAHEAD_FUSED), ("two_stream", api.GL_SCHED_LOOKAHEAD)):
+        _say("vig stack", name, name_s)
+        outs[name_s] = la.vig_stack(x0d, pd, dil, w.k, schedule=sc)
+    torch.cuda.synchronize()
+    la.close()
+    for k_, v in outs.items():
+        assert torch.equal(v, xs[-1]), f"{name}: stack ({k_}) differs from block-by-block"
+
+
+def test_vig_standard_schedule_teacher_forced():
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = _workload("vig_ti", 2)
+    L = 3
+    x0d = to_dev(I.make_features(w))
+    ps = [I.make_vig_params(w, l) for l in range(L)]
+    pd = [_dev_params(p) for p in ps]
+    dil = list(w.dilations[:L])
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.current_stream())
+    ws = api.vig_workspace(x0d, w.k)
+    # block by block: graph from this block's own U
+    xs = [x0d]
+    for l in range(L):
+        u = api.linear(xs[-1], pd[l]["W_in"], pd[l]["b_in"])
+        idx = api.knn_graph(u, w.k, dil[l])
+        x_out, u_out = la.vig_block(xs[-1], idx, pd[l], ws)
+        torch.cuda.synchronize()
+        assert torch.equal(u, u_out)
+        ref = O.vig_block_ref(from_dev(xs[-1]).value, idx.cpu().numpy(), _host_params(ps[l]))
+        check_close(from_dev(x_out).value, ref, w.dtype, f"standard block {l}")
+        check_idx(idx.cpu().numpy(), O.knn_distances(from_dev(u).value), w.k, dil[l],
+                  label=f"standard graph {l}")
+        xs.append(x_out)
+    st = la.vig_stack(x0d, pd, dil, w.k, schedule=api.GL_SCHED_STANDARD)
+    torch.cuda.synchronize()
+    la.close()
+    assert torch.equal(st, xs[-1])
+
+
+def test_vig_zero_branches_are_identity():
+    """W_out = 0 and W_2 = 0, no biases: every schedule returns X^0 bit for bit."""
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = _workload("vig_ti", 2)
+    L = 4
+    x0d = to_dev(I.make_features(w))
+    pd = []
+    for l in range(L):
+        p = _dev_params(I.make_vig_params(w, l, bias=False))
+        p["W_out"] = torch.zeros_like(p["W_out"])
+        p["W_2"] = torch.zeros_like(p["W_2"])
+        pd.append(p)
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    for sc in (api.GL_SCHED_LOOKAHEAD_FUSED, api.GL_SCHED_LOOKAHEAD, api.GL_SCHED_STANDARD):
+        out = la.vig_stack(x0d, pd, list(w.dilations[:L]), w.k, schedule=sc)
+        torch.cuda.synchronize()
+        assert torch.equal(out, x0d), sc
+    la.close()
