@@ -17,6 +17,11 @@ the stream each kernel runs on) and the CPU oracle's rate on a bounded sample.
     python bench.py [--steps K] [--warmup W] [--workload vig_ti]
     python bench.py --only knn|mrconv|stack --steps K   (for profiler runs)
     python bench.py --only copy                          (HBM counter calibration)
+    python bench.py --only full --steps K                (full-block stack, for profiler runs)
+
+After the headline, the full GraphLeap ViG block (FC1, leap-ahead graph,
+MRConv, FC2 + residual, FFN + residual; gl_vig_stack) is timed on the same
+workload and reported under "full_block", with its own oracle sample.
 """
 from __future__ import annotations
 
@@ -109,6 +114,88 @@ def cpu_baseline(w, images: int) -> dict:
                       f"to the full batch"}
 
 
+def cpu_full_block(w, images: int, blocks: int) -> dict:
+    from threadpoolctl import threadpool_limits
+
+    import oracle as O
+    from paper_2604_21290_amd import inputs as I
+
+    S = min(images, w.B)
+    ws = I.with_batch(w, S)
+    x = I.make_features(ws)
+    ps = [{n: v.value for n, v in I.make_vig_params(ws, l).items()} for l in range(blocks)]
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        O.vig_stack_ref(x.value, ps, w.dilations[:blocks], w.k)
+        dt = time.perf_counter() - t0
+    scale = w.B / S
+    return {"value": blocks / (dt * scale), "unit": "layers/s", "cores": 1, "kind": "oracle",
+            "sample": f"oracle.vig_stack_ref (fp64, lookahead, 1 thread) on {S} of {w.B} "
+                      f"images for {blocks} blocks in {dt:.2f} s; scaled x{scale:g}"}
+
+
+def full_block(args, w, api, I, dev, torch) -> dict:
+    """Time the full ViG block stack (gl_vig_stack) under its three schedules
+    and profile its launches."""
+    B, N, C = w.B, w.N, w.C
+    L = w.L
+    x0 = dev(I.make_features(w))
+    params = [{n: dev(v) for n, v in I.make_vig_params(w, l).items()} for l in range(L)]
+    s_up = torch.cuda.current_stream()
+    la = api.Lookahead(s_up, torch.cuda.Stream())
+    ws = api.vig_workspace(x0, w.k)
+    out = torch.empty_like(x0)
+    dil = list(w.dilations)
+    steps = max(10, args.steps // 4)
+
+    def run(sc):
+        la.vig_stack(x0, params, dil, w.k, schedule=sc, ws=ws, x_out=out)
+
+    def timed(sc, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(s_up)
+        for _ in range(n):
+            run(sc)
+        e1.record(s_up)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    res = {}
+    for name, sc in (("fused", api.GL_SCHED_LOOKAHEAD_FUSED), ("lookahead", api.GL_SCHED_LOOKAHEAD),
+                     ("standard", api.GL_SCHED_STANDARD)):
+        for _ in range(max(2, args.warmup // 4)):
+            run(sc)
+        m = timed(sc, steps)
+        res[name] = {"ms_per_step": m, "layers_per_s": L / (m / 1e3)}
+    if args.only == "full":
+        la.close()
+        return {"schedules": res}
+    n_rec = steps * L * 5 + 16
+    la.set_profiling(n_rec)
+    for _ in range(steps):
+        run(api.GL_SCHED_LOOKAHEAD_FUSED)
+    torch.cuda.synchronize()
+    kern = {}
+    for key, which in (("linear", api.GL_TIME_LINEAR), ("graphleap_block", api.GL_TIME_FUSED),
+                       ("knn_graph", api.GL_TIME_BUILD), ("mrconv", api.GL_TIME_UPDATE)):
+        t = la.kernel_times_ms(which, n_rec)
+        if t:
+            kern[key] = {"launches_per_step": len(t) / steps, "avg_us": sum(t) / len(t) * 1e3,
+                         "us_per_step": sum(t) / steps * 1e3}
+    la.set_profiling(0)
+    la.close()
+    # algorithmic flop per layer: Gram + MRConv FC + FC1 + FC2 + FFN (C -> 4C -> C)
+    flops = 2.0 * B * N * w.M * C + 2.0 * B * N * C * (2 * C + C + C + 8 * C)
+    best = res["fused"]
+    peak = PEAK_TFLOPS[w.dtype]
+    tf = flops / (best["ms_per_step"] / L * 1e-3) / 1e12
+    return {"layers_per_s": best["layers_per_s"], "ms_per_step": best["ms_per_step"],
+            "schedule": "fused", "schedules": res, "kernels": kern,
+            "flop_per_layer": flops, "tflops": tf, "mfma_frac": tf / peak,
+            "entry": "gl_vig_stack"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -116,7 +203,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="vig_ti")
     ap.add_argument("--schedule", default="fused", choices=["fused", "lookahead", "standard"])
-    ap.add_argument("--only", default=None, choices=["stack", "knn", "mrconv", "copy"])
+    ap.add_argument("--only", default=None, choices=["stack", "knn", "mrconv", "copy", "full"])
+    ap.add_argument("--no-full-block", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -166,6 +254,10 @@ def main() -> int:
             b.copy_(a)
         torch.cuda.synchronize()
         log(f"copied {n} bytes x {args.steps}")
+        return 0
+    if args.only == "full":
+        r = full_block(args, w, api, I, dev, torch)
+        log("full block", json.dumps(r))
         return 0
     if args.only == "knn":
         keys = api.pool_keys(x0, w.H, w.W, w.pool_r) if w.pool_r > 1 else None
@@ -289,11 +381,20 @@ def main() -> int:
                     "per_launch": f"{fb_flops:.4g} flop (byte floor {fb_bytes:.4g})"}
     log("kernels", json.dumps(kernels))
 
+    full = None
+    if not args.no_full_block:
+        log("full ViG block stack")
+        full = full_block(args, w, api, I, dev, torch)
+        log("full block", json.dumps(full))
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         cpu = cpu_baseline(w, args.cpu_images)
         log("cpu", json.dumps(cpu))
+        if full is not None:
+            full["cpu_oracle"] = cpu_full_block(w, 2, min(w.L, 4))
+            log("cpu full block", json.dumps(full["cpu_oracle"]))
 
     line = {
         "metric": METRIC, "value": value, "unit": "layers/s", "n_gpus": 1, "steps": args.steps,
@@ -303,6 +404,7 @@ def main() -> int:
                    "M": w.M, "C": w.C, "k": w.k, "blocks": w.L, "dilations": dil,
                    "schedule": args.schedule},
         "roofline": roof, "cpu_baseline": cpu, "kernels": kernels, "schedules": schedules,
+        "full_block": full,
         "image_layers_per_s": value * w.B, "source_sha": kernel_source_sha(),
     }
     print(json.dumps(line), flush=True)

@@ -7,16 +7,18 @@
 //   * FC1, FC2 + residual and the FFN of the full ViG block (Eq. 11, 14, 15):
 //     act_in = GELU gives sigma(U~) W_out^T, act_out = GELU the FFN's hidden
 //     layer, residual the two skip connections.
-// A workgroup owns a 128 x 128 output tile, so W is read once per 128 rows
-// and A once per 128 output channels.
-//   - 4 waves in a 2 x 2 layout; each wave holds a 64 x 64 accumulator block
-//     (4 x 4 MFMA tiles of 16 x 16) in registers.
-//   - The contraction runs in steps of 64 bytes per row (32 bf16 or 16 fp32
-//     channels).  Both operands are K-contiguous, so one 16-byte vector per
-//     lane is exactly an MFMA operand slice.  A step's A and B tiles
-//     (128 rows x 64 bytes each) pass through LDS, double-buffered: the
-//     global loads of step s+1 are in flight while step s is multiplied, and
-//     one barrier per step separates the buffers.
+// A workgroup owns a 64 x 64 output tile, so W is read once per 64 rows and
+// A once per 64 output channels.
+//   - 4 waves in a 2 x 2 layout; each wave holds a 32 x 32 accumulator block
+//     (2 x 2 MFMA tiles of 16 x 16) in registers.
+//   - The contraction runs in stages of 256 bytes per row (4 MFMA k-steps:
+//     128 bf16 or 64 fp32 channels), so the short contractions of the ViG
+//     layers (K = 192 .. 1280) take 1 .. 10 stages, each one global round
+//     trip.  Both operands are K-contiguous, so one 16-byte vector per lane is
+//     exactly an MFMA operand slice.  A stage's A and B tiles (64 rows x 256
+//     bytes each) pass through LDS, double-buffered: the global loads of stage
+//     s+1 are in flight while stage s is multiplied, and one barrier per stage
+//     separates the buffers.
 //   - act_in is applied to A's elements as they are staged (fp32, rounded back
 //     to the storage type, as if the caller had stored sigma(A)).
 //   - Epilogue in fp32: + bias, act_out, + residual, rounded once.
@@ -25,12 +27,22 @@
 
 namespace gl {
 
-constexpr int kGmBM = 128, kGmBN = 128, kGmThreads = 256;
-constexpr int kGmStep = 64;                // bytes per row per contraction step
-constexpr int kGmRow = kGmStep + 16;       // LDS row stride (spreads rows over banks)
-constexpr int kGmTile = kGmBM * kGmRow;    // one operand tile: 10 KB
+constexpr int kGmThreads = 256;
 
-size_t gemm_smem_bytes() { return (size_t)4 * kGmTile; }
+// Tile configurations: BM x BM output tiles, STEP bytes of K per row per stage.
+//   64 x 64, 256 B: short contractions or few tiles (the ViG block's layers);
+//   128 x 128, 128 B: large GEMMs (e.g. the ViG-B update), where W and A are
+//   re-read half as often.
+template <int BM, int STEP>
+struct GemmCfg {
+  static constexpr int kRow = STEP + 16;                 // LDS row stride
+  static constexpr int kTile = BM * kRow;                // one operand tile of one stage
+  static constexpr int kVec = BM * STEP / 16 / kGmThreads;  // 16-byte loads per thread, operand
+  static constexpr int kTpw = BM / 32;                   // MFMA tiles per wave and dimension
+  static constexpr size_t kSmem = (size_t)4 * kTile;
+};
+
+size_t gemm_smem_bytes() { return GemmCfg<128, 128>::kSmem; }
 
 // GELU of the 16-byte vector's elements, rounded back to the storage type.
 template <int DT>
@@ -50,39 +62,41 @@ __device__ __forceinline__ u32x4 gelu_vec(u32x4 v) {
   return __builtin_bit_cast(u32x4, f);
 }
 
-template <int DT, int ACT_IN, int ACT_OUT>
+template <int DT, int ACT_IN, int ACT_OUT, int BM, int STEP>
 __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
   extern __shared__ __align__(16) char smem[];
-  constexpr int ES = DT ? 2 : 4;
+  using G = GemmCfg<BM, STEP>;
+  constexpr int kGmBM = BM, kGmBN = BM, kGmStep = STEP, kGmRow = G::kRow, kGmTile = G::kTile;
+  constexpr int kGmVec = G::kVec, TPW = G::kTpw, SPR = STEP / 16;
   const int R = a.R, K = a.K, Cout = a.Cout;
-  const int rowb = K * ES;                  // a multiple of 16
-  const int nsteps = (rowb + kGmStep - 1) / kGmStep;
+  const int rowb = K * (DT ? 2 : 4);        // a multiple of 16
+  const int nstages = (rowb + kGmStep - 1) / kGmStep;
   const int ntn = (Cout + kGmBN - 1) / kGmBN;
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
   const int mt = blk / ntn, nt = blk - mt * ntn;
   const int m0 = mt * kGmBM, n0 = nt * kGmBN;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, t = lane & 15;
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w >> 1, wn = w & 1;       // the wave's quadrant (16 TPW rows and columns)
 
-  // staging: vector v = tid + 256 i of a tile is row v / 4, 16-byte slot v % 4
+  // staging: vector v = tid + 256 i of a tile is row v / SPR, 16-byte slot v % SPR
   const char* Ab = static_cast<const char*>(a.A);
   const char* Wb = static_cast<const char*>(a.W);
-  const char* ag[2];
-  const char* bg[2];
-  int slot[2], lo[2];
+  const char* ag[kGmVec];
+  const char* bg[kGmVec];
+  int slot[kGmVec], lo[kGmVec];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int v = tid + kGmThreads * i, r = v >> 2;
-    slot[i] = (v & 3) * 16;
+  for (int i = 0; i < kGmVec; ++i) {
+    const int v = tid + kGmThreads * i, r = v / SPR;
+    slot[i] = (v % SPR) * 16;
     ag[i] = Ab + (size_t)min(m0 + r, R - 1) * rowb + slot[i];
     bg[i] = Wb + (size_t)min(n0 + r, Cout - 1) * rowb + slot[i];
     lo[i] = r * kGmRow + slot[i];
   }
-  u32x4 ra[2], rb[2];
+  u32x4 ra[kGmVec], rb[kGmVec];
   auto gload = [&](int s) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < kGmVec; ++i) {
       const bool in = s * kGmStep + slot[i] < rowb;
       const int off = in ? s * kGmStep : 0;
       ra[i] = *reinterpret_cast<const u32x4*>(ag[i] + off);
@@ -90,66 +104,61 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
       if (!in) ra[i] = rb[i] = u32x4{0, 0, 0, 0};
     }
   };
-  auto act = [&]() {
-    if (ACT_IN) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i) ra[i] = gelu_vec<DT>(ra[i]);
-    }
-  };
   auto sstore = [&](int buf) {
     char* sa = smem + buf * 2 * kGmTile;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      *reinterpret_cast<u32x4*>(sa + lo[i]) = ra[i];
+    for (int i = 0; i < kGmVec; ++i) {
+      *reinterpret_cast<u32x4*>(sa + lo[i]) = ACT_IN ? gelu_vec<DT>(ra[i]) : ra[i];
       *reinterpret_cast<u32x4*>(sa + kGmTile + lo[i]) = rb[i];
     }
   };
 
-  f32x4 acc[4][4];
+  f32x4 acc[TPW][TPW];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TPW; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TPW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   gload(0);
-  act();
   sstore(0);
   __syncthreads();
-  for (int s = 0; s < nsteps; ++s) {
-    if (s + 1 < nsteps) gload(s + 1);
+  for (int s = 0; s < nstages; ++s) {
+    if (s + 1 < nstages) gload(s + 1);
     const char* sa = smem + (s & 1) * 2 * kGmTile;
-    uint4 af[4], bf[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      af[i] = *reinterpret_cast<const uint4*>(sa + (wm * 64 + i * 16 + t) * kGmRow + g * 16);
-      bf[i] = *reinterpret_cast<const uint4*>(sa + kGmTile + (wn * 64 + i * 16 + t) * kGmRow + g * 16);
-    }
+    for (int kk = 0; kk < kGmStep / 64; ++kk) {
+      uint4 af[TPW], bf[TPW];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (DT) {
-          acc[i][j] = mfma_bf16(af[i], bf[j], acc[i][j]);
-        } else {
-          const float4 x4 = __builtin_bit_cast(float4, af[i]);
-          const float4 y4 = __builtin_bit_cast(float4, bf[j]);
-          acc[i][j] = mfma_f32(x4.x, y4.x, acc[i][j]);
-          acc[i][j] = mfma_f32(x4.y, y4.y, acc[i][j]);
-          acc[i][j] = mfma_f32(x4.z, y4.z, acc[i][j]);
-          acc[i][j] = mfma_f32(x4.w, y4.w, acc[i][j]);
-        }
+      for (int i = 0; i < TPW; ++i) {
+        af[i] = *reinterpret_cast<const uint4*>(sa + (wm * 16 * TPW + i * 16 + t) * kGmRow +
+                                                kk * 64 + g * 16);
+        bf[i] = *reinterpret_cast<const uint4*>(sa + kGmTile + (wn * 16 * TPW + i * 16 + t) * kGmRow +
+                                                kk * 64 + g * 16);
       }
-    if (s + 1 < nsteps) {
-      act();
-      sstore((s + 1) & 1);
+#pragma unroll
+      for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) {
+          if (DT) {
+            acc[i][j] = mfma_bf16(af[i], bf[j], acc[i][j]);
+          } else {
+            const float4 x4 = __builtin_bit_cast(float4, af[i]);
+            const float4 y4 = __builtin_bit_cast(float4, bf[j]);
+            acc[i][j] = mfma_f32(x4.x, y4.x, acc[i][j]);
+            acc[i][j] = mfma_f32(x4.y, y4.y, acc[i][j]);
+            acc[i][j] = mfma_f32(x4.z, y4.z, acc[i][j]);
+            acc[i][j] = mfma_f32(x4.w, y4.w, acc[i][j]);
+          }
+        }
     }
+    if (s + 1 < nstages) sstore((s + 1) & 1);
     __syncthreads();
   }
 
   // -- epilogue: lane (g, t) of tile (i, j) holds rows 4g..4g+3, column t --------
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int n = n0 + wn * 64 + j * 16 + t;
+  for (int j = 0; j < TPW; ++j) {
+    const int n = n0 + wn * 16 * TPW + j * 16 + t;
     if (n >= Cout) continue;
     float bn = 0.f;
     if (a.bias) {
@@ -157,10 +166,10 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
               : static_cast<const float*>(a.bias)[n];
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < TPW; ++i)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int row = m0 + wm * 64 + i * 16 + 4 * g + v;
+        const int row = m0 + wm * 16 * TPW + i * 16 + 4 * g + v;
         if (row >= R) continue;
         float y = acc[i][j][v] + bn;
         if (ACT_OUT) y = gelu_f32(y);
@@ -175,18 +184,31 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
   }
 }
 
+template <int BM, int STEP>
+const void* gemm_fn(int v) {
+  static const void* const fns[8] = {
+      (const void*)&gemm_nt_kernel<0, 0, 0, BM, STEP>, (const void*)&gemm_nt_kernel<0, 0, 1, BM, STEP>,
+      (const void*)&gemm_nt_kernel<0, 1, 0, BM, STEP>, (const void*)&gemm_nt_kernel<0, 1, 1, BM, STEP>,
+      (const void*)&gemm_nt_kernel<1, 0, 0, BM, STEP>, (const void*)&gemm_nt_kernel<1, 0, 1, BM, STEP>,
+      (const void*)&gemm_nt_kernel<1, 1, 0, BM, STEP>, (const void*)&gemm_nt_kernel<1, 1, 1, BM, STEP>};
+  return fns[v];
+}
+
 hipError_t launch_gemm_nt(const GemmArgs& a, int dt_bf16, hipStream_t stream, hipEvent_t ev0,
                           hipEvent_t ev1) {
-  const int nm = (a.R + kGmBM - 1) / kGmBM, nn = (a.Cout + kGmBN - 1) / kGmBN;
-  const dim3 grid(nm * nn), block(kGmThreads);
   const int v = (dt_bf16 ? 4 : 0) + (a.act_in ? 2 : 0) + (a.act_out ? 1 : 0);
-  static const void* const fns[8] = {
-      (const void*)&gemm_nt_kernel<0, 0, 0>, (const void*)&gemm_nt_kernel<0, 0, 1>,
-      (const void*)&gemm_nt_kernel<0, 1, 0>, (const void*)&gemm_nt_kernel<0, 1, 1>,
-      (const void*)&gemm_nt_kernel<1, 0, 0>, (const void*)&gemm_nt_kernel<1, 0, 1>,
-      (const void*)&gemm_nt_kernel<1, 1, 0>, (const void*)&gemm_nt_kernel<1, 1, 1>};
-  const void* fn = fns[v];
-  return launch_with_smem(fn, grid, block, gemm_smem_bytes(), stream, ev0, ev1, a);
+  const size_t rowb = (size_t)a.K * (dt_bf16 ? 2 : 4);
+  // large tiles once they alone give every CU a tile and K is long
+  const long tiles128 = (long)((a.R + 127) / 128) * ((a.Cout + 127) / 128);
+  const dim3 block(kGmThreads);
+  if (tiles128 >= 256 && rowb >= 1024) {
+    const dim3 grid((unsigned)tiles128);
+    return launch_with_smem(gemm_fn<128, 128>(v), grid, block, GemmCfg<128, 128>::kSmem, stream,
+                            ev0, ev1, a);
+  }
+  const dim3 grid((unsigned)(((a.R + 63) / 64) * ((a.Cout + 63) / 64)));
+  return launch_with_smem(gemm_fn<64, 256>(v), grid, block, GemmCfg<64, 256>::kSmem, stream, ev0,
+                          ev1, a);
 }
 
 }  // namespace gl
