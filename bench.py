@@ -134,6 +134,47 @@ def cpu_full_block(w, images: int, blocks: int) -> dict:
                       f"images for {blocks} blocks in {dt:.2f} s; scaled x{scale:g}"}
 
 
+def graph_replay(args, w, api, torch, x0, Wd, bd, dil, ws, out):
+    """The fused-schedule step captured once in a HIP graph (one stream) and
+    replayed; each replay is checked against the eager result first."""
+    s = torch.cuda.Stream()
+    lag = api.Lookahead(s, s)
+    ref = torch.empty_like(out)
+
+    def step(o):
+        lag.stack(x0, w.H, w.W, Wd, bd, dil, w.k, w.pool_r, schedule=api.GL_SCHED_LOOKAHEAD_FUSED,
+                  ws=ws, x_out=o)
+
+    with torch.cuda.stream(s):
+        step(ref)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    gout = torch.empty_like(out)
+    with torch.cuda.graph(g, stream=s):
+        step(gout)
+    for _ in range(3):
+        gout.zero_()
+        with torch.cuda.stream(s):
+            g.replay()
+        torch.cuda.synchronize()
+        if not torch.equal(gout, ref):
+            log("graph replay differs from the eager stack; not reported")
+            lag.close()
+            return None
+    n = max(10, args.steps // 4)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):       # replay() launches on the current stream
+        e0.record(s)
+        for _ in range(n):
+            g.replay()
+        e1.record(s)
+    torch.cuda.synchronize()
+    m = e0.elapsed_time(e1) / n
+    lag.close()
+    return {"ms_per_step": m, "layers_per_s": w.L / (m / 1e3)}
+
+
 def full_block(args, w, api, I, dev, torch) -> dict:
     """Time the full ViG block stack (gl_vig_stack) under its three schedules
     and profile its launches."""
@@ -311,6 +352,9 @@ def main() -> int:
                 step(sc)
             m = time_steps(max(10, args.steps // 4), sc)
             schedules[name] = {"ms_per_step": m, "layers_per_s": w.L / (m / 1e3)}
+        g = graph_replay(args, w, api, torch, x0, Wd, bd, dil, ws, out)
+        if g is not None:
+            schedules["fused_hip_graph"] = g
         log("schedules", json.dumps(schedules))
 
     # per-kernel durations: the same steps again, every launch stamped with a

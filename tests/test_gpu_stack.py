@@ -211,3 +211,37 @@ def test_profiling_records_builds():
     la.close()
     # bootstrap build; blocks 0 and L-1 are plain updates; blocks 1..L-2 one launch each
     assert (len(b), len(u), len(f)) == (1, 2, w.L - 2)
+
+
+def test_stack_hip_graph_replay():
+    """The fused-schedule stack captured in a HIP graph: every replay, with
+    eager work and synchronisations between replays, equals the eager run."""
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = I.with_batch(I.WORKLOADS["vig_ti"], 4)
+    x0d = to_dev(I.make_features(w))
+    Wst, bst = _weights(w, w.L, zero_bias=False)
+    Wd, bd = to_dev(Wst), to_dev(bst)
+    s = torch.cuda.Stream()
+    la = api.Lookahead(s, s)
+    ws = api.make_stack_workspace(x0d, w.H, w.W, w.k)
+    ref = torch.empty_like(x0d)
+    with torch.cuda.stream(s):
+        la.stack(x0d, w.H, w.W, Wd, bd, list(w.dilations), w.k,
+                 schedule=api.GL_SCHED_LOOKAHEAD_FUSED, ws=ws, x_out=ref)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    out = torch.empty_like(x0d)
+    with torch.cuda.graph(g, stream=s):
+        la.stack(x0d, w.H, w.W, Wd, bd, list(w.dilations), w.k,
+                 schedule=api.GL_SCHED_LOOKAHEAD_FUSED, ws=ws, x_out=out)
+    for r in range(4):
+        out.zero_()
+        junk = api.knn_graph(x0d, w.k, 2)          # eager work between replays
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), f"replay {r} differs"
+        del junk
+    la.close()
