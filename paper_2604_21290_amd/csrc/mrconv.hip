@@ -66,12 +66,12 @@ const void* gather_fn_kb(int KB) {
 }
 
 // The fused tile streams all of W through every workgroup of 16*rt nodes;
-// beyond 16 KB of W per node (or when the tile does not fit LDS) the two-pass
-// form, which reads W once per 128 nodes, is used.
+// beyond 8 KB of W per node (or when the tile does not fit LDS) the two-pass
+// form, which reads W once per 64 or 128 nodes, is used.
 bool mrconv_use_split(int C, int Cout, int dt_bf16, int rt) {
   if (rt < 1) return true;
   const size_t wbytes = (size_t)Cout * 2 * C * (dt_bf16 ? 2 : 4);
-  return wbytes / (size_t)(16 * rt) > 16384;
+  return wbytes / (size_t)(16 * rt) > 8192;
 }
 
 size_t mrconv_split_ws_bytes(int R, int C, int dt_bf16) {
