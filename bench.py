@@ -48,6 +48,11 @@ DESCR = {
     "pyr_s2": "Pyramid stage 2: 2 blocks, B=32, 28x28 (N=784), C=160, keys pooled 2x2 -> 196, k=9",
     "hires": "High-res stress: 4 blocks, B=8, 56x56 (N=3136), C=96, full N x N kNN, k=16, d=2",
     "single": "Single isotropic layer: B=1, N=196, C=192, fp32, k=9, d=1",
+    "vig_ti_448": "ViG-Ti at 448x448 input: 12 blocks, B=32, 28x28 patches (N=784), C=192, k=9, "
+                  "dilation ceil(l/4)",
+    "vig_s": "ViG-S isotropic stack: 12 blocks, B=32, N=196, C=320, k=9, dilation ceil(l/4)",
+    "pyr_s3": "Pyramid stage 3: 6 blocks, B=32, 14x14 (N=196), C=400, k=9, d=1",
+    "pyr_s4": "Pyramid stage 4: 2 blocks, B=32, 7x7 (N=49), C=640, k=9, d=1",
 }
 
 

@@ -126,6 +126,13 @@ WORKLOADS = {
     "pyr_s2": Workload("pyr_s2", 32, 28, 28, 160, 9, (1, 1), BF16, pool_r=2, seed=41),
     "hires": Workload("hires", 8, 56, 56, 96, 16, (2, 2, 2, 2), BF16, seed=5,
                       features="mixture"),
+    # further shapes of the paper's model table and its 448 x 448 inputs
+    "vig_ti_448": Workload("vig_ti_448", 32, 28, 28, 192, 9,
+                           tuple(math.ceil(l / 4) for l in range(1, 13)), BF16, seed=6),
+    "vig_s": Workload("vig_s", 32, 14, 14, 320, 9,
+                      tuple(math.ceil(l / 4) for l in range(1, 13)), BF16, seed=7),
+    "pyr_s3": Workload("pyr_s3", 32, 14, 14, 400, 9, (1,) * 6, BF16, seed=42),
+    "pyr_s4": Workload("pyr_s4", 32, 7, 7, 640, 9, (1, 1), BF16, seed=43),
 }
 
 

@@ -28,14 +28,15 @@ def _knn_case(x: I.Stored, k, d, keys: I.Stored | None = None, rows=None, label=
 
 
 # -- the workloads at full size (sampled rows where N = 3136) -----------------
-@pytest.mark.parametrize("name", ["single", "vig_ti", "vig_b", "hires"])
+@pytest.mark.parametrize("name", ["single", "vig_ti", "vig_b", "hires", "vig_ti_448", "vig_s",
+                                  "pyr_s3", "pyr_s4"])
 def test_knn_workload_full(name):
     require_gpu()
     from paper_2604_21290_amd import api
     w = I.WORKLOADS[name]
     x = I.make_features(w)
     rows = None
-    if w.N > 1000:
+    if w.N > 500:
         rows = np.sort(np.random.default_rng(99).choice(w.N, 384, replace=False))
     xd = to_dev(x)
     D = O.knn_distances(x.value, rows=rows)

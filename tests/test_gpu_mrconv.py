@@ -27,7 +27,8 @@ def _mr_case(x, idx, Wt, bias=None, keys=None, label=""):
     return check_close(got, ref, x.dtype, label)
 
 
-@pytest.mark.parametrize("name", ["single", "vig_ti", "vig_b", "pyr_s1", "pyr_s2", "hires"])
+@pytest.mark.parametrize("name", ["single", "vig_ti", "vig_b", "pyr_s1", "pyr_s2", "hires",
+                                  "vig_ti_448", "vig_s", "pyr_s3", "pyr_s4"])
 def test_mrconv_workload_full(name):
     """Full-size update with the workload's own graph (built by the oracle on
     a sample of images for speed; indices are inputs here)."""

@@ -91,6 +91,10 @@ CASES = [
     ("pyr_s1", 8, 4, 384),
     ("pyr_s2", 8, 4, None),
     ("hires", None, 2, 384),
+    ("vig_ti_448", 8, 2, 256),
+    ("vig_s", 8, 4, None),
+    ("pyr_s3", 8, 4, None),
+    ("pyr_s4", None, 4, None),
 ]
 
 
@@ -110,7 +114,8 @@ def test_lookahead_blocks_teacher_forced(case):
     teacher_forced_checks(w, xs, graphs, Wst, bst, n_img=n_img, rows=rows)
 
 
-@pytest.mark.parametrize("name", ["single", "vig_ti", "vig_b", "pyr_s1", "pyr_s2", "hires"])
+@pytest.mark.parametrize("name", ["single", "vig_ti", "vig_b", "pyr_s1", "pyr_s2", "hires",
+                                  "vig_ti_448", "vig_s", "pyr_s3", "pyr_s4"])
 def test_stack_entry_matches_blocks_and_serial(name):
     """gl_graphleap_stack at the full workload size (the launch configuration
     the benchmark times) equals the block-by-block run bit for bit, and the

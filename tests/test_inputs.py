@@ -26,6 +26,7 @@ def test_workloads_shapes():
     assert (W["pyr_s1"].N, W["pyr_s1"].M) == (3136, 196)
     assert (W["pyr_s2"].N, W["pyr_s2"].M) == (784, 196)
     assert (W["hires"].N, W["hires"].M, W["hires"].k) == (3136, 3136, 16)
+    assert (W["vig_ti_448"].N, W["vig_s"].C, W["pyr_s3"].C, W["pyr_s4"].N) == (784, 320, 400, 49)
     for w in W.values():
         assert w.k * max(w.dilations) <= w.M
 
