@@ -28,6 +28,8 @@ notes):
     key nodes and MRConv gathers the pooled (unnormalised) key rows.
   * The lookahead stack uses G(X^0) for blocks 0 and 1 and G(X^(l-1)) for
     block l >= 2; each graph gets the dilation of the block that consumes it.
+  * Multi-head MRConv splits the channels into H equal contiguous heads; head
+    h's outputs see only head h's channels of x_i and of m_i.
   * The full ViG block (Eq. 11-15, Alg. 1): sigma is the exact GELU
     x Phi(x); fully connected layers are x W^T + b with W[out, in] and an
     optional bias; there is no normalisation layer (the equations have none);
@@ -165,6 +167,30 @@ def mrconv_ref(x: np.ndarray, idx: np.ndarray, W: np.ndarray, b: np.ndarray | No
     if b is not None:
         out = out + np.asarray(b, dtype=np.float64)
     return (out, xcat) if return_concat else out
+
+
+def mrconv_heads_ref(x: np.ndarray, idx: np.ndarray, Wh: np.ndarray, b: np.ndarray | None = None,
+                     keys: np.ndarray | None = None) -> np.ndarray:
+    """Multi-head MRConv update (Sec. II-A; the per-head W_x,h / W_m,h of
+    Sec. IV-C2): channels split into H equal contiguous heads of hd = C/H;
+    output head h is  x_h W_x,h^T + m_h W_m,h^T  (+ b), with x_h and m_h the
+    head's channels of x_i and of the max-relative m_i.
+
+    Wh: [H, hd, 2 hd], row o of head h = [W_x,h[o, :] | W_m,h[o, :]].
+    Returns [B, N, C]."""
+    x = np.asarray(x, dtype=np.float64)
+    Wh = np.asarray(Wh, dtype=np.float64)
+    H, hd = Wh.shape[0], Wh.shape[1]
+    m = max_relative_ref(x, idx, keys)
+    outs = []
+    for h in range(H):
+        sl = slice(h * hd, (h + 1) * hd)
+        cat = np.concatenate([x[..., sl], m[..., sl]], axis=-1)
+        outs.append(cat @ Wh[h].T)
+    out = np.concatenate(outs, axis=-1)
+    if b is not None:
+        out = out + np.asarray(b, dtype=np.float64)
+    return out
 
 
 # ----------------------------------------------------------------------------

@@ -360,6 +360,64 @@ def pin_stack_pooled_graph_source(ref):
 
 
 # ---------------------------------------------------------------------------
+# multi-head MRConv pins (Sec. II-A, Sec. IV-C2)
+# ---------------------------------------------------------------------------
+def bf_mrconv_heads(x, idx, Wh, bias=None):
+    """Pure-Python per-head loops."""
+    x = np.asarray(x).tolist()
+    idx = np.asarray(idx).tolist()
+    Wh = np.asarray(Wh).tolist()
+    H, hd = len(Wh), len(Wh[0])
+    B, N, C = len(x), len(x[0]), len(x[0][0])
+    out = np.zeros((B, N, C))
+    for b in range(B):
+        for i in range(N):
+            m = [max(x[b][j][c] - x[b][i][c] for j in idx[b][i]) for c in range(C)]
+            for h in range(H):
+                xs = x[b][i][h * hd:(h + 1) * hd]
+                ms = m[h * hd:(h + 1) * hd]
+                for o in range(hd):
+                    s = math.fsum(a * w for a, w in zip(xs + ms, Wh[h][o]))
+                    out[b, i, h * hd + o] = s + (0.0 if bias is None else bias[h * hd + o])
+    return out
+
+
+def pin_mrconv_heads_bruteforce(ref):
+    rng = np.random.default_rng(51)
+    x = rng.standard_normal((2, 7, 6))
+    idx = rng.integers(0, 7, (2, 7, 3))
+    Wh = rng.standard_normal((3, 2, 4))
+    b = rng.standard_normal(6)
+    assert np.allclose(ref.mrconv_heads_ref(x, idx, Wh, b), bf_mrconv_heads(x, idx, Wh, b),
+                       atol=1e-12)
+
+
+def pin_mrconv_heads_one_head_is_dense(ref):
+    """H = 1 is the dense update with W = [W_x | W_m]."""
+    rng = np.random.default_rng(52)
+    x = rng.standard_normal((2, 9, 5))
+    idx = rng.integers(0, 9, (2, 9, 4))
+    W = rng.standard_normal((5, 10))
+    assert np.allclose(ref.mrconv_heads_ref(x, idx, W[None]), ref.mrconv_ref(x, idx, W),
+                       atol=1e-12)
+
+
+def pin_mrconv_heads_locality(ref):
+    """Changing head h's input channels changes only head h's outputs."""
+    rng = np.random.default_rng(53)
+    x = rng.standard_normal((1, 8, 8))
+    idx = np.tile(np.arange(8)[None, :, None], (1, 1, 2))
+    idx[..., 1] = (idx[..., 1] + 3) % 8
+    Wh = rng.standard_normal((4, 2, 4))
+    a = ref.mrconv_heads_ref(x, idx, Wh)
+    x2 = x.copy()
+    x2[..., 4:6] += rng.standard_normal((1, 8, 2))   # head 2
+    c = ref.mrconv_heads_ref(x2, idx, Wh)
+    assert np.array_equal(a[..., :4], c[..., :4]) and np.array_equal(a[..., 6:], c[..., 6:])
+    assert not np.allclose(a[..., 4:6], c[..., 4:6])
+
+
+# ---------------------------------------------------------------------------
 # full ViG block pins (Eq. 11-15, Alg. 1)
 # ---------------------------------------------------------------------------
 PHI1 = 0.8413447460685429   # standard normal CDF at 1 (printed tables)
@@ -499,7 +557,8 @@ PINS = [
     pin_stack_single_layer, pin_stack_identity_weights, pin_stack_circle_two_blocks,
     pin_stack_pooled_graph_source, pin_gelu_closed_form, pin_linear_bruteforce,
     pin_vig_block_bruteforce, pin_vig_block_residual_identity, pin_vig_block_hand,
-    pin_vig_stack_graph_source,
+    pin_vig_stack_graph_source, pin_mrconv_heads_bruteforce, pin_mrconv_heads_one_head_is_dense,
+    pin_mrconv_heads_locality,
 ]
 
 

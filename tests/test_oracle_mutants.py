@@ -166,6 +166,24 @@ def _vig_stack_factory(graph_from="u", lag=1, block=None):
     return stack
 
 
+def _heads_factory(shift_m=False, swap=False):
+    def mh(x, idx, Wh, b=None, keys=None):
+        x = np.asarray(x, dtype=np.float64)
+        Wh = np.asarray(Wh, dtype=np.float64)
+        H, hd = Wh.shape[0], Wh.shape[1]
+        m = R.max_relative_ref(x, idx, keys)
+        outs = []
+        for h in range(H):
+            sl = slice(h * hd, (h + 1) * hd)
+            hm = ((h + 1) % H) if shift_m else h
+            slm = slice(hm * hd, (hm + 1) * hd)
+            parts = [m[..., slm], x[..., sl]] if swap else [x[..., sl], m[..., slm]]
+            outs.append(np.concatenate(parts, axis=-1) @ Wh[h].T)
+        out = np.concatenate(outs, axis=-1)
+        return out if b is None else out + b
+    return mh
+
+
 MUTANTS = {
     "knn_no_normalisation": dict(knn_ref=_knn_factory(normalize=False)),
     "knn_descending": dict(knn_ref=_knn_factory(descending=True)),
@@ -190,6 +208,8 @@ MUTANTS = {
     "block_ffn_bias_dropped": dict(vig_block_ref=_block_factory(drop_b1=True)),
     "vig_stack_graph_from_x": dict(vig_stack_ref=_vig_stack_factory(graph_from="x")),
     "vig_stack_no_lookahead": dict(vig_stack_ref=_vig_stack_factory(lag=0)),
+    "heads_m_from_next_head": dict(mrconv_heads_ref=_heads_factory(shift_m=True)),
+    "heads_halves_swapped": dict(mrconv_heads_ref=_heads_factory(swap=True)),
 }
 
 
