@@ -180,6 +180,34 @@ def graph_replay(args, w, api, torch, x0, Wd, bd, dil, ws, out):
     return {"ms_per_step": m, "layers_per_s": w.L / (m / 1e3)}
 
 
+def heads_update(args, w, api, torch, x0, idx, Wdense, H=16) -> dict | None:
+    """The multi-head MRConv update (gl_mrconv_heads, H heads, block-diagonal
+    W) against the dense update with the same W, averaged over launches."""
+    if w.C % H or w.pool_r > 1:
+        return None
+    hd = w.C // H
+    Wb = torch.zeros_like(Wdense)
+    for h in range(H):
+        Wb[h * hd:(h + 1) * hd, h * hd:(h + 1) * hd] = Wdense[h * hd:(h + 1) * hd, h * hd:(h + 1) * hd]
+        Wb[h * hd:(h + 1) * hd, w.C + h * hd:w.C + (h + 1) * hd] = \
+            Wdense[h * hd:(h + 1) * hd, w.C + h * hd:w.C + (h + 1) * hd]
+    out = torch.empty_like(x0)
+    res = {"heads": H}
+    n = max(20, args.steps // 4)
+    for name, hh in (("dense_us", 1), ("heads_us", H)):
+        for _ in range(3):
+            api.mrconv(x0, idx, Wb, out=out, heads=hh)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(n):
+            api.mrconv(x0, idx, Wb, out=out, heads=hh)
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = e0.elapsed_time(e1) / n * 1e3
+    return res
+
+
 def full_block(args, w, api, I, dev, torch) -> dict:
     """Time the full ViG block stack (gl_vig_stack) under its three schedules
     and profile its launches."""
@@ -429,6 +457,10 @@ def main() -> int:
                     "traffic": load_traffic("graphleap_block", args.workload),
                     "per_launch": f"{fb_flops:.4g} flop (byte floor {fb_bytes:.4g})"}
     log("kernels", json.dumps(kernels))
+    hu = heads_update(args, w, api, torch, x0, ws["idx"][0], Wd[0])
+    if hu is not None:
+        kernels["mrconv_heads"] = hu
+        log("multi-head update", json.dumps(hu))
 
     full = None
     if not args.no_full_block:

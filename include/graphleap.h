@@ -139,6 +139,24 @@ gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
                     gl_dtype dt, void* out, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * gl_mrconv_heads -- the multi-head MRConv update (Sec. II-A; per-head
+ * W_x,h / W_m,h of Sec. IV-C2): channels split into `heads` equal contiguous
+ * heads of hd = C / heads, and output head h sees only head h's channels of
+ * x_i and of m_i:
+ *   out[b,i,h*hd + o] = sum_{c<hd} x[b,i,h*hd+c] W[h*hd+o, h*hd+c]
+ *                     + sum_{c<hd} m[b,i,h*hd+c] W[h*hd+o, C+h*hd+c] + bias[h*hd+o]
+ * W is the dense [C, 2C] = [W_x | W_m] of gl_mrconv and MUST hold zeros
+ * outside the heads' diagonal blocks of each half.  The kernel skips the
+ * contraction steps a 16-column output tile does not need, but steps that
+ * straddle a block edge do multiply the zeros.  Cout == C.  Everything else
+ * is as gl_mrconv; heads == 1 is gl_mrconv.
+ * Limits: heads >= 1, C % heads == 0.
+ * -------------------------------------------------------------------------*/
+gl_status gl_mrconv_heads(const void* x, int B, int N, int C, const void* keys, int M,
+                          const int32_t* idx, int k, const void* W, const void* bias, int heads,
+                          gl_dtype dt, void* out, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Lookahead handle (Sec. IV-A, IV-F; the look-ahead buffer of Sec. IV-G).
  * Holds two HIP events that order the build stream against the update
  * stream; the caller owns both streams and every tensor.  Streams must be

@@ -42,6 +42,7 @@ SIGNATURES = {
     "gl_knn_graph": [_vp, _i, _i, _i, _vp, _i, _i, _i, _i, _vp, _vp],
     "gl_pool_keys": [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp],
     "gl_mrconv": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp],
+    "gl_mrconv_heads": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp],
     "gl_lookahead_create": [_vp, _vp, ctypes.POINTER(_vp)],
     "gl_lookahead_destroy": [_vp],
     "gl_lookahead_set_profiling": [_vp, _i],
@@ -141,16 +142,21 @@ def pool_keys(x: torch.Tensor, H: int, W: int, r: int, out: torch.Tensor | None 
 
 def mrconv(x: torch.Tensor, idx: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = None,
            keys: torch.Tensor | None = None, out: torch.Tensor | None = None,
-           stream=None) -> torch.Tensor:
-    """out[B, N, Cout] = [x_i, max_j (keys_j - x_i)] W^T + bias."""
+           stream=None, heads: int = 1) -> torch.Tensor:
+    """out[B, N, Cout] = [x_i, max_j (keys_j - x_i)] W^T + bias.  heads > 1: the
+    multi-head update (W block-diagonal by heads in each half, Cout == C)."""
     B, N, C = x.shape
     M = N if keys is None else keys.shape[1]
     k = idx.shape[2]
     Cout = W.shape[0]
     if out is None:
         out = torch.empty((B, N, Cout), dtype=x.dtype, device=x.device)
-    _call("gl_mrconv", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(W), _p(bias), Cout, _dt(x),
-          _p(out), _s(stream))
+    if heads != 1:
+        _call("gl_mrconv_heads", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(W), _p(bias), heads,
+              _dt(x), _p(out), _s(stream))
+    else:
+        _call("gl_mrconv", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(W), _p(bias), Cout, _dt(x),
+              _p(out), _s(stream))
     return out
 
 

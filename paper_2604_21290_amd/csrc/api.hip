@@ -355,6 +355,31 @@ gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
   return e == hipSuccess ? GL_OK : hip_fail(e, "mrconv launch");
 }
 
+gl_status gl_mrconv_heads(const void* x, int B, int N, int C, const void* keys, int M,
+                          const int32_t* idx, int k, const void* W, const void* bias, int heads,
+                          gl_dtype dt, void* out, hipStream_t stream) {
+  int rt = 0;
+  gl_status s = check_mrconv(x, B, N, C, keys, M, idx, k, W, bias, C, dt, out, &rt);
+  if (s != GL_OK) return s;
+  if (heads < 1 || C % heads)
+    return fail(GL_ERR_BAD_SHAPE, "mrconv_heads: heads=%d must divide C=%d", heads, C);
+  const int dtb = dt == GL_BF16;
+  void* ws = nullptr;
+  hipError_t e;
+  if (gl::mrconv_use_split(C, C, dtb, rt)) {
+    if ((e = hipMallocAsync(&ws, gl::mrconv_split_ws_bytes(B * N, C, dtb), stream)) != hipSuccess)
+      return hip_fail(e, "hipMallocAsync (MRConv workspace)");
+  }
+  gl::MrArgs a = gl::make_mr_args(x, keys ? keys : x, idx, W, bias, out, B, N, M, C, C, k);
+  a.heads = heads;
+  e = gl::launch_mrconv_args(a, dtb, rt, ws, stream);
+  if (ws) {
+    hipError_t f = hipFreeAsync(ws, stream);
+    if (e == hipSuccess) e = f;
+  }
+  return e == hipSuccess ? GL_OK : hip_fail(e, "mrconv launch");
+}
+
 gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_lookahead_t* out) {
   if (!out) return fail(GL_ERR_NULL_PTR, "lookahead_create: out is NULL");
   *out = nullptr;

@@ -112,6 +112,7 @@ MrArgs make_mr_args(const void* x, const void* keys, const int32_t* idx, const v
   a.C = C;
   a.Cout = Cout;
   a.k = k;
+  a.heads = 1;
   return a;
 }
 

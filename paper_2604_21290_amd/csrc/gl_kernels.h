@@ -28,6 +28,7 @@ struct MrArgs {
   const void* bias;   // [Cout] or null
   void* out;          // [B*N, Cout]
   int R, N, M, C, Cout, k;
+  int heads;          // > 1: W is block-diagonal by heads (Cout == C); zero blocks are skipped
 };
 
 struct GemmArgs {
@@ -88,6 +89,10 @@ hipError_t launch_mrconv(const void* x, const void* keys, const int32_t* idx, co
                          const void* bias, void* out, int B, int N, int M, int C, int Cout, int k,
                          int dt_bf16, int rt, void* split_ws, hipStream_t stream,
                          hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// The same with the arguments packed (a.heads > 1 for the multi-head update).
+hipError_t launch_mrconv_args(const MrArgs& a, int dt_bf16, int rt, void* split_ws,
+                              hipStream_t stream, hipEvent_t ev0 = nullptr,
+                              hipEvent_t ev1 = nullptr);
 bool mrconv_use_split(int C, int Cout, int dt_bf16, int rt);
 size_t mrconv_split_ws_bytes(int R, int C, int dt_bf16);
 size_t gemm_smem_bytes();

@@ -82,7 +82,17 @@ hipError_t launch_mrconv(const void* x, const void* keys, const int32_t* idx, co
                          const void* bias, void* out, int B, int N, int M, int C, int Cout, int k,
                          int dt_bf16, int rt, void* split_ws, hipStream_t stream, hipEvent_t ev0,
                          hipEvent_t ev1) {
-  MrArgs a = make_mr_args(x, keys, idx, W, bias, out, B, N, M, C, Cout, k);
+  return launch_mrconv_args(make_mr_args(x, keys, idx, W, bias, out, B, N, M, C, Cout, k), dt_bf16,
+                            rt, split_ws, stream, ev0, ev1);
+}
+
+hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split_ws,
+                              hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  MrArgs a = a0;
+  const int C = a.C, Cout = a.Cout, k = a.k;
+  const void* W = a.W;
+  const void* bias = a.bias;
+  void* out = a.out;
   const int KB = mrconv_k_bucket(k);
   if (mrconv_use_split(C, Cout, dt_bf16, rt)) {
     if (!split_ws) return hipErrorInvalidValue;

@@ -46,9 +46,21 @@ __device__ __forceinline__ void store_vec(char* p, const float* f) {
 // W operands of k-steps s0 .. s0+kMrKU-1 for the wave's output tiles
 // w + 4*(4p + c4), c4 < 4 (16 columns each).  Tiles past Cout are not loaded;
 // k past 2C reads column 0 (the MFMA gets a zero operand there).
+// Multi-head update (a.heads > 1, Cout == C): does the 16-column output tile
+// starting at n0 need contraction step s?  Only the channels of the heads the
+// tile's columns belong to, in the x half and in the m half, are non-zero in
+// the block-diagonal W.  Wave-uniform.
+__device__ __forceinline__ bool mr_step_needed(const MrArgs& a, int n0, int s, int kstep) {
+  if (a.heads <= 1) return true;
+  const int hd = a.C / a.heads;
+  const int lo = (n0 / hd) * hd, hi = (min(n0 + 15, a.Cout - 1) / hd + 1) * hd;
+  const int k0 = s * kstep, k1 = k0 + kstep;
+  return (k0 < hi && k1 > lo) || (k0 < a.C + hi && k1 > a.C + lo);
+}
+
 template <int DT>
-__device__ __forceinline__ void mr_load_w(uint4 (&bw)[kMrKU][4], const char* Wb, int w, int p,
-                                          int s0, int K2, int Cout, int g, int t) {
+__device__ __forceinline__ void mr_load_w(uint4 (&bw)[kMrKU][4], const MrArgs& a, const char* Wb,
+                                          int w, int p, int s0, int K2, int Cout, int g, int t) {
   constexpr int ES = DT ? 2 : 4;
   constexpr int KSTEP = DT ? 32 : 16;
 #pragma unroll
@@ -58,6 +70,7 @@ __device__ __forceinline__ void mr_load_w(uint4 (&bw)[kMrKU][4], const char* Wb,
     const char* wrow = Wb + (size_t)min(n0 + t, Cout - 1) * K2 * ES;
 #pragma unroll
     for (int u = 0; u < kMrKU; ++u) {
+      if (!mr_step_needed(a, n0, s0 + u, KSTEP)) continue;  // wave-uniform
       const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
       bw[u][c4] = *reinterpret_cast<const uint4*>(wrow + (size_t)(kk < K2 ? kk : 0) * ES);
     }
@@ -169,7 +182,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
   const int NCT = (Cout + 15) >> 4;
   const char* Wb = static_cast<const char*>(a.W);
   uint4 bw[kMrKU][4];
-  if (w < NCT) mr_load_w<DT>(bw, Wb, w, 0, 0, K2, Cout, g, t);
+  if (w < NCT) mr_load_w<DT>(bw, a, Wb, w, 0, 0, K2, Cout, g, t);
   __syncthreads();
 
   mr_gather_rows<DT, KB>(a, row0, TM, sIdx, sA, lds_row);
@@ -186,7 +199,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
 #pragma unroll
     for (int c4 = 0; c4 < 4; ++c4) nvalid[c4] = (w + 4 * (4 * p + c4)) * 16 < Cout;
     for (int s0 = 0; s0 < ksteps; s0 += kMrKU) {
-      if (p != 0 || s0 != 0) mr_load_w<DT>(bw, Wb, w, p, s0, K2, Cout, g, t);
+      if (p != 0 || s0 != 0) mr_load_w<DT>(bw, a, Wb, w, p, s0, K2, Cout, g, t);
       bool kin[kMrKU];
 #pragma unroll
       for (int u = 0; u < kMrKU; ++u) kin[u] = (s0 + u) * KSTEP + g * (KSTEP / 4) < K2;
@@ -200,6 +213,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
                           : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int c4 = 0; c4 < 4; ++c4) {
+          if (!mr_step_needed(a, (w + 4 * (4 * p + c4)) * 16, s0 + u, KSTEP)) continue;
           const uint4 bv = (kin[u] && nvalid[c4]) ? bw[u][c4] : make_uint4(0, 0, 0, 0);
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt) {

@@ -158,3 +158,12 @@ def test_vig_validation():
     st = L.gl_vig_stack(None, P(0), 2, 196, 192, 2, 9, (ctypes.c_int * 2)(1, 1),
                         ctypes.byref(pp), 1, 2, P(5), 1 << 30, P(9))
     assert api.STATUS[st] == "GL_ERR_BAD_HANDLE"
+
+
+@host_only
+def test_mrconv_heads_validation():
+    L = api.lib()
+    st = L.gl_mrconv_heads(P(0), 2, 196, 192, None, 196, P(10), 9, P(20), None, 5, 1, P(30), None)
+    assert api.STATUS[st] == "GL_ERR_BAD_SHAPE"          # 5 does not divide 192
+    st = L.gl_mrconv_heads(P(0), 2, 196, 192, None, 196, P(10), 9, P(20), None, 0, 1, P(30), None)
+    assert api.STATUS[st] == "GL_ERR_BAD_SHAPE"

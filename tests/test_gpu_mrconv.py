@@ -108,3 +108,54 @@ def test_mrconv_deterministic():
     b = api.mrconv(x, idx, Wt)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+# -- multi-head update (gl_mrconv_heads) --------------------------------------------
+HEADS = [
+    # label, workload, batch, heads
+    ("vig_ti_h4", "vig_ti", 4, 4),
+    ("vig_ti_h16", "vig_ti", 4, 16),
+    ("pyr_s2_h4", "pyr_s2", 4, 4),
+    ("vig_b_h16_two_pass", "vig_b", 4, 16),
+    ("single_fp32_h3", "single", 1, 3),
+]
+
+
+def _block_diag(Wh: np.ndarray) -> np.ndarray:
+    """Dense [C, 2C] = [W_x | W_m] from per-head [H, hd, 2hd]."""
+    H, hd = Wh.shape[0], Wh.shape[1]
+    C = H * hd
+    W = np.zeros((C, 2 * C))
+    for h in range(H):
+        W[h * hd:(h + 1) * hd, h * hd:(h + 1) * hd] = Wh[h][:, :hd]
+        W[h * hd:(h + 1) * hd, C + h * hd:C + (h + 1) * hd] = Wh[h][:, hd:]
+    return W
+
+
+@pytest.mark.parametrize("case", HEADS, ids=[c[0] for c in HEADS])
+def test_mrconv_heads(case):
+    require_gpu()
+    from paper_2604_21290_amd import api
+    label, name, B, H = case
+    w = I.with_batch(I.WORKLOADS[name], B)
+    x = I.make_features(w)
+    keys = None
+    if w.pool_r > 1:
+        keys = I.store(O.pool_keys_ref(x.value, w.H, w.W, w.pool_r), w.dtype)
+    idx = I.random_indices(w.seed, w.B, w.N, w.k, w.M)
+    hd = w.C // H
+    g = np.random.default_rng(H * 1000 + w.C)
+    Wh = I.store(g.uniform(-1, 1, (H, hd, 2 * hd)) / np.sqrt(2 * hd), w.dtype)
+    Wd = I.store(_block_diag(Wh.value), w.dtype)
+    b = I.make_bias(w, 0, zero=False)
+    _say("mrconv heads", label, "H", H, "hd", hd)
+    xd, idd = to_dev(x), torch.from_numpy(idx).cuda()
+    kd = None if keys is None else to_dev(keys)
+    out = api.mrconv(xd, idd, to_dev(Wd), to_dev(b), keys=kd, heads=H)
+    dense = api.mrconv(xd, idd, to_dev(Wd), to_dev(b), keys=kd)
+    torch.cuda.synchronize()
+    ref = O.mrconv_heads_ref(x.value, idx, Wh.value, b.value,
+                             keys=None if keys is None else keys.value)
+    check_close(from_dev(out).value, ref, w.dtype, label)
+    # skipped steps only ever multiplied zeros: same as the dense update
+    assert torch.equal(out, dense), label
