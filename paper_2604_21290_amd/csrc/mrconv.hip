@@ -26,8 +26,25 @@ __global__ __launch_bounds__(kMrThreads) __attribute__((amdgpu_waves_per_eu(3, 8
   mrconv_tile<DT, RT, KB>(smem, a, blk * 16 * RT);
 }
 
-template <int DT, int RT>
+// The multi-head update: the per-tile step tests need registers the
+// three-waves-per-SIMD budget does not leave, so this one is not held to it.
+template <int DT, int RT, int KB>
+__global__ __launch_bounds__(kMrThreads) void mrconv_heads_kernel(MrArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  const int blk = xcd_remap(blockIdx.x, gridDim.x);
+  mrconv_tile<DT, RT, KB, true>(smem, a, blk * 16 * RT);
+}
+
+template <int DT, int RT, bool HEADS = false>
 const void* mrconv_fn_kb(int KB) {
+  if (HEADS) {
+    switch (KB) {
+      case 9: return (const void*)&mrconv_heads_kernel<DT, RT, 9>;
+      case 16: return (const void*)&mrconv_heads_kernel<DT, RT, 16>;
+      case 32: return (const void*)&mrconv_heads_kernel<DT, RT, 32>;
+      default: return (const void*)&mrconv_heads_kernel<DT, RT, 64>;
+    }
+  }
   switch (KB) {
     case 9: return (const void*)&mrconv_kernel<DT, RT, 9>;
     case 16: return (const void*)&mrconv_kernel<DT, RT, 16>;
@@ -117,8 +134,14 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
   const int TM = 16 * rt;
   const size_t smem = mrconv_smem_bytes(C, k, dt_bf16, rt);
   const dim3 grid((a.R + TM - 1) / TM), block(kMrThreads);
-  const void* fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2>(KB) : mrconv_fn_kb<1, 1>(KB))
-                           : (rt == 2 ? mrconv_fn_kb<0, 2>(KB) : mrconv_fn_kb<0, 1>(KB));
+  const void* fn;
+  if (a.heads > 1) {
+    fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2, true>(KB) : mrconv_fn_kb<1, 1, true>(KB))
+                 : (rt == 2 ? mrconv_fn_kb<0, 2, true>(KB) : mrconv_fn_kb<0, 1, true>(KB));
+  } else {
+    fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2>(KB) : mrconv_fn_kb<1, 1>(KB))
+                 : (rt == 2 ? mrconv_fn_kb<0, 2>(KB) : mrconv_fn_kb<0, 1>(KB));
+  }
   return launch_with_smem(fn, grid, block, smem, stream, ev0, ev1, a);
 }
 

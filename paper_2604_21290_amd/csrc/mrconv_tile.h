@@ -58,7 +58,7 @@ __device__ __forceinline__ bool mr_step_needed(const MrArgs& a, int n0, int s, i
   return (k0 < hi && k1 > lo) || (k0 < a.C + hi && k1 > a.C + lo);
 }
 
-template <int DT>
+template <int DT, bool HEADS>
 __device__ __forceinline__ void mr_load_w(uint4 (&bw)[kMrKU][4], const MrArgs& a, const char* Wb,
                                           int w, int p, int s0, int K2, int Cout, int g, int t) {
   constexpr int ES = DT ? 2 : 4;
@@ -70,7 +70,7 @@ __device__ __forceinline__ void mr_load_w(uint4 (&bw)[kMrKU][4], const MrArgs& a
     const char* wrow = Wb + (size_t)min(n0 + t, Cout - 1) * K2 * ES;
 #pragma unroll
     for (int u = 0; u < kMrKU; ++u) {
-      if (!mr_step_needed(a, n0, s0 + u, KSTEP)) continue;  // wave-uniform
+      if (HEADS && !mr_step_needed(a, n0, s0 + u, KSTEP)) continue;  // wave-uniform
       const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
       bw[u][c4] = *reinterpret_cast<const uint4*>(wrow + (size_t)(kk < K2 ? kk : 0) * ES);
     }
@@ -154,7 +154,8 @@ __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM
 
 // TM = 16*RT nodes starting at flattened node row0.  smem holds
 // mrconv_smem_bytes(C, k, RT) bytes.  Called by all 256 threads.
-template <int DT, int RT, int KB>
+// HEADS: the multi-head update (a.heads > 1), which skips the zero blocks of W.
+template <int DT, int RT, int KB, bool HEADS = false>
 __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row0) {
   constexpr int TM = 16 * RT;
   constexpr int ES = DT ? 2 : 4;
@@ -182,7 +183,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
   const int NCT = (Cout + 15) >> 4;
   const char* Wb = static_cast<const char*>(a.W);
   uint4 bw[kMrKU][4];
-  if (w < NCT) mr_load_w<DT>(bw, a, Wb, w, 0, 0, K2, Cout, g, t);
+  if (w < NCT) mr_load_w<DT, HEADS>(bw, a, Wb, w, 0, 0, K2, Cout, g, t);
   __syncthreads();
 
   mr_gather_rows<DT, KB>(a, row0, TM, sIdx, sA, lds_row);
@@ -199,7 +200,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
 #pragma unroll
     for (int c4 = 0; c4 < 4; ++c4) nvalid[c4] = (w + 4 * (4 * p + c4)) * 16 < Cout;
     for (int s0 = 0; s0 < ksteps; s0 += kMrKU) {
-      if (p != 0 || s0 != 0) mr_load_w<DT>(bw, a, Wb, w, p, s0, K2, Cout, g, t);
+      if (p != 0 || s0 != 0) mr_load_w<DT, HEADS>(bw, a, Wb, w, p, s0, K2, Cout, g, t);
       bool kin[kMrKU];
 #pragma unroll
       for (int u = 0; u < kMrKU; ++u) kin[u] = (s0 + u) * KSTEP + g * (KSTEP / 4) < K2;
@@ -213,7 +214,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
                           : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int c4 = 0; c4 < 4; ++c4) {
-          if (!mr_step_needed(a, (w + 4 * (4 * p + c4)) * 16, s0 + u, KSTEP)) continue;
+          if (HEADS && !mr_step_needed(a, (w + 4 * (4 * p + c4)) * 16, s0 + u, KSTEP)) continue;
           const uint4 bv = (kin[u] && nvalid[c4]) ? bw[u][c4] : make_uint4(0, 0, 0, 0);
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt) {
