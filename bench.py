@@ -96,7 +96,9 @@ def algorithmic(w, es):
     return knn_flops, knn_bytes, mr_flops, mr_bytes
 
 
-def cpu_baseline(w, images: int) -> dict:
+def cpu_baseline(w, images: int, min_seconds: float = 10.0) -> dict:
+    """The oracle's stack on `images` of the batch, repeated until at least
+    `min_seconds` of single-thread CPU work have been timed."""
     import numpy as np  # noqa: F401
     from threadpoolctl import threadpool_limits
 
@@ -108,15 +110,18 @@ def cpu_baseline(w, images: int) -> dict:
     x = I.make_features(ws)
     Ws = [I.make_weight(ws, l).value for l in range(w.L)]
     bs = [I.make_bias(ws, l).value for l in range(w.L)]
+    reps, dt = 0, 0.0
     with threadpool_limits(1):
-        t0 = time.perf_counter()
-        O.stack_ref(x.value, Ws, bs, w.dilations, w.k, w.H, w.W, w.pool_r)
-        dt = time.perf_counter() - t0
+        while dt < min_seconds:
+            t0 = time.perf_counter()
+            O.stack_ref(x.value, Ws, bs, w.dilations, w.k, w.H, w.W, w.pool_r)
+            dt += time.perf_counter() - t0
+            reps += 1
     scale = w.B / S
-    return {"value": w.L / (dt * scale), "unit": "layers/s", "cores": 1, "kind": "oracle",
+    return {"value": w.L * reps / (dt * scale), "unit": "layers/s", "cores": 1, "kind": "oracle",
             "sample": f"oracle.stack_ref (fp64 numpy, lookahead schedule, 1 thread) on {S} of "
-                      f"{w.B} images for all {w.L} blocks in {dt:.2f} s; time scaled x{scale:g} "
-                      f"to the full batch"}
+                      f"{w.B} images for all {w.L} blocks, {reps} run(s) in {dt:.2f} s"
+                      + (f"; time scaled x{scale:g} to the full batch" if scale != 1 else "")}
 
 
 def cpu_full_block(w, images: int, blocks: int) -> dict:
@@ -279,7 +284,8 @@ def main() -> int:
     ap.add_argument("--schedule", default="fused", choices=["fused", "lookahead", "standard"])
     ap.add_argument("--only", default=None, choices=["stack", "knn", "mrconv", "copy", "full"])
     ap.add_argument("--no-full-block", action="store_true")
-    ap.add_argument("--cpu-images", type=int, default=16)
+    ap.add_argument("--cpu-images", type=int, default=32)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
 
@@ -471,7 +477,7 @@ def main() -> int:
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
-        cpu = cpu_baseline(w, args.cpu_images)
+        cpu = cpu_baseline(w, args.cpu_images, args.cpu_seconds)
         log("cpu", json.dumps(cpu))
         if full is not None:
             full["cpu_oracle"] = cpu_full_block(w, 2, min(w.L, 4))
