@@ -213,6 +213,61 @@ def heads_update(args, w, api, torch, x0, idx, Wdense, H=16) -> dict | None:
     return res
 
 
+def step_percentiles(torch, step, stream, n: int) -> dict:
+    """Per-stack times: one event pair per step on the stream that ends it."""
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(n):
+        step()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    import numpy as np
+    t = np.array([ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(n)])
+    return {"n": n, "median_us": float(np.median(t)), "p10_us": float(np.percentile(t, 10)),
+            "p90_us": float(np.percentile(t, 90))}
+
+
+def cold_gather(w, api, torch, x0, idx, W, b, out, mr_bytes, reps: int = 20) -> dict:
+    """The MRConv update warm and cold.  Warm: `reps` launches back to back,
+    so the queue never drains.  Cold: a 512 MiB write before the launch evicts
+    L2 and the 256 MB Infinity Cache; the launch is queued behind the write, and
+    its time is the median of (write + update) minus the median of the write alone."""
+    import numpy as np
+    keys = api.pool_keys(x0, w.H, w.W, w.pool_r) if w.pool_r > 1 else None
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream()
+
+    def timed(fn) -> float:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(s)
+        fn()
+        e1.record(s)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3
+
+    def upd():
+        api.mrconv(x0, idx, W, b, keys=keys, out=out)
+
+    def many():
+        for _ in range(reps):
+            upd()
+
+    timed(many)
+    warm = timed(many) / reps
+    pair, alone = [], []
+    for i in range(reps):
+        pair.append(timed(lambda: (flush.fill_(i & 0xFF), upd())))
+        alone.append(timed(lambda: flush.fill_((i + 1) & 0xFF)))
+    cold = float(np.median(pair) - np.median(alone))
+    del flush
+    return {"warm_us": warm, "cold_us": cold, "hbm_gbs_warm": mr_bytes / warm / 1e3,
+            "hbm_gbs_cold": mr_bytes / cold / 1e3, "hbm_frac_cold": mr_bytes / cold / 1e3 / PEAK_HBM_GBS,
+            "method": f"warm: {reps} back-to-back launches; cold: median(512 MiB write + launch) "
+                      f"- median(write alone) over {reps} pairs"}
+
+
 def full_block(args, w, api, I, dev, torch) -> dict:
     """Time the full ViG block stack (gl_vig_stack) under its three schedules
     and profile its launches."""
@@ -395,6 +450,12 @@ def main() -> int:
         if g is not None:
             schedules["fused_hip_graph"] = g
         log("schedules", json.dumps(schedules))
+        # build/update overlap: the serial schedule against the two overlapped ones
+        t_ser = schedules["standard"]["ms_per_step"]
+        overlap = {"serial_over_lookahead": t_ser / schedules["lookahead"]["ms_per_step"],
+                   "serial_over_fused": t_ser / schedules["fused"]["ms_per_step"]}
+        per_step = step_percentiles(torch, step, s_up, args.steps)
+        log("per-stack times", json.dumps(per_step))
 
     # per-kernel durations: the same steps again, every launch stamped with a
     # start and an end HIP event by its own dispatch, on its own stream
@@ -463,6 +524,14 @@ def main() -> int:
                     "traffic": load_traffic("graphleap_block", args.workload),
                     "per_launch": f"{fb_flops:.4g} flop (byte floor {fb_bytes:.4g})"}
     log("kernels", json.dumps(kernels))
+    if "mrconv" in kernels or "graphleap_block" in kernels:
+        kernels.setdefault("mrconv", {})["cold_cache"] = cold_gather(
+            w, api, torch, x0, ws["idx"][0], Wd[0], bd[0], out, mr_bytes)
+        log("mrconv warm/cold", json.dumps(kernels["mrconv"]["cold_cache"]))
+    # the whole layer against its roofline: F = Gram + FC flop, Y = the block's byte floor
+    t_floor = max(fb_flops / (peak * 1e12), fb_bytes / (PEAK_HBM_GBS * 1e9))
+    layer_roofline = {"layers_per_s": 1.0 / t_floor, "frac": value * t_floor,
+                      "flop_per_layer": fb_flops, "bytes_per_layer": fb_bytes}
     hu = heads_update(args, w, api, torch, x0, ws["idx"][0], Wd[0])
     if hu is not None:
         kernels["mrconv_heads"] = hu
@@ -491,7 +560,7 @@ def main() -> int:
                    "M": w.M, "C": w.C, "k": w.k, "blocks": w.L, "dilations": dil,
                    "schedule": args.schedule},
         "roofline": roof, "cpu_baseline": cpu, "kernels": kernels, "schedules": schedules,
-        "full_block": full,
+        "full_block": full, "per_stack": per_step, "overlap": overlap, "layer_roofline": layer_roofline,
         "image_layers_per_s": value * w.B, "source_sha": kernel_source_sha(),
     }
     print(json.dumps(line), flush=True)
