@@ -603,7 +603,7 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
                                              C, C, k);
       void* ws;
       if ((s = block_ws(h, B, N, C, dt, rts[l], &ws)) != GL_OK) return s;
-      if (build && !gl::knn_use_stream(M, C, dtb) && !ws) {
+      if (build && !gl::knn_separate(M, C, dtb) && !ws) {
         next = 1 - cur;
         const gl::KnnArgs ka = gl::make_knn_args(a.x_in, keys, B, N, C, M, k, dilations[l + 1],
                                                  iw[next]);
@@ -780,7 +780,7 @@ gl_status enqueue_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, in
   void* mws;
   if ((s = block_ws(h, B, N, C, dt, rt, &mws)) != GL_OK) return s;
   const bool fused = schedule == GL_SCHED_LOOKAHEAD_FUSED && idx_next &&
-                     !gl::knn_use_stream(N, C, dtb) && !mws;
+                     !gl::knn_separate(N, C, dtb) && !mws;
   if (fused) {
     const gl::KnnArgs ka = gl::make_knn_args(u, u, B, N, C, N, k, dil_next, idx_next);
     const gl::MrArgs ma = gl::make_mr_args(u, u, idx_use, p.W_upd, p.b_upd, w.ut, B, N, N, C, C, k);

@@ -85,6 +85,30 @@ __device__ __forceinline__ uint32_t list_element(const uint32_t* L, int e, int l
   return row_broadcast16(v, e & 15, lane);
 }
 
+// Merge this lane's 16 candidates v (one row per 16 lanes) into the row's
+// sorted list L of the KK smallest keys; tau is the list's KK-th key (all ones
+// while the list is not full).  Candidates not below tau are dropped first; the
+// rest are sorted per lane and merged 16 at a time, smallest first.
+template <int R>
+__device__ __forceinline__ void select_chunk(uint32_t* L, uint32_t& tau, uint32_t (&v)[16], int KK,
+                                             int t, int lane) {
+  bool pass = false;
+#pragma unroll
+  for (int m = 0; m < 16; ++m) pass |= v[m] < tau;
+  if (__any(pass)) {
+#pragma unroll
+    for (int m = 0; m < 16; ++m) v[m] = v[m] < tau ? v[m] : 0xffffffffu;
+    sort_regs_asc<16>(v);
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      if (!__any(v[m] < tau)) break;
+      const uint32_t c = sort16_lanes(v[m], t);
+      merge16_into_list<R>(L, c, t);
+      tau = list_element<R>(L, KK - 1, lane);
+    }
+  }
+}
+
 // One 16-row query tile of one image: rows row0 .. row0+15 of x_b against
 // all M keys of keys_b; writes idx_b[row, 0..k-1].  smem holds
 // knn_smem_bytes() bytes (the candidate strip).  Called by all 256 threads.
@@ -215,21 +239,7 @@ __device__ __forceinline__ void knn_tile(char* smem, const char* __restrict__ xb
     }
     __syncthreads();  // the strip is free for the next chunk
 
-    bool pass = false;
-#pragma unroll
-    for (int m = 0; m < 16; ++m) pass |= v[m] < tau;
-    if (__any(pass)) {
-#pragma unroll
-      for (int m = 0; m < 16; ++m) v[m] = v[m] < tau ? v[m] : 0xffffffffu;
-      sort_regs_asc<16>(v);
-#pragma unroll
-      for (int m = 0; m < 16; ++m) {
-        if (!__any(v[m] < tau)) break;
-        const uint32_t c = sort16_lanes(v[m], t);
-        merge16_into_list<R>(L, c, t);
-        tau = list_element<R>(L, KK - 1, lane);
-      }
-    }
+    select_chunk<R>(L, tau, v, KK, t, lane);
   }
 
   // -- dilation and output: idx[row, e/dil] = index of list element e ---------

@@ -91,6 +91,14 @@ EDGE = [
     ("stream_wide_C384_fp32", 1, 70, 300, 384, 9, 2, I.F32, "normal"),
     ("stream_C160_R4", 2, 64, 784, 160, 16, 4, I.BF16, "unit"),
     ("stream_fp32_C96", 1, 130, 3136, 96, 16, 2, I.F32, "normal"),
+    # LDS-staged wide kernel (bf16, C >= 512, M <= 256): key-row buckets 64 / 128 /
+    # 224 / 256, a partial last stage (C = 520), K' = 64, one query row
+    ("wide_M64_bucket", 2, 50, 64, 512, 9, 2, I.BF16, "unit"),
+    ("wide_M65_C520_KK64", 1, 33, 65, 520, 16, 4, I.BF16, "normal"),
+    ("wide_M200_ragged", 3, 97, 200, 512, 9, 3, I.BF16, "unit"),
+    ("wide_M256_max", 1, 70, 256, 640, 16, 2, I.BF16, "unit"),
+    ("wide_self_unnormalised", 2, 196, None, 640, 9, 1, I.BF16, "normal"),
+    ("wide_N1", 2, 1, 30, 512, 3, 1, I.BF16, "unit"),
 ]
 
 
@@ -104,10 +112,11 @@ def test_knn_edges(case):
     _say(label, _knn_case(x, k, d, keys, label=label))
 
 
-def test_knn_duplicates_and_zero_rows():
+@pytest.mark.parametrize("C", [32, 512])
+def test_knn_duplicates_and_zero_rows(C):
     require_gpu()
     g = np.random.default_rng(5)
-    a = g.standard_normal((2, 64, 32))
+    a = g.standard_normal((2, 64, C))
     a[:, 40] = a[:, 3]          # exact duplicate: row 40's nearest must be 3
     a[:, 50] = a[:, 3]
     a[:, 10] = 0.0              # zero rows

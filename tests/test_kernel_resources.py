@@ -1,7 +1,7 @@
 """Register budget of the latency-bound kernels (CPU; compiles for gfx950).
 
 The one-launch block kernel, the fused MRConv and the in-register kNN run at
-three waves per SIMD; if the register allocator has to spill to scratch
+three waves per SIMD, the wide kNN at two; if the register allocator has to spill to scratch
 memory to meet that, they slow down without failing any parity test.  This
 test compiles their sources with the resource-usage remarks and requires no
 scratch for every instantiation of them."""
@@ -16,7 +16,8 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2604_21290_amd", "csrc")
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
-KERNELS = {"block.hip": "block_kernel", "mrconv.hip": "13mrconv_kernel", "knn.hip": "knn_kernel"}
+KERNELS = {"block.hip": "block_kernel", "mrconv.hip": "13mrconv_kernel", "knn.hip": "knn_kernel",
+           "knn_wide.hip": "knn_wide_kernel"}
 
 
 def _usage(src: str, tmp) -> list:
