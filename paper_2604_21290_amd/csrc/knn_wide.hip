@@ -1,5 +1,5 @@
 // Dilated kNN graph build for wide channels and small key sets (Sec. II-B
-// Eq. 4; Sec. IV-B; Alg. 2): bf16 rows of C >= 512 channels, M <= 256 keys.
+// Eq. 4; Sec. IV-B; Alg. 2): bf16 rows of C >= 256 channels, M <= 256 keys.
 //
 // The in-register kernel reads every key row once per 16 query rows; at
 // C = 640 that is 13 full passes over the keys of an image through L2 for each
@@ -59,10 +59,12 @@ size_t wide_smem(int M) {
 // waves per SIMD, for twice the key staging.
 constexpr int kWdQW = 2;
 
-// From C = 512 on it beats the in-register kernel at every shape measured
-// (about 2x at C = 640); at C = 320-400 the two are close and data-dependent.
+// From C = 256 on it beats the in-register kernel at every shape measured
+// (1.1x at C = 400, 1.5x at C = 320, 2.5x at C = 640).  At C = 192 it is
+// faster too, but the build then needs its own launch, and the one-launch
+// block with the in-register build is faster than the two launches.
 bool knn_use_wide(int M, int C, int dt_bf16) {
-  return dt_bf16 && M <= kWdMaxKeys && C >= 512 && C % 8 == 0;
+  return dt_bf16 && M <= kWdMaxKeys && C >= 256 && C % 8 == 0;
 }
 
 template <int R, int QW, int KROWS>
@@ -111,12 +113,20 @@ __global__ __launch_bounds__(kWdThreads) void knn_wide_kernel(KnnArgs a) {
   };
   auto sstore = [&](int s, int buf) {
     char* d = smem + buf * G::kBuf;
-    const bool in = s * kWdStep + slot < rowb;
+    if ((s + 1) * kWdStep <= rowb) {  // wave-uniform: the whole stage is inside C
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const u32x4 v = in ? st[i] : u32x4{0, 0, 0, 0};
-      ss[i] = sumsq_bf16x8(__builtin_bit_cast(uint4, v), ss[i]);
-      *reinterpret_cast<u32x4*>(d + lo[i]) = v;
+      for (int i = 0; i < NV; ++i) {
+        ss[i] = sumsq_bf16x8(__builtin_bit_cast(uint4, st[i]), ss[i]);
+        *reinterpret_cast<u32x4*>(d + lo[i]) = st[i];
+      }
+    } else {
+      const bool in = s * kWdStep + slot < rowb;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const u32x4 v = in ? st[i] : u32x4{0, 0, 0, 0};
+        ss[i] = sumsq_bf16x8(__builtin_bit_cast(uint4, v), ss[i]);
+        *reinterpret_cast<u32x4*>(d + lo[i]) = v;
+      }
     }
   };
 
@@ -134,13 +144,14 @@ __global__ __launch_bounds__(kWdThreads) void knn_wide_kernel(KnnArgs a) {
     for (int kk = 0; kk < kWdStep / 64; ++kk) {
       const uint4 af = *reinterpret_cast<const uint4*>(sa + (16 * wr + t) * kWdRow + kk * 64 + g * 16);
 #pragma unroll
+      // every staged key tile is multiplied (tiles past M hold repeated rows and
+      // are masked in the epilogue): a branch here would make the compiler copy
+      // the accumulators around it
       for (int j = 0; j < NKT; ++j) {
         const int kt = wk + SPLIT * j;
-        if (kt < nkt) {  // wave-uniform
-          const uint4 bf =
-              *reinterpret_cast<const uint4*>(sa + (QR + 16 * kt + t) * kWdRow + kk * 64 + g * 16);
-          acc[j] = mfma_bf16(af, bf, acc[j]);
-        }
+        const uint4 bf =
+            *reinterpret_cast<const uint4*>(sa + (QR + 16 * kt + t) * kWdRow + kk * 64 + g * 16);
+        acc[j] = mfma_bf16(af, bf, acc[j]);
       }
     }
     if (s + 1 < nstage) sstore(s + 1, (s + 1) & 1);

@@ -91,7 +91,7 @@ EDGE = [
     ("stream_wide_C384_fp32", 1, 70, 300, 384, 9, 2, I.F32, "normal"),
     ("stream_C160_R4", 2, 64, 784, 160, 16, 4, I.BF16, "unit"),
     ("stream_fp32_C96", 1, 130, 3136, 96, 16, 2, I.F32, "normal"),
-    # LDS-staged wide kernel (bf16, C >= 512, M <= 256): key-row buckets 64 / 128 /
+    # LDS-staged wide kernel (bf16, C >= 256, M <= 256): key-row buckets 64 / 128 /
     # 224 / 256, a partial last stage (C = 520), K' = 64, one query row
     ("wide_M64_bucket", 2, 50, 64, 512, 9, 2, I.BF16, "unit"),
     ("wide_M65_C520_KK64", 1, 33, 65, 520, 16, 4, I.BF16, "normal"),
@@ -99,6 +99,7 @@ EDGE = [
     ("wide_M256_max", 1, 70, 256, 640, 16, 2, I.BF16, "unit"),
     ("wide_self_unnormalised", 2, 196, None, 640, 9, 1, I.BF16, "normal"),
     ("wide_N1", 2, 1, 30, 512, 3, 1, I.BF16, "unit"),
+    ("wide_C264_partial", 2, 45, 100, 264, 9, 2, I.BF16, "normal"),
 ]
 
 
