@@ -7,10 +7,10 @@
 //   * FC1, FC2 + residual and the FFN of the full ViG block (Eq. 11, 14, 15):
 //     act_in = GELU gives sigma(U~) W_out^T, act_out = GELU the FFN's hidden
 //     layer, residual the two skip connections.
-// A workgroup owns a 64 x 64 output tile, so W is read once per 64 rows and
-// A once per 64 output channels.
-//   - 4 waves in a 2 x 2 layout; each wave holds a 32 x 32 accumulator block
-//     (2 x 2 MFMA tiles of 16 x 16) in registers.
+// A workgroup owns a 64 x 64 or 128 x 128 output tile, so W is read once per
+// 64 or 128 rows and A once per 64 or 128 output channels.
+//   - 4 waves in a 2 x 2 layout, or 8 in a 4 x 2 layout; each wave holds its
+//     block of the tile (2 x 2 ... 2 x 4 MFMA tiles of 16 x 16) in registers.
 //   - The contraction runs in stages of 256 bytes per row (4 MFMA k-steps:
 //     128 bf16 or 64 fp32 channels), so the short contractions of the ViG
 //     layers (K = 192 .. 1280) take 1 .. 10 stages, each one global round
@@ -27,18 +27,24 @@
 
 namespace gl {
 
-constexpr int kGmThreads = 256;
+constexpr int kGm128Waves = 8;  // waves of the 128 x 128 configuration
 
 // Tile configurations: BM x BM output tiles, STEP bytes of K per row per stage.
 //   64 x 64, 256 B: short contractions or few tiles (the ViG block's layers);
 //   128 x 128, 128 B: large GEMMs (e.g. the ViG-B update), where W and A are
 //   re-read half as often.
-template <int BM, int STEP>
+// NW waves: 4 in a 2 x 2 layout (wave tile BM/2 x BM/2), or 8 in a 4 x 2
+// layout (BM/4 x BM/2), which keeps twice as many waves in flight per CU for
+// the same LDS.
+template <int BM, int STEP, int NW = 4>
 struct GemmCfg {
+  static constexpr int kThreads = 64 * NW;
   static constexpr int kRow = STEP + 16;                 // LDS row stride
   static constexpr int kTile = BM * kRow;                // one operand tile of one stage
-  static constexpr int kVec = BM * STEP / 16 / kGmThreads;  // 16-byte loads per thread, operand
-  static constexpr int kTpw = BM / 32;                   // MFMA tiles per wave and dimension
+  static constexpr int kVec = BM * STEP / 16 / kThreads; // 16-byte loads per thread, operand
+  static constexpr int kWm = NW == 8 ? 4 : 2;            // waves along the rows
+  static constexpr int kTpwM = BM / 16 / kWm;            // MFMA tiles per wave, rows
+  static constexpr int kTpwN = BM / 32;                  // MFMA tiles per wave, columns
   static constexpr size_t kSmem = (size_t)4 * kTile;
 };
 
@@ -62,12 +68,13 @@ __device__ __forceinline__ u32x4 gelu_vec(u32x4 v) {
   return __builtin_bit_cast(u32x4, f);
 }
 
-template <int DT, int ACT_IN, int ACT_OUT, int BM, int STEP>
-__global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
+template <int DT, int ACT_IN, int ACT_OUT, int BM, int STEP, int NW = 4>
+__global__ __launch_bounds__(64 * NW) void gemm_nt_kernel(GemmArgs a) {
   extern __shared__ __align__(16) char smem[];
-  using G = GemmCfg<BM, STEP>;
+  using G = GemmCfg<BM, STEP, NW>;
   constexpr int kGmBM = BM, kGmBN = BM, kGmStep = STEP, kGmRow = G::kRow, kGmTile = G::kTile;
-  constexpr int kGmVec = G::kVec, TPW = G::kTpw, SPR = STEP / 16;
+  constexpr int kGmVec = G::kVec, TPWM = G::kTpwM, TPWN = G::kTpwN, SPR = STEP / 16;
+  constexpr int kGmThreads = G::kThreads;
   const int R = a.R, K = a.K, Cout = a.Cout;
   const int rowb = K * (DT ? 2 : 4);        // a multiple of 16
   const int nstages = (rowb + kGmStep - 1) / kGmStep;
@@ -77,7 +84,7 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
   const int m0 = mt * kGmBM, n0 = nt * kGmBN;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, t = lane & 15;
-  const int wm = w >> 1, wn = w & 1;       // the wave's quadrant (16 TPW rows and columns)
+  const int wm = w >> 1, wn = w & 1;       // the wave's block: 16 TPWM rows, 16 TPWN columns
 
   // staging: vector v = tid + 256 i of a tile is row v / SPR, 16-byte slot v % SPR
   const char* Ab = static_cast<const char*>(a.A);
@@ -113,11 +120,11 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
     }
   };
 
-  f32x4 acc[TPW][TPW];
+  f32x4 acc[TPWM][TPWN];
 #pragma unroll
-  for (int i = 0; i < TPW; ++i)
+  for (int i = 0; i < TPWM; ++i)
 #pragma unroll
-    for (int j = 0; j < TPW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TPWN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   gload(0);
   sstore(0);
@@ -127,18 +134,19 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
     const char* sa = smem + (s & 1) * 2 * kGmTile;
 #pragma unroll
     for (int kk = 0; kk < kGmStep / 64; ++kk) {
-      uint4 af[TPW], bf[TPW];
+      uint4 af[TPWM], bf[TPWN];
 #pragma unroll
-      for (int i = 0; i < TPW; ++i) {
-        af[i] = *reinterpret_cast<const uint4*>(sa + (wm * 16 * TPW + i * 16 + t) * kGmRow +
+      for (int i = 0; i < TPWM; ++i)
+        af[i] = *reinterpret_cast<const uint4*>(sa + (wm * 16 * TPWM + i * 16 + t) * kGmRow +
                                                 kk * 64 + g * 16);
-        bf[i] = *reinterpret_cast<const uint4*>(sa + kGmTile + (wn * 16 * TPW + i * 16 + t) * kGmRow +
+#pragma unroll
+      for (int j = 0; j < TPWN; ++j)
+        bf[j] = *reinterpret_cast<const uint4*>(sa + kGmTile + (wn * 16 * TPWN + j * 16 + t) * kGmRow +
                                                 kk * 64 + g * 16);
-      }
 #pragma unroll
-      for (int i = 0; i < TPW; ++i)
+      for (int i = 0; i < TPWM; ++i)
 #pragma unroll
-        for (int j = 0; j < TPW; ++j) {
+        for (int j = 0; j < TPWN; ++j) {
           if (DT) {
             acc[i][j] = mfma_bf16(af[i], bf[j], acc[i][j]);
           } else {
@@ -157,8 +165,8 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
 
   // -- epilogue: lane (g, t) of tile (i, j) holds rows 4g..4g+3, column t --------
 #pragma unroll
-  for (int j = 0; j < TPW; ++j) {
-    const int n = n0 + wn * 16 * TPW + j * 16 + t;
+  for (int j = 0; j < TPWN; ++j) {
+    const int n = n0 + wn * 16 * TPWN + j * 16 + t;
     if (n >= Cout) continue;
     float bn = 0.f;
     if (a.bias) {
@@ -166,10 +174,10 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
               : static_cast<const float*>(a.bias)[n];
     }
 #pragma unroll
-    for (int i = 0; i < TPW; ++i)
+    for (int i = 0; i < TPWM; ++i)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int row = m0 + wm * 16 * TPW + i * 16 + 4 * g + v;
+        const int row = m0 + wm * 16 * TPWM + i * 16 + 4 * g + v;
         if (row >= R) continue;
         float y = acc[i][j][v] + bn;
         if (ACT_OUT) y = gelu_f32(y);
@@ -184,13 +192,13 @@ __global__ __launch_bounds__(kGmThreads) void gemm_nt_kernel(GemmArgs a) {
   }
 }
 
-template <int BM, int STEP>
+template <int BM, int STEP, int NW = 4>
 const void* gemm_fn(int v) {
   static const void* const fns[8] = {
-      (const void*)&gemm_nt_kernel<0, 0, 0, BM, STEP>, (const void*)&gemm_nt_kernel<0, 0, 1, BM, STEP>,
-      (const void*)&gemm_nt_kernel<0, 1, 0, BM, STEP>, (const void*)&gemm_nt_kernel<0, 1, 1, BM, STEP>,
-      (const void*)&gemm_nt_kernel<1, 0, 0, BM, STEP>, (const void*)&gemm_nt_kernel<1, 0, 1, BM, STEP>,
-      (const void*)&gemm_nt_kernel<1, 1, 0, BM, STEP>, (const void*)&gemm_nt_kernel<1, 1, 1, BM, STEP>};
+      (const void*)&gemm_nt_kernel<0, 0, 0, BM, STEP, NW>, (const void*)&gemm_nt_kernel<0, 0, 1, BM, STEP, NW>,
+      (const void*)&gemm_nt_kernel<0, 1, 0, BM, STEP, NW>, (const void*)&gemm_nt_kernel<0, 1, 1, BM, STEP, NW>,
+      (const void*)&gemm_nt_kernel<1, 0, 0, BM, STEP, NW>, (const void*)&gemm_nt_kernel<1, 0, 1, BM, STEP, NW>,
+      (const void*)&gemm_nt_kernel<1, 1, 0, BM, STEP, NW>, (const void*)&gemm_nt_kernel<1, 1, 1, BM, STEP, NW>};
   return fns[v];
 }
 
@@ -200,15 +208,20 @@ hipError_t launch_gemm_nt(const GemmArgs& a, int dt_bf16, hipStream_t stream, hi
   const size_t rowb = (size_t)a.K * (dt_bf16 ? 2 : 4);
   // large tiles once they alone give every CU a tile and K is long
   const long tiles128 = (long)((a.R + 127) / 128) * ((a.Cout + 127) / 128);
-  const dim3 block(kGmThreads);
   if (tiles128 >= 256 && rowb >= 1024) {
-    const dim3 grid((unsigned)tiles128);
-    return launch_with_smem(gemm_fn<128, 128>(v), grid, block, GemmCfg<128, 128>::kSmem, stream,
-                            ev0, ev1, a);
+    constexpr int NW = kGm128Waves;
+    const dim3 grid((unsigned)tiles128), block(64 * NW);
+    return launch_with_smem(gemm_fn<128, 128, NW>(v), grid, block, GemmCfg<128, 128, NW>::kSmem,
+                            stream, ev0, ev1, a);
   }
+  // with a GELU on either side the 64 x 64 tile is VALU-heavy, and 8 waves
+  // overlap it better; plain products are as fast or faster with 4
   const dim3 grid((unsigned)(((a.R + 63) / 64) * ((a.Cout + 63) / 64)));
-  return launch_with_smem(gemm_fn<64, 256>(v), grid, block, GemmCfg<64, 256>::kSmem, stream, ev0,
-                          ev1, a);
+  if (a.act_in || a.act_out)
+    return launch_with_smem(gemm_fn<64, 256, 8>(v), grid, dim3(512), GemmCfg<64, 256, 8>::kSmem,
+                            stream, ev0, ev1, a);
+  return launch_with_smem(gemm_fn<64, 256, 4>(v), grid, dim3(256), GemmCfg<64, 256, 4>::kSmem,
+                          stream, ev0, ev1, a);
 }
 
 }  // namespace gl
