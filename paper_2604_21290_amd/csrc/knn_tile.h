@@ -132,9 +132,9 @@ __device__ __forceinline__ void knn_tile(char* smem, const char* __restrict__ xb
   // Operands of one batch: k-steps s0 .. s0+KU-1 of the query rows and of the
   // wave's key tiles w, w+4, w+8, w+12 in the chunk at chunk0 (rows clamped;
   // channels past C read channel 0 and are zeroed when used).  Tiles past the
-  // chunk repeat tile w; they are multiplied like the others and dropped in
-  // the epilogue, since a branch around the MFMAs makes the compiler copy the
-  // accumulators between register files at every step.
+  // chunk repeat tile w; in bf16 they are multiplied like the others and
+  // dropped in the epilogue, since a branch around the MFMAs makes the compiler
+  // copy the accumulators between register files at every step.
   uint4 bf[kKnnKU][kKnnTPP], af[kKnnKU];
   auto load_batch = [&](int chunk0, int ntiles, int s0) {
     int kr[kKnnTPP];
@@ -185,6 +185,9 @@ __device__ __forceinline__ void knn_tile(char* smem, const char* __restrict__ xb
           if (chunk0 == 0) qss = DT ? sumsq_bf16x8(a, qss) : sumsq_f32x4(a, qss);
 #pragma unroll
           for (int p = 0; p < kKnnTPP; ++p) {
+            // (fp32 keeps the test: its four MFMAs per step leave no registers
+            // for the extra tile in the one-launch block)
+            if (!DT && w + 4 * p >= ntiles) continue;
             const uint4 b = in ? bf[u][p] : make_uint4(0, 0, 0, 0);
             if (DT) {
               acc[p] = mfma_bf16(a, b, acc[p]);
