@@ -38,6 +38,11 @@ LIN = [
     ("ragged_k_tail", 131, 40, 70, 1, 1, True, True, I.BF16),
     ("fp32_all", 257, 36, 130, 1, 1, True, True, I.F32),
     ("one_row", 1, 8, 1, 0, 0, False, False, I.BF16),
+    # the 128 x 128, 8-wave tile: ragged rows, columns and last K stage; GELU on
+    # either side; fp32
+    ("big128_ragged", 33000, 520, 200, 0, 0, True, True, I.BF16),
+    ("big128_gelu_out", 16384, 640, 640, 0, 1, False, True, I.BF16),
+    ("big128_gelu_in_fp32", 33000, 256, 260, 1, 0, True, True, I.F32),
 ]
 
 
