@@ -102,16 +102,18 @@ __global__ __launch_bounds__(kWdThreads) void knn_wide_kernel(KnnArgs a) {
                     : kb + (size_t)min(r - QR, M - 1) * rowb + slot;
     lo[i] = r * kWdRow + slot;
   }
-  u32x4 st[NV];
+  // two register sets: while one stage is multiplied out of LDS, the next is
+  // waiting in one set and the one after is on its way into the other
+  u32x4 st0[NV], st1[NV];
   float ss[NV];
 #pragma unroll
   for (int i = 0; i < NV; ++i) ss[i] = 0.f;
-  auto gload = [&](int s) {
+  auto gload = [&](u32x4 (&st)[NV], int s) {
     const int off = s * kWdStep + slot < rowb ? s * kWdStep : 0;
 #pragma unroll
     for (int i = 0; i < NV; ++i) st[i] = *reinterpret_cast<const u32x4*>(src[i] + off);
   };
-  auto sstore = [&](int s, int buf) {
+  auto sstore = [&](u32x4 (&st)[NV], int s, int buf) {
     char* d = smem + buf * G::kBuf;
     if ((s + 1) * kWdStep <= rowb) {  // wave-uniform: the whole stage is inside C
 #pragma unroll
@@ -133,20 +135,15 @@ __global__ __launch_bounds__(kWdThreads) void knn_wide_kernel(KnnArgs a) {
   f32x4 acc[NKT];
 #pragma unroll
   for (int j = 0; j < NKT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  gload(0);
-  sstore(0, 0);
-  __syncthreads();
-  for (int s = 0; s < nstage; ++s) {
-    if (s + 1 < nstage) gload(s + 1);
+  auto multiply = [&](int s) {
     const char* sa = smem + (s & 1) * G::kBuf;
 #pragma unroll
     for (int kk = 0; kk < kWdStep / 64; ++kk) {
       const uint4 af = *reinterpret_cast<const uint4*>(sa + (16 * wr + t) * kWdRow + kk * 64 + g * 16);
-#pragma unroll
       // every staged key tile is multiplied (tiles past M hold repeated rows and
       // are masked in the epilogue): a branch here would make the compiler copy
       // the accumulators around it
+#pragma unroll
       for (int j = 0; j < NKT; ++j) {
         const int kt = wk + SPLIT * j;
         const uint4 bf =
@@ -154,7 +151,28 @@ __global__ __launch_bounds__(kWdThreads) void knn_wide_kernel(KnnArgs a) {
         acc[j] = mfma_bf16(af, bf, acc[j]);
       }
     }
-    if (s + 1 < nstage) sstore(s + 1, (s + 1) & 1);
+  };
+
+  // At the top of step s, stage s is in LDS buffer s & 1 and stage s + 1 is in
+  // flight into st1 (even s) or st0 (odd s).  The loop runs whole pairs of
+  // steps with no conditions, so that each register set keeps its role and no
+  // branch surrounds the MFMAs: stages past the last (at most two, plus one
+  // when the count is odd) load in-range addresses and are stored as zeros,
+  // which add nothing to the accumulators or the norms.
+  const int npair = (nstage + 1) >> 1;
+  gload(st0, 0);
+  gload(st1, 1);
+  sstore(st0, 0, 0);
+  __syncthreads();
+  for (int pr = 0; pr < npair; ++pr) {
+    const int s = 2 * pr;
+    gload(st0, s + 2);
+    multiply(s);
+    sstore(st1, s + 1, 1);
+    __syncthreads();
+    gload(st1, s + 3);
+    multiply(s + 1);
+    sstore(st0, s + 2, 0);
     __syncthreads();
   }
 
