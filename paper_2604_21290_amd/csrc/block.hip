@@ -11,6 +11,7 @@
 // Workgroup ids are split between the roles in groups of 8 (one per XCD), so
 // both roles spread over every XCD from the first wave of dispatch on.
 #include "knn_tile.h"
+#include "knn_wide.h"
 #include "mrconv_tile.h"
 
 namespace gl {
@@ -33,13 +34,19 @@ __device__ __forceinline__ bool block_role_is_build(int i, int nb, int nu, int* 
   return false;
 }
 
-template <int DT, int R, int RT, int KB>
+// WK > 0: the build role is the LDS-staged tile (32 query rows, WK key rows
+// staged) instead of the in-register one (16 query rows).
+template <int DT, int R, int RT, int KB, int WK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void block_kernel(KnnArgs ka, MrArgs ma, int nb, int nu) {
   extern __shared__ __align__(16) char smem[];
   constexpr int ES = DT ? 2 : 4;
   int j;
   if (block_role_is_build(blockIdx.x, nb, nu, &j)) {
     j = xcd_remap(j, nb);
+    if constexpr (WK > 0) {
+      knn_wide_tile<R, kWdQW, WK, false>(smem, ka, j);
+      return;
+    }
     const int nt = (ka.N + kKnnRows - 1) / kKnnRows;
     const int b = j / nt, tile = j - b * nt;
     knn_tile<DT, R>(smem, static_cast<const char*>(ka.x) + (size_t)b * ka.N * ka.C * ES,
@@ -52,36 +59,50 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) voi
   }
 }
 
-template <int DT, int R, int RT>
+template <int DT, int R, int RT, int WK>
 const void* block_fn_kb(int KB) {
   switch (KB) {
-    case 9: return (const void*)&block_kernel<DT, R, RT, 9>;
-    case 16: return (const void*)&block_kernel<DT, R, RT, 16>;
-    case 32: return (const void*)&block_kernel<DT, R, RT, 32>;
-    default: return (const void*)&block_kernel<DT, R, RT, 64>;
+    case 9: return (const void*)&block_kernel<DT, R, RT, 9, WK>;
+    case 16: return (const void*)&block_kernel<DT, R, RT, 16, WK>;
+    case 32: return (const void*)&block_kernel<DT, R, RT, 32, WK>;
+    default: return (const void*)&block_kernel<DT, R, RT, 64, WK>;
   }
 }
 
-template <int DT, int R>
+template <int DT, int R, int WK>
 const void* block_fn_rt(int RT, int KB) {
-  return RT == 2 ? block_fn_kb<DT, R, 2>(KB) : block_fn_kb<DT, R, 1>(KB);
+  return RT == 2 ? block_fn_kb<DT, R, 2, WK>(KB) : block_fn_kb<DT, R, 1, WK>(KB);
 }
 
-template <int DT>
+template <int DT, int WK = 0>
 const void* block_fn(int R, int RT, int KB) {
-  return R == 1 ? block_fn_rt<DT, 1>(RT, KB)
-                : R == 2 ? block_fn_rt<DT, 2>(RT, KB) : block_fn_rt<DT, 4>(RT, KB);
+  return R == 1 ? block_fn_rt<DT, 1, WK>(RT, KB)
+                : R == 2 ? block_fn_rt<DT, 2, WK>(RT, KB) : block_fn_rt<DT, 4, WK>(RT, KB);
+}
+
+// Key rows the build role stages when it is the LDS-staged tile (the
+// standalone build would use that kernel too), else 0: 128 up to 128 keys,
+// 224 up to 224.  Larger key sets are not built inside the block.
+int block_wide_rows(const KnnArgs& ka, int dt_bf16) {
+  if (!knn_use_wide(ka.M, ka.C, dt_bf16)) return 0;
+  return ka.M <= 128 ? 128 : 224;
 }
 
 hipError_t launch_block(const KnnArgs& ka, const MrArgs& ma, int dt_bf16, int rt,
                         hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
-  const int nb = ka.B * ((ka.N + kKnnRows - 1) / kKnnRows);
+  const int wk = block_wide_rows(ka, dt_bf16);
+  const bool wide = wk > 0;
+  const int qr = wide ? 16 * kWdQW : kKnnRows;
+  const int nb = ka.B * ((ka.N + qr - 1) / qr);
   const int TM = 16 * rt;
   const int nu = (ma.R + TM - 1) / TM;
-  const size_t smem = std::max(knn_smem_bytes(ka.C, dt_bf16),
+  const size_t wsm = wk == 128 ? WideGeom<kWdQW, 128>::kSmem : WideGeom<kWdQW, 224>::kSmem;
+  const size_t smem = std::max(wide ? wsm : knn_smem_bytes(ka.C, dt_bf16),
                                mrconv_smem_bytes(ma.C, ma.k, dt_bf16, rt));
   const int R = knn_list_regs(ka.KK), KB = mrconv_k_bucket(ma.k);
-  const void* fn = dt_bf16 ? block_fn<1>(R, rt, KB) : block_fn<0>(R, rt, KB);
+  const void* fn = wk == 224 ? block_fn<1, 224>(R, rt, KB)
+                   : wk == 128 ? block_fn<1, 128>(R, rt, KB)
+                   : dt_bf16 ? block_fn<1>(R, rt, KB) : block_fn<0>(R, rt, KB);
   const dim3 grid(nb + nu), block(256);
   struct {
     KnnArgs ka;

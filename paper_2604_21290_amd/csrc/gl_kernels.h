@@ -76,12 +76,13 @@ hipError_t launch_knn(const void* x, const void* keys, int B, int N, int C, int 
 bool knn_use_stream(int M, int C, int dt_bf16);
 hipError_t launch_knn_stream(const KnnArgs& a, int dt_bf16, hipStream_t stream, hipEvent_t ev0,
                              hipEvent_t ev1);
-// Wide bf16 rows (C >= 256) against at most 256 keys use the LDS-staged kernel.
+// bf16 rows of C >= 128 against at most 256 keys use the LDS-staged kernel.
 bool knn_use_wide(int M, int C, int dt_bf16);
 hipError_t launch_knn_wide(const KnnArgs& a, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
-// Either of the two: the build is not the in-register tile the one-launch block embeds.
+// The build cannot be a role of the one-launch block: streamed keys, or the
+// LDS-staged tile with more key rows than the block's variants stage (224).
 inline bool knn_separate(int M, int C, int dt_bf16) {
-  return knn_use_stream(M, C, dt_bf16) || knn_use_wide(M, C, dt_bf16);
+  return knn_use_stream(M, C, dt_bf16) || (knn_use_wide(M, C, dt_bf16) && M > 224);
 }
 
 int mrconv_lds_row_bytes(int C, int dt_bf16);
