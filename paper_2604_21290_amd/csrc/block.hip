@@ -16,6 +16,10 @@
 
 namespace gl {
 
+constexpr int kBlockWideWaves = 2;     // waves per SIMD the LDS-staged variant is compiled for
+constexpr bool kBlockWideDB = true;    // its build role with two staging register sets
+constexpr bool kBlockWideT3 = true;    // its update role gathering in one round
+
 // Role of dispatch id i among nb build and nu update workgroups; j is the
 // workgroup's index within its role.
 __device__ __forceinline__ bool block_role_is_build(int i, int nb, int nu, int* j) {
@@ -34,38 +38,61 @@ __device__ __forceinline__ bool block_role_is_build(int i, int nb, int nu, int* 
   return false;
 }
 
-// WK > 0: the build role is the LDS-staged tile (32 query rows, WK key rows
-// staged) instead of the in-register one (16 query rows).
+// Both roles of one launch.  WK > 0: the build role is the LDS-staged tile
+// (32 query rows, WK key rows staged) instead of the in-register one (16 query
+// rows); that variant takes 74 KB of LDS, so two workgroups per CU, and is
+// compiled for two waves per SIMD, which leaves it the registers for the
+// tile's second staging set and for a one-round gather.
 template <int DT, int R, int RT, int KB, int WK>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void block_kernel(KnnArgs ka, MrArgs ma, int nb, int nu) {
-  extern __shared__ __align__(16) char smem[];
+__device__ __forceinline__ void block_body(char* smem, const KnnArgs& ka, const MrArgs& ma, int nb, int nu) {
   constexpr int ES = DT ? 2 : 4;
   int j;
   if (block_role_is_build(blockIdx.x, nb, nu, &j)) {
     j = xcd_remap(j, nb);
     if constexpr (WK > 0) {
-      knn_wide_tile<R, kWdQW, WK, false>(smem, ka, j);
-      return;
+      knn_wide_tile<R, kWdQW, WK, kBlockWideDB>(smem, ka, j);
+    } else {
+      const int nt = (ka.N + kKnnRows - 1) / kKnnRows;
+      const int b = j / nt, tile = j - b * nt;
+      knn_tile<DT, R>(smem, static_cast<const char*>(ka.x) + (size_t)b * ka.N * ka.C * ES,
+                      static_cast<const char*>(ka.keys) + (size_t)b * ka.M * ka.C * ES, ka.N, ka.C,
+                      ka.M, ka.k, ka.dil, ka.KK, ka.ib, ka.qscale, ka.qmax, tile * kKnnRows,
+                      ka.idx + (size_t)b * ka.N * ka.k);
     }
-    const int nt = (ka.N + kKnnRows - 1) / kKnnRows;
-    const int b = j / nt, tile = j - b * nt;
-    knn_tile<DT, R>(smem, static_cast<const char*>(ka.x) + (size_t)b * ka.N * ka.C * ES,
-                    static_cast<const char*>(ka.keys) + (size_t)b * ka.M * ka.C * ES, ka.N, ka.C,
-                    ka.M, ka.k, ka.dil, ka.KK, ka.ib, ka.qscale, ka.qmax, tile * kKnnRows,
-                    ka.idx + (size_t)b * ka.N * ka.k);
   } else {
     j = xcd_remap(j, nu);
-    mrconv_tile<DT, RT, KB>(smem, ma, j * 16 * RT);
+    mrconv_tile<DT, RT, KB, false, (WK > 0) && kBlockWideT3>(smem, ma, j * 16 * RT);
   }
+}
+
+template <int DT, int R, int RT, int KB, int WK>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void block_kernel(KnnArgs ka, MrArgs ma, int nb, int nu) {
+  extern __shared__ __align__(16) char smem[];
+  block_body<DT, R, RT, KB, WK>(smem, ka, ma, nb, nu);
+}
+
+template <int DT, int R, int RT, int KB, int WK>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kBlockWideWaves, 8))) void block_kernel_wide(KnnArgs ka, MrArgs ma, int nb, int nu) {
+  extern __shared__ __align__(16) char smem[];
+  block_body<DT, R, RT, KB, WK>(smem, ka, ma, nb, nu);
 }
 
 template <int DT, int R, int RT, int WK>
 const void* block_fn_kb(int KB) {
-  switch (KB) {
-    case 9: return (const void*)&block_kernel<DT, R, RT, 9, WK>;
-    case 16: return (const void*)&block_kernel<DT, R, RT, 16, WK>;
-    case 32: return (const void*)&block_kernel<DT, R, RT, 32, WK>;
-    default: return (const void*)&block_kernel<DT, R, RT, 64, WK>;
+  if constexpr (WK > 0) {
+    switch (KB) {
+      case 9: return (const void*)&block_kernel_wide<DT, R, RT, 9, WK>;
+      case 16: return (const void*)&block_kernel_wide<DT, R, RT, 16, WK>;
+      case 32: return (const void*)&block_kernel_wide<DT, R, RT, 32, WK>;
+      default: return (const void*)&block_kernel_wide<DT, R, RT, 64, WK>;
+    }
+  } else {
+    switch (KB) {
+      case 9: return (const void*)&block_kernel<DT, R, RT, 9, WK>;
+      case 16: return (const void*)&block_kernel<DT, R, RT, 16, WK>;
+      case 32: return (const void*)&block_kernel<DT, R, RT, 32, WK>;
+      default: return (const void*)&block_kernel<DT, R, RT, 64, WK>;
+    }
   }
 }
 

@@ -81,7 +81,9 @@ __device__ __forceinline__ void mr_load_w(uint4 (&bw)[kMrKU][4], const MrArgs& a
 // (dst + r * dst_stride, LDS or global memory) receives [x_i | m_i] with
 // m_i = max_t keys[idx[i, t]] - x_i.  sIdx holds the TM x k neighbour lists
 // (clamped to [0, M)).  Rows past R are not written.  Called by all 256 threads.
-template <int DT, int KB>
+// T3: three tasks per thread in flight instead of two (a caller with registers
+// to spare takes the 32-node tile's 768 tasks of C = 192 in one round).
+template <int DT, int KB, bool T3 = false>
 __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM,
                                                const int32_t* sIdx, char* dst, size_t dst_stride) {
   constexpr int ES = DT ? 2 : 4;
@@ -92,7 +94,7 @@ __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM
   // Each task is one (node, 16-byte channel vector); with a small neighbour
   // bucket two tasks keep their loads in flight together.
   constexpr int KG = KB < 16 ? KB : 16;    // neighbour loads in flight per group
-  constexpr int TPT = KB <= 9 ? 2 : 1;     // tasks per thread per iteration
+  constexpr int TPT = KB <= 9 ? (T3 ? 3 : 2) : 1;  // tasks per thread per iteration
   const int ntask = TM * CG;
   for (int e0 = tid; e0 < ntask; e0 += TPT * kMrThreads) {
     float mx[TPT][VEC];
@@ -155,7 +157,7 @@ __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM
 // TM = 16*RT nodes starting at flattened node row0.  smem holds
 // mrconv_smem_bytes(C, k, RT) bytes.  Called by all 256 threads.
 // HEADS: the multi-head update (a.heads > 1), which skips the zero blocks of W.
-template <int DT, int RT, int KB, bool HEADS = false>
+template <int DT, int RT, int KB, bool HEADS = false, bool T3 = false>
 __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row0) {
   constexpr int TM = 16 * RT;
   constexpr int ES = DT ? 2 : 4;
@@ -186,7 +188,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
   if (w < NCT) mr_load_w<DT, HEADS>(bw, a, Wb, w, 0, 0, K2, Cout, g, t);
   __syncthreads();
 
-  mr_gather_rows<DT, KB>(a, row0, TM, sIdx, sA, lds_row);
+  mr_gather_rows<DT, KB, T3>(a, row0, TM, sIdx, sA, lds_row);
   __syncthreads();
 
   // -- FC on MFMA -----------------------------------------------------------------
