@@ -132,7 +132,8 @@ gl_status gl_pool_keys(const void* x, int B, int H, int W, int C, int r, gl_dtyp
  *        [0, M) inside the kernel (no fault; the result is then undefined).
  *   W    [Cout, 2C] (dt); bias [Cout] (dt) or NULL for zero bias.
  *   out  [B, N, Cout] (dt); must not overlap x, keys, idx, W or bias.
- * Limits: 1 <= k <= GL_MAX_K; Cout >= 1.
+ * Limits: 1 <= k <= GL_MAX_K; Cout >= 1; one image's keys M * C * s bytes
+ * below 32 GiB (2^31 16-byte vectors), else GL_ERR_BAD_SHAPE.
  * -------------------------------------------------------------------------*/
 gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
                     const int32_t* idx, int k, const void* W, const void* bias, int Cout,

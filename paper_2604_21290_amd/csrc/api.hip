@@ -99,6 +99,9 @@ gl_status check_mrconv(const void* x, int B, int N, int C, const void* keys, int
   if (k < 1 || k > GL_MAX_K) return fail(GL_ERR_BAD_K, "mrconv: k=%d outside [1, %d]", k, GL_MAX_K);
   if (C % vec_width(dt))
     return fail(GL_ERR_UNSUPPORTED, "mrconv: C=%d must be a multiple of %d", C, vec_width(dt));
+  // the kernels address a neighbour row by its offset in 16-byte vectors (int32)
+  if ((long long)M * (C / vec_width(dt)) > INT_MAX)
+    return fail(GL_ERR_BAD_SHAPE, "mrconv: M=%d rows of C=%d exceed 2^31 16-byte vectors per image", M, C);
   const int dtb = dt == GL_BF16;
   // rt = 0: the fused LDS tile does not fit; the two-pass form is used
   int rt = gl::mrconv_row_tiles(C, k, dtb, 65536);

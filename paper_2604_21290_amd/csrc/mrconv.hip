@@ -64,7 +64,7 @@ __global__ __launch_bounds__(kMrThreads) void mr_gather_kernel(MrArgs a, void* x
   for (int e = threadIdx.x; e < kMrGatherRows * a.k; e += kMrThreads) {
     const int r = e / a.k, tt = e - r * a.k, row = row0 + r;
     const int j = row < a.R ? a.idx[(size_t)row * a.k + tt] : 0;
-    sIdx[e] = min(max(j, 0), a.M - 1);
+    sIdx[e] = min(max(j, 0), a.M - 1) * (a.C * ES / 16);
   }
   __syncthreads();
   const size_t stride = (size_t)2 * a.C * ES;

@@ -79,8 +79,10 @@ __device__ __forceinline__ void mr_load_w(uint4 (&bw)[kMrKU][4], const MrArgs& a
 
 // Gather-max of TM nodes from flattened node row0 (Eq. 2): row r of dst
 // (dst + r * dst_stride, LDS or global memory) receives [x_i | m_i] with
-// m_i = max_t keys[idx[i, t]] - x_i.  sIdx holds the TM x k neighbour lists
-// (clamped to [0, M)).  Rows past R are not written.  Called by all 256 threads.
+// m_i = max_t keys[idx[i, t]] - x_i.  sIdx holds the TM x k neighbour lists,
+// each entry j (clamped to [0, M)) stored as its row offset in 16-byte vectors,
+// j * C / VEC, so a load address is one shift-add.  Rows past R are not
+// written.  Called by all 256 threads.
 // T3: three tasks per thread in flight instead of two (a caller with registers
 // to spare takes the 32-node tile's 768 tasks of C = 192 in one round).
 template <int DT, int KB, bool T3 = false>
@@ -122,8 +124,8 @@ __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM
 #pragma unroll
         for (int u = 0; u < KG; ++u) {
           const int tt = t0 + u;
-          const int j = nb[q][tt < k ? tt : 0];
-          raw[q][u] = *reinterpret_cast<const uint4*>(kbase[q] + (size_t)j * C * ES);
+          const uint32_t jo = (uint32_t)nb[q][tt < k ? tt : 0];
+          raw[q][u] = *reinterpret_cast<const uint4*>(kbase[q] + ((size_t)jo << 4));
         }
 #pragma unroll
       for (int q = 0; q < TPT; ++q)
@@ -173,7 +175,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
   for (int e = tid; e < TM * k; e += kMrThreads) {
     const int r = e / k, tt = e - r * k, row = row0 + r;
     const int j = row < R ? a.idx[(size_t)row * k + tt] : 0;
-    sIdx[e] = min(max(j, 0), M - 1);
+    sIdx[e] = min(max(j, 0), M - 1) * (C * ES / 16);
   }
 
   // -- FC geometry; the first batch of W operands is requested here, after the

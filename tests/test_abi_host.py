@@ -92,6 +92,8 @@ def test_mrconv_validation():
     assert _mr(k=0) == "GL_ERR_BAD_K"
     assert _mr(k=65) == "GL_ERR_BAD_K"
     assert _mr(C=20) == "GL_ERR_UNSUPPORTED"
+    # one image's keys beyond 2^31 16-byte vectors (the kernels' row offsets)
+    assert _mr(keys=P(10), M=1 << 24, C=1024) == "GL_ERR_BAD_SHAPE"
     # too wide for one LDS tile: not rejected, the two-pass form takes it (and
     # fails only at its workspace allocation here, with no GPU)
     assert _mr(C=8192) == "GL_ERR_HIP"
