@@ -137,6 +137,28 @@ def pool_keys_ref(x: np.ndarray, H: int, W: int, r: int) -> np.ndarray:
     return out
 
 
+def max_pool_nodes_ref(x: np.ndarray, H: int, W: int, r: int) -> np.ndarray:
+    """Inter-stage node reduction of pyramid models (Sec. IV-E: node counts are
+    reduced between stages by max pooling): r x r windows of the row-major
+    H x W node grid, stride r,
+        out[b, p*(W/r) + q, c] = max_{u,v < r} x[b, (p*r + u)*W + (q*r + v), c].
+    """
+    x = np.asarray(x, dtype=np.float64)
+    B, N, C = x.shape
+    if N != H * W or H % r or W % r:
+        raise ValueError("bad pooling shape")
+    Hr, Wr = H // r, W // r
+    out = np.empty((B, Hr * Wr, C))
+    for p in range(Hr):
+        for q in range(Wr):
+            best = np.full((B, C), -np.inf)
+            for u in range(r):
+                for v in range(r):
+                    best = np.maximum(best, x[:, (p * r + u) * W + (q * r + v), :])
+            out[:, p * Wr + q, :] = best
+    return out
+
+
 # ----------------------------------------------------------------------------
 # MRConv  (Sec. II-A, Eq. 2 and Eq. 3; split W_x / W_m of Sec. IV-C2)
 # ----------------------------------------------------------------------------

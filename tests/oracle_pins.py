@@ -2,8 +2,8 @@
 invariants and independent pure-Python brute force.
 
 Each pin takes an oracle-like namespace `ref` (with knn_ref, max_relative_ref,
-mrconv_ref, pool_keys_ref, stack_ref, gelu_ref, linear_ref, vig_block_ref,
-vig_stack_ref) and raises AssertionError on failure, so
+mrconv_ref, pool_keys_ref, max_pool_nodes_ref, stack_ref, gelu_ref, linear_ref,
+vig_block_ref, vig_stack_ref) and raises AssertionError on failure, so
 the same pins run against the oracle (test_oracle_pins.py) and against copies
 of it with planted mistakes (test_oracle_mutants.py), which every mistake must
 fail at least one pin.
@@ -548,6 +548,57 @@ def pin_vig_stack_graph_source(ref):
         assert np.array_equal(graphs[l], ref.knn_ref(ul, 3, dil[l]))
 
 
+# ---------------------------------------------------------------------------
+# inter-stage max pooling pins
+# ---------------------------------------------------------------------------
+def pin_max_pool_closed_form(ref):
+    """On a non-square grid whose channel 0 increases along rows and channel 1
+    along columns, each window's maximum sits at its bottom-right node."""
+    H, W, r = 6, 10, 2
+    yy, xx = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    x = np.zeros((2, H * W, 3))
+    x[..., 0] = yy.ravel() * W + xx.ravel()
+    x[..., 1] = -(xx.ravel() * 100.0) + yy.ravel()     # largest at the window's left column
+    x[..., 2] = -7.5
+    out = ref.max_pool_nodes_ref(x, H, W, r)
+    Wr = W // r
+    assert out.shape == (2, (H // r) * Wr, 3)
+    for p in range(H // r):
+        for q in range(Wr):
+            assert out[0, p * Wr + q, 0] == (p * r + r - 1) * W + q * r + r - 1
+            assert out[1, p * Wr + q, 1] == -(q * r) * 100.0 + p * r + r - 1
+            assert out[0, p * Wr + q, 2] == -7.5
+    assert np.array_equal(ref.max_pool_nodes_ref(x, H, W, 1), x)
+
+
+def pin_max_pool_bruteforce(ref):
+    """Pure-Python maxima over each window of a random 4 x 6 grid, r = 2."""
+    g = np.random.default_rng(5)
+    H, W, r, C = 4, 6, 2, 3
+    x = g.standard_normal((1, H * W, C))
+    out = ref.max_pool_nodes_ref(x, H, W, r)
+    for p in range(H // r):
+        for q in range(W // r):
+            for c in range(C):
+                vals = [float(x[0, (p * r + u) * W + q * r + v, c]) for u in range(r) for v in range(r)]
+                assert out[0, p * (W // r) + q, c] == max(vals)
+
+
+def pin_max_pool_dominates_mean(ref):
+    """max >= mean over every window, with equality exactly where the window
+    is constant."""
+    g = np.random.default_rng(6)
+    H, W, r = 8, 8, 4
+    x = g.standard_normal((2, H * W, 4))
+    # channel 3 constant per window
+    yy, xx = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    x[..., 3] = ((yy // r) * 10 + (xx // r)).ravel()
+    mx = ref.max_pool_nodes_ref(x, H, W, r)
+    mean = ref.pool_keys_ref(x, H, W, r)
+    assert np.all(mx[..., :3] > mean[..., :3])
+    assert np.array_equal(mx[..., 3], mean[..., 3])
+
+
 PINS = [
     pin_circle_closed_form_fixture, pin_circle_knn, pin_knn_bruteforce, pin_knn_self_first,
     pin_knn_duplicates_lower_index, pin_knn_permutation_equivariant, pin_knn_scale_invariant,
@@ -558,7 +609,8 @@ PINS = [
     pin_stack_pooled_graph_source, pin_gelu_closed_form, pin_linear_bruteforce,
     pin_vig_block_bruteforce, pin_vig_block_residual_identity, pin_vig_block_hand,
     pin_vig_stack_graph_source, pin_mrconv_heads_bruteforce, pin_mrconv_heads_one_head_is_dense,
-    pin_mrconv_heads_locality,
+    pin_mrconv_heads_locality, pin_max_pool_closed_form, pin_max_pool_bruteforce,
+    pin_max_pool_dominates_mean,
 ]
 
 

@@ -184,6 +184,22 @@ def _heads_factory(shift_m=False, swap=False):
     return mh
 
 
+def _max_pool_factory(offset=0, transposed=False, mean=False):
+    def mp(x, H, W, r):
+        x = np.asarray(x, dtype=np.float64)
+        B, N, C = x.shape
+        Hr, Wr = H // r, W // r
+        out = np.empty((B, Hr * Wr, C))
+        for p in range(Hr):
+            for q in range(Wr):
+                rows = [min((p * r + u + offset) * W + (q * r + v), N - 1) for u in range(r) for v in range(r)]
+                vals = x[:, rows, :]
+                o = q * Hr + p if transposed else p * Wr + q
+                out[:, o, :] = vals.mean(1) if mean else vals.max(1)
+        return out
+    return mp
+
+
 MUTANTS = {
     "knn_no_normalisation": dict(knn_ref=_knn_factory(normalize=False)),
     "knn_descending": dict(knn_ref=_knn_factory(descending=True)),
@@ -210,6 +226,9 @@ MUTANTS = {
     "vig_stack_no_lookahead": dict(vig_stack_ref=_vig_stack_factory(lag=0)),
     "heads_m_from_next_head": dict(mrconv_heads_ref=_heads_factory(shift_m=True)),
     "heads_halves_swapped": dict(mrconv_heads_ref=_heads_factory(swap=True)),
+    "max_pool_window_shifted": dict(max_pool_nodes_ref=_max_pool_factory(offset=1)),
+    "max_pool_output_transposed": dict(max_pool_nodes_ref=_max_pool_factory(transposed=True)),
+    "max_pool_is_mean": dict(max_pool_nodes_ref=_max_pool_factory(mean=True)),
 }
 
 
