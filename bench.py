@@ -213,6 +213,46 @@ def heads_update(args, w, api, torch, x0, idx, Wdense, H=16) -> dict | None:
     return res
 
 
+# ViG-Py-S stage widths: the projection that follows each stage boundary
+NEXT_STAGE_WIDTH = {80: 160, 160: 400, 400: 640}
+
+
+def stage_transition(w, api, torch, x0, es: int, reps: int = 50) -> dict | None:
+    """The stage boundary after a pyramid stage: 2 x 2 max pooling of the node
+    grid (HBM-bound: the grid read once, a quarter of it written) and the
+    width projection on the pooled nodes (gl_linear), each timed with HIP
+    events on the stream its launches go to."""
+    Cn = NEXT_STAGE_WIDTH.get(w.C)
+    if w.pool_r <= 1 or Cn is None or w.H % 2 or w.W % 2:
+        return None
+    s = torch.cuda.current_stream()
+    pooled = torch.empty((w.B, (w.H // 2) * (w.W // 2), w.C), dtype=x0.dtype, device=x0.device)
+    g = torch.Generator(device=x0.device).manual_seed(5)
+    Wp = (torch.rand((Cn, w.C), generator=g, device=x0.device) * 0.2 - 0.1).to(x0.dtype)
+    bp = torch.zeros(Cn, dtype=x0.dtype, device=x0.device)
+    y = torch.empty((w.B, pooled.shape[1], Cn), dtype=x0.dtype, device=x0.device)
+
+    def timed(fn) -> float:
+        for _ in range(5):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(reps):
+            fn()
+        e1.record(s)
+        e1.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+
+    t_pool = timed(lambda: api.max_pool_nodes(x0, w.H, w.W, 2, out=pooled, stream=s))
+    t_proj = timed(lambda: api.linear(pooled, Wp, bp, out=y, stream=s))
+    pool_bytes = (w.B * w.N * w.C + pooled.numel()) * es
+    proj_flops = 2 * pooled.shape[0] * pooled.shape[1] * w.C * Cn
+    return {"grid": f"{w.H}x{w.W} -> {w.H // 2}x{w.W // 2}", "width": f"{w.C} -> {Cn}",
+            "max_pool_us": t_pool * 1e6, "max_pool_hbm_gbs": pool_bytes / t_pool / 1e9,
+            "max_pool_hbm_frac": pool_bytes / t_pool / 1e9 / PEAK_HBM_GBS,
+            "projection_us": t_proj * 1e6, "projection_tflops": proj_flops / t_proj / 1e12}
+
+
 def step_percentiles(torch, step, stream, n: int) -> dict:
     """Per-stack times: one event pair per step on the stream that ends it."""
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
@@ -532,6 +572,10 @@ def main() -> int:
     t_floor = max(fb_flops / (peak * 1e12), fb_bytes / (PEAK_HBM_GBS * 1e9))
     layer_roofline = {"layers_per_s": 1.0 / t_floor, "frac": value * t_floor,
                       "flop_per_layer": fb_flops, "bytes_per_layer": fb_bytes}
+    st = stage_transition(w, api, torch, x0, es)
+    if st is not None:
+        kernels["stage_transition"] = st
+        log("stage transition", json.dumps(st))
     hu = heads_update(args, w, api, torch, x0, ws["idx"][0], Wd[0])
     if hu is not None:
         kernels["mrconv_heads"] = hu

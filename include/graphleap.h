@@ -100,8 +100,9 @@ gl_status gl_knn_graph(const void* x, int B, int N, int C, const void* keys, int
 
 /* ---------------------------------------------------------------------------
  * gl_pool_keys -- r x r average pooling of the H x W node grid, used as the
- * key set of pyramid stages (key pooling of the pyramid workloads; the
- * paper reduces nodes between stages by pooling, Sec. IV-E).
+ * key set of the pyramid-stage workloads (a smaller key set for the kNN
+ * graph of each node; the paper's own reduction between stages is the max
+ * pooling of gl_max_pool_nodes, Sec. IV-E).
  *
  *   keys_out[b, p*(W/r) + q, c] = mean_{u,v<r} x[b, (p*r+u)*W + (q*r+v), c]
  * accumulated in fp32 and rounded once to dt.
@@ -110,6 +111,24 @@ gl_status gl_knn_graph(const void* x, int B, int N, int C, const void* keys, int
  * -------------------------------------------------------------------------*/
 gl_status gl_pool_keys(const void* x, int B, int H, int W, int C, int r, gl_dtype dt,
                        void* keys_out, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * gl_max_pool_nodes -- node reduction between the stages of a pyramid model:
+ * r x r max pooling of the H x W node grid, stride r (Sec. IV-E: node counts
+ * are reduced between stages by max pooling; r = 2 halves each grid side).
+ * The width change that follows a stage boundary is a gl_linear projection.
+ *
+ *   out[b, p*(W/r) + q, c] = max_{u,v<r} x[b, (p*r+u)*W + (q*r+v), c]
+ * exactly (a maximum of stored values needs no rounding).
+ *   x [B, H*W, C] (dt), row-major grid; out [B, (H/r)*(W/r), C] (dt), must not
+ *   overlap x.  Caller owns both (device memory); enqueued on `stream`.
+ * Errors: GL_ERR_NULL_PTR, GL_ERR_UNSUPPORTED (dtype, C not a multiple of 8
+ * (bf16) or 4 (fp32)), GL_ERR_BAD_SHAPE, GL_ERR_ALIGNMENT (16 bytes),
+ * GL_ERR_ALIAS, GL_ERR_HIP.
+ * Limits: H % r == 0, W % r == 0, r >= 1.
+ * -------------------------------------------------------------------------*/
+gl_status gl_max_pool_nodes(const void* x, int B, int H, int W, int C, int r, gl_dtype dt,
+                            void* out, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * gl_mrconv -- max-relative graph convolution (Sec. II-A Eq. 2 and Eq. 3),

@@ -41,6 +41,7 @@ class VigParams(ctypes.Structure):
 SIGNATURES = {
     "gl_knn_graph": [_vp, _i, _i, _i, _vp, _i, _i, _i, _i, _vp, _vp],
     "gl_pool_keys": [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp],
+    "gl_max_pool_nodes": [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp],
     "gl_mrconv": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp],
     "gl_mrconv_heads": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp],
     "gl_lookahead_create": [_vp, _vp, ctypes.POINTER(_vp)],
@@ -137,6 +138,16 @@ def pool_keys(x: torch.Tensor, H: int, W: int, r: int, out: torch.Tensor | None 
     if out is None:
         out = torch.empty((B, (H // r) * (W // r), C), dtype=x.dtype, device=x.device)
     _call("gl_pool_keys", _p(x), B, H, W, C, r, _dt(x), _p(out), _s(stream))
+    return out
+
+
+def max_pool_nodes(x: torch.Tensor, H: int, W: int, r: int = 2, out: torch.Tensor | None = None,
+                   stream=None) -> torch.Tensor:
+    """Node reduction between pyramid stages: r x r max pooling of the H x W grid."""
+    B, N, C = x.shape
+    if out is None:
+        out = torch.empty((B, (H // r) * (W // r), C), dtype=x.dtype, device=x.device)
+    _call("gl_max_pool_nodes", _p(x), B, H, W, C, r, _dt(x), _p(out), _s(stream))
     return out
 
 

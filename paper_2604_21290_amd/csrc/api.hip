@@ -335,6 +335,14 @@ gl_status gl_pool_keys(const void* x, int B, int H, int W, int C, int r, gl_dtyp
   return e == hipSuccess ? GL_OK : hip_fail(e, "pool launch");
 }
 
+gl_status gl_max_pool_nodes(const void* x, int B, int H, int W, int C, int r, gl_dtype dt,
+                            void* out, hipStream_t stream) {
+  gl_status s = check_pool(x, B, H, W, C, r, dt, out);
+  if (s != GL_OK) return s;
+  hipError_t e = gl::launch_pool(x, out, B, H, W, C, r, dt == GL_BF16, stream, true);
+  return e == hipSuccess ? GL_OK : hip_fail(e, "max pool launch");
+}
+
 gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
                     const int32_t* idx, int k, const void* W, const void* bias, int Cout,
                     gl_dtype dt, void* out, hipStream_t stream) {

@@ -113,7 +113,9 @@ MrArgs make_mr_args(const void* x, const void* keys, const int32_t* idx, const v
 hipError_t launch_block(const KnnArgs& ka, const MrArgs& ma, int dt_bf16, int rt,
                         hipStream_t stream, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
+// r x r average (key pooling) or, with max_pool, maximum (inter-stage node
+// reduction) of the H x W node grid.
 hipError_t launch_pool(const void* x, void* keys, int B, int H, int W, int C, int r, int dt_bf16,
-                       hipStream_t stream);
+                       hipStream_t stream, bool max_pool = false);
 
 }  // namespace gl

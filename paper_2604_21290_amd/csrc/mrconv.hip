@@ -146,10 +146,13 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
 }
 
 // ---------------------------------------------------------------------------
-// r x r average pooling of the node grid into key nodes (pyramid stages).
-// One thread per (image, key node, 16-byte channel vector).
+// r x r pooling of the node grid, stride r: the average (key nodes of pyramid
+// stages) or the maximum (node reduction between pyramid stages, Sec. IV-E).
+// One thread per (image, output node, 16-byte channel vector); the window's
+// r*r loads of a thread are independent.  The maximum of stored values is
+// exact; the average is accumulated in fp32 and rounded once.
 // ---------------------------------------------------------------------------
-template <int DT>
+template <int DT, bool MAX>
 __global__ __launch_bounds__(256) void pool_kernel(const void* __restrict__ x,
                                                    void* __restrict__ keys, int B, int H, int W,
                                                    int C, int r) {
@@ -166,29 +169,36 @@ __global__ __launch_bounds__(256) void pool_kernel(const void* __restrict__ x,
   const int p = o / Wr, q = o - p * Wr;
   float acc[VEC];
 #pragma unroll
-  for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
+  for (int i = 0; i < VEC; ++i) acc[i] = MAX ? -INFINITY : 0.f;
   const char* xb = static_cast<const char*>(x) + ((size_t)b * H * W * C + cg * VEC) * ES;
   for (int u = 0; u < r; ++u) {
     for (int v = 0; v < r; ++v) {
       float f[VEC];
       load_vec<DT>(xb + (size_t)((p * r + u) * W + (q * r + v)) * C * ES, f);
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) acc[i] += f[i];
+      for (int i = 0; i < VEC; ++i) acc[i] = MAX ? fmaxf(acc[i], f[i]) : acc[i] + f[i];
     }
   }
-  const float inv = 1.f / (float)(r * r);
+  if (!MAX) {
+    const float inv = 1.f / (float)(r * r);
 #pragma unroll
-  for (int i = 0; i < VEC; ++i) acc[i] *= inv;
+    for (int i = 0; i < VEC; ++i) acc[i] *= inv;
+  }
   store_vec<DT>(static_cast<char*>(keys) + ((size_t)(b * Mo + o) * C + cg * VEC) * ES, acc);
 }
 
 hipError_t launch_pool(const void* x, void* keys, int B, int H, int W, int C, int r, int dt_bf16,
-                       hipStream_t stream) {
+                       hipStream_t stream, bool max_pool) {
   const int VEC = dt_bf16 ? 8 : 4;
   const long total = (long)B * (H / r) * (W / r) * (C / VEC);
   dim3 grid((unsigned)((total + 255) / 256)), block(256);
-  if (dt_bf16) hipLaunchKernelGGL(pool_kernel<1>, grid, block, 0, stream, x, keys, B, H, W, C, r);
-  else hipLaunchKernelGGL(pool_kernel<0>, grid, block, 0, stream, x, keys, B, H, W, C, r);
+  if (max_pool) {
+    if (dt_bf16) hipLaunchKernelGGL((pool_kernel<1, true>), grid, block, 0, stream, x, keys, B, H, W, C, r);
+    else hipLaunchKernelGGL((pool_kernel<0, true>), grid, block, 0, stream, x, keys, B, H, W, C, r);
+  } else {
+    if (dt_bf16) hipLaunchKernelGGL((pool_kernel<1, false>), grid, block, 0, stream, x, keys, B, H, W, C, r);
+    else hipLaunchKernelGGL((pool_kernel<0, false>), grid, block, 0, stream, x, keys, B, H, W, C, r);
+  }
   return hipGetLastError();
 }
 

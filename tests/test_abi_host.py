@@ -116,6 +116,23 @@ def test_pool_validation():
     assert _pool(out=ctypes.c_void_p(A + 16)) == "GL_ERR_ALIAS"
 
 
+def _max_pool(x=P(0), B=2, H=56, W=56, C=80, r=2, dt=1, out=P(40)):
+    return api.STATUS[api.lib().gl_max_pool_nodes(x, B, H, W, C, r, dt, out, None)]
+
+
+@host_only
+def test_max_pool_validation():
+    assert _max_pool(x=None) == "GL_ERR_NULL_PTR"
+    assert _max_pool(out=None) == "GL_ERR_NULL_PTR"
+    assert _max_pool(dt=2) == "GL_ERR_UNSUPPORTED"
+    assert _max_pool(H=55) == "GL_ERR_BAD_SHAPE"            # 55 % 2 != 0
+    assert _max_pool(r=0) == "GL_ERR_BAD_SHAPE"
+    assert _max_pool(C=12) == "GL_ERR_UNSUPPORTED"            # bf16 needs C % 8 == 0
+    assert _max_pool(C=10, dt=0) == "GL_ERR_UNSUPPORTED"      # fp32 needs C % 4 == 0
+    assert _max_pool(out=ctypes.c_void_p(A * 40 + 8)) == "GL_ERR_ALIGNMENT"
+    assert _max_pool(out=ctypes.c_void_p(A + 16)) == "GL_ERR_ALIAS"
+
+
 @host_only
 def test_handle_validation():
     L = api.lib()
