@@ -186,7 +186,9 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
   const int ksteps = (K2 + KSTEP - 1) / KSTEP;
   const int NCT = (Cout + 15) >> 4;
   const char* Wb = static_cast<const char*>(a.W);
-  uint4 bw[kMrKU][4];
+  // output tiles past Cout are never loaded: their operands stay zero (their
+  // results are not stored either)
+  uint4 bw[kMrKU][4] = {};
   if (w < NCT) mr_load_w<DT, HEADS>(bw, a, Wb, w, 0, 0, K2, Cout, g, t);
   __syncthreads();
 
@@ -219,7 +221,8 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
 #pragma unroll
         for (int c4 = 0; c4 < 4; ++c4) {
           if (HEADS && !mr_step_needed(a, (w + 4 * (4 * p + c4)) * 16, s0 + u, KSTEP)) continue;
-          const uint4 bv = (kin[u] && nvalid[c4]) ? bw[u][c4] : make_uint4(0, 0, 0, 0);
+          // past 2C the A operand is zero and bv a real W element (column 0)
+          const uint4 bv = bw[u][c4];
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt) {
             if (DT) {
