@@ -240,25 +240,36 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
       }
     }
     // -- epilogue: + bias, round once, store ------------------------------------
+    // a full tile (all TM nodes below R, Cout a multiple of 16; uniform)
+    // stores without per-lane guards
+    const bool full = row0 + TM <= R && (Cout & 15) == 0;
 #pragma unroll
     for (int c4 = 0; c4 < 4; ++c4) {
+      if (!nvalid[c4]) continue;  // wave-uniform
       const int n = (w + 4 * (4 * p + c4)) * 16 + t;
-      if (!nvalid[c4] || n >= Cout) continue;
+      const int nc = min(n, Cout - 1);
       float bn = 0.f;
       if (a.bias) {
-        bn = DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(a.bias)[n])
-                : static_cast<const float*>(a.bias)[n];
+        bn = DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(a.bias)[nc])
+                : static_cast<const float*>(a.bias)[nc];
       }
+      auto put = [&](int rt, int v) {
+        const size_t o = (size_t)(row0 + rt * 16 + 4 * g + v) * Cout + n;
+        const float y = acc[rt][c4][v] + bn;
+        if (DT) static_cast<uint16_t*>(a.out)[o] = (uint16_t)f32_to_bf16_bits(y);
+        else static_cast<float*>(a.out)[o] = y;
+      };
+      if (full) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
+        for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int row = row0 + rt * 16 + 4 * g + v;
-          if (row >= R) continue;
-          const float y = acc[rt][c4][v] + bn;
-          if (DT) static_cast<uint16_t*>(a.out)[(size_t)row * Cout + n] = (uint16_t)f32_to_bf16_bits(y);
-          else static_cast<float*>(a.out)[(size_t)row * Cout + n] = y;
-        }
+          for (int v = 0; v < 4; ++v) put(rt, v);
+      } else {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (n < Cout && row0 + rt * 16 + 4 * g + v < R) put(rt, v);
       }
     }
   }
