@@ -131,10 +131,9 @@ def cpu_baseline(w, images: int, min_seconds: float = 10.0) -> dict:
     parts = [p for p in np.array_split(np.arange(S), P) if len(p)]
     tasks = lambda reps: [(x[p], Ws, bs, list(w.dilations), w.k, w.H, w.W, w.pool_r, reps) for p in parts]
     with ProcessPoolExecutor(len(parts), mp_context=multiprocessing.get_context("spawn")) as ex:
-        t0 = time.perf_counter()
-        list(ex.map(_oracle_stack_worker, tasks(1)))   # untimed: worker start-up and imports
-        first = time.perf_counter() - t0
-        reps = max(1, int(np.ceil(min_seconds / (first * len(parts)))))
+        # untimed: worker start-up and imports; its CPU seconds size the timed run
+        first = sum(ex.map(_oracle_stack_worker, tasks(1)))
+        reps = max(1, int(np.ceil(min_seconds / first)))
         t0 = time.perf_counter()
         busy = sum(ex.map(_oracle_stack_worker, tasks(reps)))
         wall = time.perf_counter() - t0
