@@ -85,6 +85,37 @@ __device__ __forceinline__ uint32_t lane_xor16(uint32_t v, int j) {
 // value of lane 15 - t within the lane's row of 16
 __device__ __forceinline__ uint32_t lane_reverse16(uint32_t v) { return dpp_mov<0x140>(v); }
 
+// min (low) or max (!low) of v and the value of lane t ^ (1 << j) in the
+// lane's row of 16.  The minimum and the maximum each read the partner through
+// a DPP move of their own whose unused `old` operand is the operation's
+// identity, so the compiler folds each move into its v_min_u32 / v_max_u32
+// (every lane's source is inside its row, so `old` never reaches a result).
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_min(uint32_t v, uint32_t src) {
+  return min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)0xffffffffu, (int)src, CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_max(uint32_t v, uint32_t src) {
+  return max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)src, CTRL, 0xF, 0xF, false));
+}
+// Both results are computed by every lane (a DPP read in lane-divergent
+// control flow would see inactive partners) and the wanted one selected.
+__device__ __forceinline__ uint32_t lane_cas16(uint32_t v, int j, bool low) {
+  uint32_t mn, mx;
+  switch (j) {
+    case 0: mn = dpp_min<0xB1>(v, v); mx = dpp_max<0xB1>(v, v); break;    // quad_perm [1,0,3,2]
+    case 1: mn = dpp_min<0x4E>(v, v); mx = dpp_max<0x4E>(v, v); break;    // quad_perm [2,3,0,1]
+    case 2: {                                                              // half-row mirror,
+      const uint32_t m = dpp_mov<0x141>(v);                                // then quad reverse
+      mn = dpp_min<0x1B>(v, m);
+      mx = dpp_max<0x1B>(v, m);
+      break;
+    }
+    default: mn = dpp_min<0x128>(v, v); mx = dpp_max<0x128>(v, v); break;  // row rotate by 8
+  }
+  return low ? mn : mx;
+}
+
 // value of lane (16*(lane/16) + src) for a wave-uniform src in [0, 16)
 __device__ __forceinline__ uint32_t row_broadcast16(uint32_t v, int src, int lane) {
   const uint32_t r0 = __builtin_amdgcn_readlane(v, src);

@@ -42,10 +42,9 @@ __device__ __forceinline__ uint32_t sort16_lanes(uint32_t c, int t) {
   for (int s = 1; s <= 4; ++s) {
 #pragma unroll
     for (int j = s - 1; j >= 0; --j) {
-      const uint32_t p = lane_xor16(c, 1 << j);
       const bool up = ((t >> s) & 1) == 0;
       const bool lower = ((t >> j) & 1) == 0;
-      c = (lower == up) ? min(c, p) : max(c, p);
+      c = lane_cas16(c, j, lower == up);
     }
   }
   return c;
@@ -68,8 +67,7 @@ __device__ __forceinline__ void merge16_into_list(uint32_t* L, uint32_t c, int t
   for (int j = 3; j >= 0; --j) {
 #pragma unroll
     for (int a = 0; a < R; ++a) {
-      const uint32_t p = lane_xor16(L[a], 1 << j);
-      L[a] = ((t >> j) & 1) ? max(L[a], p) : min(L[a], p);
+      L[a] = lane_cas16(L[a], j, ((t >> j) & 1) == 0);
     }
   }
 }
