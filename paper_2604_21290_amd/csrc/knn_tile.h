@@ -97,11 +97,17 @@ __device__ __forceinline__ void select_chunk(uint32_t* L, uint32_t& tau, uint32_
 #pragma unroll
     for (int m = 0; m < 16; ++m) v[m] = v[m] < tau ? v[m] : 0xffffffffu;
     sort_regs_asc<16>(v);
+    // Two layers per pass: their 16-lane sorts are independent chains that
+    // the scheduler interleaves.  The second layer may hold no key below the
+    // updated tau; merging it then changes nothing among the first KK list
+    // elements (keys are unique, so none of them can be displaced).
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
+    for (int m = 0; m < 16; m += 2) {
       if (!__any(v[m] < tau)) break;
-      const uint32_t c = sort16_lanes(v[m], t);
-      merge16_into_list<R>(L, c, t);
+      const uint32_t c0 = sort16_lanes(v[m], t);
+      const uint32_t c1 = sort16_lanes(v[m + 1], t);
+      merge16_into_list<R>(L, c0, t);
+      merge16_into_list<R>(L, c1, t);
       tau = list_element<R>(L, KK - 1, lane);
     }
   }
