@@ -60,12 +60,39 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def _code_only(src: str) -> str:
+    """C++ source with its // and /* */ comments removed (string and character
+    literals kept as they are)."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return "".join(out)
+
+
 def kernel_source_sha() -> str:
+    """Hash of the kernel sources' code: comments removed and whitespace runs
+    collapsed, so an edit of comments or layout does not retire measurements
+    taken on the same code."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2604_21290_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + fh.read())
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+            h.update(f.encode() + " ".join(_code_only(fh.read()).split()).encode())
     return h.hexdigest()[:16]
 
 
@@ -408,8 +435,8 @@ def main() -> int:
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is "
-                                   "described in the design notes, not implemented",
+        print(json.dumps({"error": "the benchmark runs on one GPU only; sharding over GPUs "
+                                   "(data-parallel over images) is not implemented",
                           "n_gpus": args.gpus}), flush=True)
         return 2
 

@@ -44,8 +44,9 @@ __device__ __forceinline__ void store_vec(char* p, const float* f) {
 }
 
 // W operands of k-steps s0 .. s0+kMrKU-1 for the wave's output tiles
-// w + 4*(4p + c4), c4 < 4 (16 columns each).  Tiles past Cout are not loaded;
-// k past 2C reads column 0 (the MFMA gets a zero operand there).
+// w + 4*(4p + c4), c4 < 4 (16 columns each).  Tiles past Cout are not loaded
+// (their registers keep zeros); k past 2C reads column 0, a real W element
+// that meets a zero A operand.
 // Multi-head update (a.heads > 1, Cout == C): does the 16-column output tile
 // starting at n0 need contraction step s?  Only the channels of the heads the
 // tile's columns belong to, in the x half and in the m half, are non-zero in

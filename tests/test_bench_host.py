@@ -1,0 +1,36 @@
+"""Host-side pieces of bench.py: the kernel-source hash that decides whether a
+committed traffic measurement still applies, and the --gpus contract."""
+import os
+import subprocess
+import sys
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_code_only_drops_comments_not_literals():
+    src = ('int a = 1; // trailing\n'
+           'const char* s = "x // kept /* kept */"; /* block\n spanning */ int b = \'/\';\n'
+           'char q = \'"\'; // after a quote character\n')
+    got = " ".join(bench._code_only(src).split())
+    assert got == 'int a = 1; const char* s = "x // kept /* kept */"; int b = \'/\'; char q = \'"\';'
+
+
+def test_source_hash_ignores_comments_and_layout(tmp_path, monkeypatch):
+    csrc = tmp_path / "paper_2604_21290_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    (csrc / "k.hip").write_text("__global__ void k(int* p) { p[0] = 1; }\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    h0 = bench.kernel_source_sha()
+    (csrc / "k.hip").write_text("// what k does\n__global__ void k(int* p) {\n  p[0] = 1;  /* one */\n}\n")
+    assert bench.kernel_source_sha() == h0
+    (csrc / "k.hip").write_text("__global__ void k(int* p) { p[0] = 2; }\n")
+    assert bench.kernel_source_sha() != h0
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in (r.stdout + r.stderr) or "1 GPU" in (r.stdout + r.stderr)
