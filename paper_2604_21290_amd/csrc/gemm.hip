@@ -45,7 +45,9 @@ struct GemmCfg {
   static constexpr int kWm = NW == 8 ? 4 : 2;            // waves along the rows
   static constexpr int kTpwM = BM / 16 / kWm;            // MFMA tiles per wave, rows
   static constexpr int kTpwN = BM / 32;                  // MFMA tiles per wave, columns
-  static constexpr size_t kSmem = (size_t)4 * kTile;
+  // a 384-byte step is only used when the whole contraction is one stage, so
+  // its tiles are not double-buffered
+  static constexpr size_t kSmem = (size_t)(STEP == 384 ? 2 : 4) * kTile;
 };
 
 size_t gemm_smem_bytes() { return GemmCfg<128, 128>::kSmem; }
@@ -126,6 +128,29 @@ __global__ __launch_bounds__(64 * NW) void gemm_nt_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < TPWN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // The residual does not depend on the product.  In the 64 x 64 tiles (short,
+  // latency-bound contractions) its elements are requested here, so they
+  // arrive during the contraction rather than after it; the 128 x 128 tiles
+  // load it in the epilogue (its registers would cost them a wave per SIMD).
+  // When the residual is `out` itself, each element is still read before
+  // this thread writes it, and the tiles of other workgroups are disjoint.
+  constexpr bool kResEarly = BM == 64;
+  float res[TPWN][TPWM][4];
+  if (kResEarly && a.residual) {
+#pragma unroll
+    for (int j = 0; j < TPWN; ++j) {
+      const int n = min(n0 + wn * 16 * TPWN + j * 16 + t, Cout - 1);
+#pragma unroll
+      for (int i = 0; i < TPWM; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const size_t o = (size_t)min(m0 + wm * 16 * TPWM + i * 16 + 4 * g + v, R - 1) * Cout + n;
+          res[j][i][v] = DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(a.residual)[o])
+                            : static_cast<const float*>(a.residual)[o];
+        }
+    }
+  }
+
   gload(0);
   sstore(0);
   __syncthreads();
@@ -183,8 +208,9 @@ __global__ __launch_bounds__(64 * NW) void gemm_nt_kernel(GemmArgs a) {
         if (ACT_OUT) y = gelu_f32(y);
         const size_t o = (size_t)row * Cout + n;
         if (a.residual) {
-          y += DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(a.residual)[o])
-                  : static_cast<const float*>(a.residual)[o];
+          if (kResEarly) y += res[j][i][v];
+          else y += DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(a.residual)[o])
+                       : static_cast<const float*>(a.residual)[o];
         }
         if (DT) static_cast<uint16_t*>(a.out)[o] = (uint16_t)f32_to_bf16_bits(y);
         else static_cast<float*>(a.out)[o] = y;
@@ -217,6 +243,14 @@ hipError_t launch_gemm_nt(const GemmArgs& a, int dt_bf16, hipStream_t stream, hi
   // with a GELU on either side the 64 x 64 tile is VALU-heavy, and 8 waves
   // overlap it better; plain products are as fast or faster with 4
   const dim3 grid((unsigned)(((a.R + 63) / 64) * ((a.Cout + 63) / 64)));
+  // rows of 257..384 bytes (K = 129..192 in bf16): one stage, one round trip
+  if (rowb > 256 && rowb <= 384) {
+    if (a.act_in || a.act_out)
+      return launch_with_smem(gemm_fn<64, 384, 8>(v), grid, dim3(512), GemmCfg<64, 384, 8>::kSmem,
+                              stream, ev0, ev1, a);
+    return launch_with_smem(gemm_fn<64, 384, 4>(v), grid, dim3(256), GemmCfg<64, 384, 4>::kSmem,
+                            stream, ev0, ev1, a);
+  }
   if (a.act_in || a.act_out)
     return launch_with_smem(gemm_fn<64, 256, 8>(v), grid, dim3(512), GemmCfg<64, 256, 8>::kSmem,
                             stream, ev0, ev1, a);

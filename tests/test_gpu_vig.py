@@ -43,6 +43,12 @@ LIN = [
     ("big128_ragged", 33000, 520, 200, 0, 0, True, True, I.BF16),
     ("big128_gelu_out", 16384, 640, 640, 0, 1, False, True, I.BF16),
     ("big128_gelu_in_fp32", 33000, 256, 260, 1, 0, True, True, I.F32),
+    # one-stage tiles (257..384 bytes of K per row): a partly filled stage,
+    # ragged rows and columns, GELU on either side, fp32
+    ("one_stage_k160_ragged", 999, 160, 72, 0, 0, True, True, I.BF16),
+    ("one_stage_k136_gelu_in_out", 515, 136, 200, 1, 1, False, True, I.BF16),
+    ("one_stage_fp32_k96", 300, 96, 100, 1, 0, True, False, I.F32),
+    ("one_stage_fp32_k68", 77, 68, 33, 0, 1, True, True, I.F32),
 ]
 
 
