@@ -240,15 +240,18 @@ hipError_t launch_gemm_nt(const GemmArgs& a, int dt_bf16, hipStream_t stream, hi
     return launch_with_smem(gemm_fn<128, 128, NW>(v), grid, block, GemmCfg<128, 128, NW>::kSmem,
                             stream, ev0, ev1, a);
   }
-  // with a GELU on either side the 64 x 64 tile is VALU-heavy, and 8 waves
-  // overlap it better; plain products are as fast or faster with 4
   const dim3 grid((unsigned)(((a.R + 63) / 64) * ((a.Cout + 63) / 64)));
+  const long tiles64 = (long)grid.x;
   // rows of 257..384 bytes (K = 129..192 in bf16): one stage, one round trip;
   // 4 waves (measured faster than 8 here, GELU layers included)
   if (rowb > 256 && rowb <= 384)
     return launch_with_smem(gemm_fn<64, 384, 4>(v), grid, dim3(256), GemmCfg<64, 384, 4>::kSmem,
                             stream, ev0, ev1, a);
-  if (a.act_in || a.act_out)
+  // with a GELU on either side the 64 x 64 tile is VALU-heavy, and 8 waves
+  // overlap it better; so do small grids (at most 512 tiles, about two per
+  // CU), which 8 waves per tile fill better; larger plain products are as
+  // fast or faster with 4
+  if (a.act_in || a.act_out || tiles64 <= 512)
     return launch_with_smem(gemm_fn<64, 256, 8>(v), grid, dim3(512), GemmCfg<64, 256, 8>::kSmem,
                             stream, ev0, ev1, a);
   return launch_with_smem(gemm_fn<64, 256, 4>(v), grid, dim3(256), GemmCfg<64, 256, 4>::kSmem,
