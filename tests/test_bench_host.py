@@ -34,3 +34,12 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode != 0
     assert "one GPU" in (r.stdout + r.stderr) or "1 GPU" in (r.stdout + r.stderr)
+
+
+def test_cpu_baseline_runs_the_oracle_in_worker_processes():
+    from paper_2604_21290_amd import inputs as I
+    w = I.WORKLOADS["single"]
+    r = bench.cpu_baseline(w, images=1, min_seconds=0.2)
+    assert r["kind"] == "oracle" and r["unit"] == "layers/s"
+    assert r["value"] > 0 and r["cores"] == 1
+    assert "single-thread processes" in r["sample"]
