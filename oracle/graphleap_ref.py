@@ -11,7 +11,9 @@ states.  Inputs are float64 arrays holding the exact values of the stored
 (fp32 or bf16) tensors.
 
 Pins (what ties each function to something other than itself) are in
-tests/test_oracle_pins.py; every function below has at least one.
+tests/oracle_pins.py, run by tests/test_oracle_pins.py; every function below
+has at least one, and tests/test_oracle_mutants.py plants mistakes in copies of
+each that the pins must catch.
 
 Readings of points the paper leaves open (each is also listed in the design
 notes):
@@ -107,12 +109,26 @@ def knn_ref(x: np.ndarray, k: int, dilation: int = 1, keys: np.ndarray | None = 
 
 def knn_distances(x: np.ndarray, keys: np.ndarray | None = None,
                   rows: np.ndarray | None = None) -> np.ndarray:
-    """Oracle squared distances between normalised rows, [B, rows, M]."""
+    """The distances G(x) ranks by (Eq. 4 on L2-normalised rows; Alg. 2 before
+    its square root): D[b, i, j] = || x[b, rows[i]]/|x| - keys[b, j]/|keys_j| ||^2,
+    [B, len(rows) or N, M].  Query rows are selected first, then normalised;
+    every key row is normalised on its own (keys = x when None)."""
     x = np.asarray(x, dtype=np.float64)
     keys = x if keys is None else np.asarray(keys, dtype=np.float64)
     rows = np.arange(x.shape[1]) if rows is None else np.asarray(rows)
     return np.stack([pairwise_sq_dist(l2_normalize(x[b, rows]), l2_normalize(keys[b]))
                      for b in range(x.shape[0])])
+
+
+def dilated_lists(D: np.ndarray, k: int, dilation: int = 1) -> np.ndarray:
+    """Dilated kNN lists from distances D [B, rows, M] (the dilated kNN of
+    Sec. IV-B): per row, the k*dilation keys of smallest (distance, index),
+    of which ranks 0, d, 2d, ..., (k-1)d are kept.  Returns [B, rows, k] int64."""
+    D = np.asarray(D, dtype=np.float64)
+    kk = k * dilation
+    if k < 1 or dilation < 1 or kk > D.shape[-1]:
+        raise ValueError("need 1 <= k, 1 <= dilation, k*dilation <= M")
+    return np.stack([knn_order(D[b], kk)[:, ::dilation][:, :k] for b in range(D.shape[0])])
 
 
 # ----------------------------------------------------------------------------

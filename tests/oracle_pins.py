@@ -210,6 +210,89 @@ def pin_knn_sorted_by_distance(ref):
 
 
 # ---------------------------------------------------------------------------
+# distances and dilated lists on their own (what the GPU parity tests rank
+# against): knn_distances and dilated_lists
+# ---------------------------------------------------------------------------
+def bf_sq_dist(x, keys=None, rows=None):
+    """Pure-Python squared distances between the normalised query rows `rows`
+    of x and every normalised key row, [B, len(rows), M]."""
+    xl = np.asarray(x).tolist()
+    kl = xl if keys is None else np.asarray(keys).tolist()
+    rows = list(range(len(xl[0]))) if rows is None else [int(r) for r in rows]
+    out = []
+    for b in range(len(xl)):
+        Ks = [_bf_unit(r) for r in kl[b]]
+        out.append([[math.fsum((a - c) ** 2 for a, c in zip(_bf_unit(xl[b][i]), kv)) for kv in Ks]
+                    for i in rows])
+    return np.array(out)
+
+
+def _dist_cases(seed, zero_query=True):
+    """Tiny inputs with zero rows, duplicate rows, keys of unequal norms
+    (pooled-style, M != N) and query-row subsets.  (A zero query row is at
+    distance |k|^2 = 1 from every key up to rounding, so its order is a
+    near-tie everywhere; the list pin leaves it out.)"""
+    rng = np.random.default_rng(seed)
+    for trial in range(4):
+        B, N, C = 2, int(rng.integers(5, 12)), int(rng.integers(2, 6))
+        x = rng.standard_normal((B, N, C)) * rng.uniform(0.2, 4.0, (B, N, 1))
+        if zero_query:
+            x[:, 1] = 0.0
+        x[:, N - 1] = x[:, 2]
+        M = int(rng.integers(4, 10))
+        keys = rng.standard_normal((B, M, C)) * rng.uniform(0.2, 4.0, (B, M, 1))
+        keys[:, M - 1] = 0.0
+        rows = np.sort(rng.choice(N, int(rng.integers(2, N)), replace=False))
+        yield trial, x, keys, rows
+
+
+def pin_knn_distances_bruteforce(ref):
+    for trial, x, keys, rows in _dist_cases(31):
+        for kk, rr in ((None, None), (keys, None), (None, rows), (keys, rows)):
+            got = ref.knn_distances(x, kk, rows=rr)
+            want = bf_sq_dist(x, kk, rr)
+            assert got.shape == want.shape, (trial, got.shape, want.shape)
+            assert np.allclose(got, want, rtol=0, atol=1e-12), (trial, np.abs(got - want).max())
+
+
+def pin_knn_distances_circle(ref):
+    """Unit vectors at angles a_i: D[i, j] = 2 - 2 cos(a_i - a_j), exactly 0 on
+    the diagonal; scaling a row does not change it."""
+    g, ang, x = circle5()
+    want = np.array([[2 - 2 * math.cos(a - b) for b in ang] for a in ang])
+    got = ref.knn_distances(x * np.array([1.0, 3.0, 0.5, 2.0, 7.0])[None, :, None])[0]
+    assert np.allclose(got, want, rtol=0, atol=1e-12)
+    assert np.all(np.diag(got) == 0.0)
+
+
+def pin_dilated_lists_bruteforce(ref):
+    """Lists by a (distance, index) tuple sort, on distances with many exact ties."""
+    rng = np.random.default_rng(32)
+    D = rng.integers(0, 4, size=(2, 7, 13)).astype(np.float64)
+    for k, d in ((1, 1), (3, 1), (4, 2), (3, 4), (13, 1), (2, 6)):
+        want = [[[sorted((D[b, i, j], j) for j in range(13))[t * d][1] for t in range(k)]
+                 for i in range(7)] for b in range(2)]
+        assert np.array_equal(ref.dilated_lists(D, k, d), np.array(want)), (k, d)
+
+
+def pin_distance_lists_are_knn_ref(ref):
+    """dilated_lists(knn_distances(...)) is the graph knn_ref and the loop
+    brute force give, for pooled-style keys, row subsets and d = 1..4; the
+    distances knn_ref returns are the brute-force ones."""
+    for trial, x, keys, rows in _dist_cases(33, zero_query=False):
+        M = keys.shape[1]
+        for d in (1, 2, 3, 4):
+            k = max(1, min(3, M // d))
+            for kk, rr in ((keys, rows), (None, rows), (keys, None)):
+                idx, D = ref.knn_ref(x, k, d, keys=kk, rows=rr, return_dist=True)
+                lists = ref.dilated_lists(ref.knn_distances(x, kk, rows=rr), k, d)
+                assert np.array_equal(lists, idx), (trial, d)
+                bf = bf_knn(x, k, d, kk)
+                assert np.array_equal(idx, bf if rr is None else bf[:, rr]), (trial, d)
+                assert np.allclose(D, bf_sq_dist(x, kk, rr), rtol=0, atol=1e-12), (trial, d)
+
+
+# ---------------------------------------------------------------------------
 # MRConv pins
 # ---------------------------------------------------------------------------
 def pin_circle_mrconv(ref):
@@ -610,7 +693,8 @@ PINS = [
     pin_vig_block_bruteforce, pin_vig_block_residual_identity, pin_vig_block_hand,
     pin_vig_stack_graph_source, pin_mrconv_heads_bruteforce, pin_mrconv_heads_one_head_is_dense,
     pin_mrconv_heads_locality, pin_max_pool_closed_form, pin_max_pool_bruteforce,
-    pin_max_pool_dominates_mean,
+    pin_max_pool_dominates_mean, pin_knn_distances_bruteforce, pin_knn_distances_circle,
+    pin_dilated_lists_bruteforce, pin_distance_lists_are_knn_ref,
 ]
 
 

@@ -4,7 +4,7 @@ import pytest
 import torch
 
 import oracle as O
-from gpu_helpers import check_close, from_dev, require_gpu, to_dev
+from gpu_helpers import check_close, from_dev, mrconv_mag, require_gpu, to_dev
 from paper_2604_21290_amd import inputs as I
 
 pytestmark = pytest.mark.gpu
@@ -22,9 +22,10 @@ def _mr_case(x, idx, Wt, bias=None, keys=None, label=""):
                      keys=None if keys is None else to_dev(keys))
     torch.cuda.synchronize()
     got = from_dev(out).value
-    ref = O.mrconv_ref(x.value, idx, Wt.value, None if bias is None else bias.value,
-                       keys=None if keys is None else keys.value)
-    return check_close(got, ref, x.dtype, label)
+    ref, xcat = O.mrconv_ref(x.value, idx, Wt.value, None if bias is None else bias.value,
+                             keys=None if keys is None else keys.value, return_concat=True)
+    return check_close(got, ref, x.dtype, label, mag=mrconv_mag(xcat, Wt.value),
+                       n_terms=xcat.shape[-1])
 
 
 @pytest.mark.parametrize("name", ["single", "vig_ti", "vig_b", "pyr_s1", "pyr_s2", "hires",

@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import oracle as O
-from gpu_helpers import check_close, check_idx, from_dev, require_gpu, to_dev
+from gpu_helpers import check_close, check_idx, from_dev, mrconv_mag, require_gpu, to_dev
 from paper_2604_21290_amd import inputs as I
 
 pytestmark = pytest.mark.gpu
@@ -77,8 +77,10 @@ def teacher_forced_checks(w, xs, graphs, Wst, bst, schedule="lookahead", n_img=N
         g = graphs[l].cpu().numpy()[sl]
         D = O.knn_distances(xg, keys_g, rows=rows)
         st = check_idx(g, D, w.k, w.dilations[l], rows=rows, label=f"{w.name} graph {l}")
-        ref = O.mrconv_ref(host[l].value[sl], g, Wst.value[l], bst.value[l], keys=keys_u)
-        rel = check_close(host[l + 1].value[sl], ref, w.dtype, f"{w.name} block {l}")
+        ref, xcat = O.mrconv_ref(host[l].value[sl], g, Wst.value[l], bst.value[l], keys=keys_u,
+                                 return_concat=True)
+        rel = check_close(host[l + 1].value[sl], ref, w.dtype, f"{w.name} block {l}",
+                          mag=mrconv_mag(xcat, Wst.value[l]), n_terms=2 * w.C)
         stats.append((l, st["near_tie_rows"], rel))
     _say(w.name, schedule, "per-block (block, near-tie rows, rel err):", stats)
 
@@ -144,6 +146,46 @@ def test_stack_entry_matches_blocks_and_serial(name):
     torch.cuda.synchronize()
     la.close()
     assert torch.equal(fused, out), "one-launch blocks differ from the two-stream schedule"
+
+
+def _fused_graph_buffer(dil, Lp):
+    """Which of the two graph buffers holds the graph the last block of an
+    Lp-block fused-schedule stack used (the stack's own buffer rotation)."""
+    cur = used = 0
+    for l in range(Lp):
+        used = cur
+        if l + 1 < Lp and not (l == 0 and dil[1] == dil[0]):
+            cur = 1 - cur
+    return used
+
+
+@pytest.mark.parametrize("name", ["vig_ti", "pyr_s2"])
+def test_fused_schedule_teacher_forced(name):
+    """The timed schedule (one launch per block) checked against the oracle
+    directly: the stack's first l+1 blocks give X^(l+1) and leave the graph
+    block l used in the workspace; each is graded on the GPU's own inputs."""
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = I.WORKLOADS[name]
+    x0 = I.make_features(w)
+    Wst, bst = _weights(w, w.L, zero_bias=False)
+    x0d, Wd, bd = to_dev(x0), to_dev(Wst), to_dev(bst)
+    dil = list(w.dilations)
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    full = la.stack(x0d, w.H, w.W, Wd, bd, dil, w.k, w.pool_r,
+                    schedule=api.GL_SCHED_LOOKAHEAD_FUSED)
+    xs, graphs = [x0d], []
+    for l in range(w.L):
+        ws = api.make_stack_workspace(x0d, w.H, w.W, w.k, w.pool_r)
+        _say("fused prefix", name, "blocks", l + 1)
+        out = la.stack(x0d, w.H, w.W, Wd[:l + 1], bd[:l + 1], dil[:l + 1], w.k, w.pool_r,
+                       schedule=api.GL_SCHED_LOOKAHEAD_FUSED, ws=ws)
+        torch.cuda.synchronize()
+        xs.append(out)
+        graphs.append(ws["idx"][_fused_graph_buffer(dil, l + 1)].clone())
+    la.close()
+    assert torch.equal(xs[-1], full), "prefix run differs from the full stack"
+    teacher_forced_checks(w, xs, graphs, Wst, bst, schedule="lookahead")
 
 
 @pytest.mark.parametrize("name", ["vig_ti", "pyr_s2"])

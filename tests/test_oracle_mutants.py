@@ -200,6 +200,35 @@ def _max_pool_factory(offset=0, transposed=False, mean=False):
     return mp
 
 
+def _dist_factory(norm_keys=True, rows_on_keys=False, ignore_rows=False, norm_after_rows=True):
+    def dist(x, keys=None, rows=None):
+        x = np.asarray(x, dtype=np.float64)
+        ks = x if keys is None else np.asarray(keys, dtype=np.float64)
+        rows_ = np.arange(x.shape[1]) if (rows is None or ignore_rows) else np.asarray(rows)
+        out = []
+        for b in range(x.shape[0]):
+            Q = R.l2_normalize(x[b])[rows_] if norm_after_rows else R.l2_normalize(x[b, rows_])
+            K = ks[b, rows_] if rows_on_keys else ks[b]
+            K = R.l2_normalize(K) if norm_keys else K
+            out.append(R.pairwise_sq_dist(Q, K))
+        return np.stack(out)
+    return dist
+
+
+def _lists_factory(offset=0, tie_high=False):
+    def lists(D, k, dilation=1):
+        D = np.asarray(D, dtype=np.float64)
+        out = []
+        for b in range(D.shape[0]):
+            if tie_high:
+                order = D.shape[-1] - 1 - np.argsort(D[b][:, ::-1], axis=1, kind="stable")
+            else:
+                order = np.argsort(D[b], axis=1, kind="stable")
+            out.append(order[:, offset:k * dilation + offset][:, ::dilation][:, :k])
+        return np.stack(out)
+    return lists
+
+
 MUTANTS = {
     "knn_no_normalisation": dict(knn_ref=_knn_factory(normalize=False)),
     "knn_descending": dict(knn_ref=_knn_factory(descending=True)),
@@ -229,6 +258,11 @@ MUTANTS = {
     "max_pool_window_shifted": dict(max_pool_nodes_ref=_max_pool_factory(offset=1)),
     "max_pool_output_transposed": dict(max_pool_nodes_ref=_max_pool_factory(transposed=True)),
     "max_pool_is_mean": dict(max_pool_nodes_ref=_max_pool_factory(mean=True)),
+    "dist_keys_not_normalised": dict(knn_distances=_dist_factory(norm_keys=False)),
+    "dist_rows_applied_to_keys": dict(knn_distances=_dist_factory(rows_on_keys=True)),
+    "dist_rows_ignored": dict(knn_distances=_dist_factory(ignore_rows=True)),
+    "dilated_lists_offset": dict(dilated_lists=_lists_factory(offset=1)),
+    "dilated_lists_tie_higher_index": dict(dilated_lists=_lists_factory(tie_high=True)),
 }
 
 
