@@ -246,16 +246,17 @@ def heads_update(args, w, api, torch, x0, idx, Wdense, H=16) -> dict | None:
         Wb[h * hd:(h + 1) * hd, w.C + h * hd:w.C + (h + 1) * hd] = \
             Wdense[h * hd:(h + 1) * hd, w.C + h * hd:w.C + (h + 1) * hd]
     out = torch.empty_like(x0)
+    mws = api.mrconv_workspace(w.B, w.N, w.C, w.k, w.C, x0.dtype, x0.device)
     res = {"heads": H}
     n = max(20, args.steps // 4)
     for name, hh in (("dense_us", 1), ("heads_us", H)):
         for _ in range(3):
-            api.mrconv(x0, idx, Wb, out=out, heads=hh)
+            api.mrconv(x0, idx, Wb, out=out, heads=hh, ws=mws)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record()
         for _ in range(n):
-            api.mrconv(x0, idx, Wb, out=out, heads=hh)
+            api.mrconv(x0, idx, Wb, out=out, heads=hh, ws=mws)
         e1.record()
         torch.cuda.synchronize()
         res[name] = e0.elapsed_time(e1) / n * 1e3
@@ -324,6 +325,7 @@ def cold_gather(w, api, torch, x0, idx, W, b, out, mr_bytes, reps: int = 20) -> 
     its time is the median of (write + update) minus the median of the write alone."""
     import numpy as np
     keys = api.pool_keys(x0, w.H, w.W, w.pool_r) if w.pool_r > 1 else None
+    mws = api.mrconv_workspace(w.B, w.N, w.C, w.k, w.C, x0.dtype, x0.device)
     flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     s = torch.cuda.current_stream()
 
@@ -337,7 +339,7 @@ def cold_gather(w, api, torch, x0, idx, W, b, out, mr_bytes, reps: int = 20) -> 
         return e0.elapsed_time(e1) * 1e3
 
     def upd():
-        api.mrconv(x0, idx, W, b, keys=keys, out=out)
+        api.mrconv(x0, idx, W, b, keys=keys, out=out, ws=mws)
 
     def many():
         for _ in range(reps):
@@ -494,8 +496,9 @@ def main() -> int:
     if args.only == "mrconv":
         keys = api.pool_keys(x0, w.H, w.W, w.pool_r) if w.pool_r > 1 else None
         idx = api.knn_graph(x0, w.k, dil[0], keys=keys)
+        mws = api.mrconv_workspace(w.B, w.N, w.C, w.k, w.C, x0.dtype, x0.device)
         for _ in range(args.steps):
-            api.mrconv(x0, idx, Wd[0], bd[0], keys=keys, out=out)
+            api.mrconv(x0, idx, Wd[0], bd[0], keys=keys, out=out, ws=mws)
         torch.cuda.synchronize()
         log(f"mrconv x {args.steps}")
         return 0

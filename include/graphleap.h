@@ -14,9 +14,13 @@
  *
  * Conventions for every call
  *   Memory.  Every tensor pointer is device memory owned by the caller.  The
- *     library allocates nothing and keeps no pointer after a call returns.
- *     Buffers must stay alive until the streams the work was enqueued on have
- *     finished it.
+ *     library allocates no device memory on any call that enqueues work: the
+ *     calls that need scratch memory take a caller-owned workspace, whose size
+ *     a *_workspace_bytes query gives, and fail with GL_ERR_WORKSPACE when it
+ *     is missing or short.  (gl_lookahead_create and
+ *     gl_lookahead_set_profiling create HIP events; nothing else is created.)
+ *     The library keeps no pointer after a call returns.  Buffers must stay
+ *     alive until the streams the work was enqueued on have finished it.
  *   Layout.  Row-major, channels last: features [B, N, C], keys [B, M, C],
  *     neighbour indices int32 [B, N, k], weights [Cout, 2C], bias [Cout].
  *     Base pointers of feature, key and weight tensors must be 16-byte
@@ -61,7 +65,8 @@ typedef enum gl_status {
   GL_ERR_ALIGNMENT = 5,    /* a tensor base pointer is not 16-byte aligned */
   GL_ERR_ALIAS = 6,        /* an output overlaps an input it must not overlap */
   GL_ERR_HIP = 7,          /* the HIP runtime reported an error */
-  GL_ERR_BAD_HANDLE = 8    /* NULL or destroyed lookahead handle */
+  GL_ERR_BAD_HANDLE = 8,   /* NULL or destroyed lookahead handle */
+  GL_ERR_WORKSPACE = 9     /* a needed workspace is NULL, too small or misaligned */
 } gl_status;
 
 typedef enum gl_schedule {
@@ -140,11 +145,15 @@ gl_status gl_max_pool_nodes(const void* x, int B, int H, int W, int C, int r, gl
  * The neighbour rows are gathered on the fly; no [B,N,k,C] edge tensor is
  * ever written.  Narrow layers gather straight into an on-chip tile and never
  * write the [B,N,2C] concatenation either.  When W is large per node (more
- * than 16 KB of W per node of the fused tile, e.g. C = Cout = 640) the call
- * runs two passes instead: the gather writes [x_i, m_i] rows to a workspace
- * of B*N*2C*s bytes, then a tiled GEMM reads them.  This call allocates that
- * workspace stream-ordered on `stream` (hipMallocAsync / hipFreeAsync); a
- * failed allocation returns GL_ERR_HIP.
+ * than 8 KB of W per node of the fused tile, e.g. C = Cout = 640) the call
+ * runs two passes instead: the gather writes [x_i, m_i] rows to the caller's
+ * workspace (B*N*2C*s bytes), then a tiled GEMM reads them.
+ * gl_mrconv_workspace_bytes() gives the size (0 when the fused tile is used;
+ * workspace may then be NULL).  A NULL, short or not 16-byte aligned
+ * workspace where one is needed returns GL_ERR_WORKSPACE; it must not overlap
+ * any other argument (GL_ERR_ALIAS).  The workspace is scratch: its contents
+ * before and after the call do not matter, and two calls in flight at once
+ * need two workspaces.
  *
  *   x    [B, N, C] (dt); keys [B, M, C] (dt) or NULL for keys = x (M == N).
  *   idx  [B, N, k] int32 in [0, M).  Out-of-range values are clamped into
@@ -154,9 +163,11 @@ gl_status gl_max_pool_nodes(const void* x, int B, int H, int W, int C, int r, gl
  * Limits: 1 <= k <= GL_MAX_K; Cout >= 1; one image's keys M * C * s bytes
  * below 32 GiB (2^31 16-byte vectors), else GL_ERR_BAD_SHAPE.
  * -------------------------------------------------------------------------*/
+size_t gl_mrconv_workspace_bytes(int B, int N, int C, int k, int Cout, gl_dtype dt);
 gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
                     const int32_t* idx, int k, const void* W, const void* bias, int Cout,
-                    gl_dtype dt, void* out, hipStream_t stream);
+                    gl_dtype dt, void* out, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * gl_mrconv_heads -- the multi-head MRConv update (Sec. II-A; per-head
@@ -169,23 +180,28 @@ gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
  * outside the heads' diagonal blocks of each half.  The kernel skips the
  * contraction steps a 16-column output tile does not need, but steps that
  * straddle a block edge do multiply the zeros.  Cout == C.  Everything else
- * is as gl_mrconv; heads == 1 is gl_mrconv.
+ * is as gl_mrconv (workspace: gl_mrconv_workspace_bytes with Cout = C);
+ * heads == 1 is gl_mrconv.
  * Limits: heads >= 1, C % heads == 0.
  * -------------------------------------------------------------------------*/
 gl_status gl_mrconv_heads(const void* x, int B, int N, int C, const void* keys, int M,
                           const int32_t* idx, int k, const void* W, const void* bias, int heads,
-                          gl_dtype dt, void* out, hipStream_t stream);
+                          gl_dtype dt, void* out, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Lookahead handle (Sec. IV-A, IV-F; the look-ahead buffer of Sec. IV-G).
  * Holds two HIP events that order the build stream against the update
- * stream; the caller owns both streams and every tensor.  Streams must be
- * distinct for the build to overlap the update; they may be equal.  For
- * layers that take the two-pass MRConv (see gl_mrconv) the handle also owns
- * the workspace, allocated on first need and grown when a larger layer needs
- * it (growing waits for the update stream); gl_lookahead_destroy frees it.
+ * stream; the caller owns both streams, every tensor and the workspace of
+ * the layers that take the two-pass MRConv (see gl_mrconv).  Streams must be
+ * distinct for the build to overlap the update; they may be equal.
  * -------------------------------------------------------------------------*/
 typedef struct gl_lookahead* gl_lookahead_t;
+
+/* Workspace bytes gl_graphleap_block / gl_graphleap_stack need for blocks of
+ * this shape (the MRConv workspace of gl_mrconv with Cout = C, keys pooled
+ * r x r when pool_r > 1); 0 when none is needed or the shape is invalid. */
+size_t gl_graphleap_workspace_bytes(int B, int H, int W, int C, int pool_r, int k, gl_dtype dt);
 
 gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_lookahead_t* out);
 gl_status gl_lookahead_destroy(gl_lookahead_t h);
@@ -237,6 +253,8 @@ gl_status gl_lookahead_bootstrap(gl_lookahead_t h, const void* x0, int B, int H,
  *           (last block, or when Ghat^(l+1) is the same graph as Ghat^l);
  *           idx_next must not overlap idx_use.
  *   Wt [C, 2C], bias [C] or NULL.
+ *   workspace: at least gl_graphleap_workspace_bytes() bytes (may be NULL
+ *           when that is 0); used on the update stream only.
  * The caller double-buffers features and graphs (two of each, Sec. IV-G
  * N_buf = 2): the handle's waits make reuse of the buffers of block l-1 by
  * block l+1 safe.
@@ -244,7 +262,8 @@ gl_status gl_lookahead_bootstrap(gl_lookahead_t h, const void* x0, int B, int H,
 gl_status gl_graphleap_block(gl_lookahead_t h, const void* x_in, int B, int H, int W, int C,
                              int pool_r, void* keys_ws, const int32_t* idx_use, int k,
                              const void* Wt, const void* bias, gl_dtype dt, void* x_out,
-                             int32_t* idx_next, int dilation_next);
+                             int32_t* idx_next, int dilation_next, void* workspace,
+                             size_t workspace_bytes);
 
 /* ---------------------------------------------------------------------------
  * gl_graphleap_stack -- L blocks of X^(l+1) = MRConv(X^l; Ghat^l) enqueued
@@ -266,12 +285,15 @@ gl_status gl_graphleap_block(gl_lookahead_t h, const void* x_in, int B, int H, i
  *     each graph).
  *   x_ws [2, B, N, C] feature ping-pong workspace; idx_ws [2, B, N, k];
  *   keys_ws [B, M, C] when pool_r > 1 else NULL;  x_out [B, N, C] = X^L.
- *   x_out, x_ws, idx_ws and keys_ws must not overlap each other or x0.
+ *   workspace: at least gl_graphleap_workspace_bytes() bytes (NULL when 0).
+ *   x_out, x_ws, idx_ws, keys_ws and workspace must not overlap each other
+ *   or x0.  Every block is checked before anything is enqueued.
  * -------------------------------------------------------------------------*/
 gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int W, int C,
                              int pool_r, int L, int k, const int* dilations, const void* Ws,
                              const void* bs, gl_dtype dt, gl_schedule schedule, void* x_ws,
-                             int32_t* idx_ws, void* keys_ws, void* x_out);
+                             int32_t* idx_ws, void* keys_ws, void* x_out, void* workspace,
+                             size_t workspace_bytes);
 
 /* ---------------------------------------------------------------------------
  * Diagnostics.
@@ -318,7 +340,8 @@ typedef struct {
 } gl_vig_params;
 
 /* Bytes of the workspace gl_vig_block and gl_vig_stack need (they carve
- * sigma-input, Y and the FFN's hidden rows out of it; the stack also U, two
+ * sigma-input, Y and the FFN's hidden rows out of it -- the hidden rows'
+ * region also serves the two-pass MRConv -- and the stack also U, two
  * feature buffers and two graphs). */
 size_t gl_vig_workspace_bytes(int B, int N, int C, int k, gl_dtype dt);
 

@@ -26,7 +26,7 @@ GL_MAX_KD, GL_MAX_M, GL_MAX_K = 64, 4096, 64
 
 STATUS = {0: "GL_OK", 1: "GL_ERR_NULL_PTR", 2: "GL_ERR_BAD_SHAPE", 3: "GL_ERR_BAD_K",
           4: "GL_ERR_UNSUPPORTED", 5: "GL_ERR_ALIGNMENT", 6: "GL_ERR_ALIAS", 7: "GL_ERR_HIP",
-          8: "GL_ERR_BAD_HANDLE"}
+          8: "GL_ERR_BAD_HANDLE", 9: "GL_ERR_WORKSPACE"}
 
 _vp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
 
@@ -42,16 +42,19 @@ SIGNATURES = {
     "gl_knn_graph": [_vp, _i, _i, _i, _vp, _i, _i, _i, _i, _vp, _vp],
     "gl_pool_keys": [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp],
     "gl_max_pool_nodes": [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp],
-    "gl_mrconv": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp],
-    "gl_mrconv_heads": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp],
+    "gl_mrconv_workspace_bytes": [_i, _i, _i, _i, _i, _i],
+    "gl_mrconv": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _sz, _vp],
+    "gl_mrconv_heads": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _sz, _vp],
     "gl_lookahead_create": [_vp, _vp, ctypes.POINTER(_vp)],
     "gl_lookahead_destroy": [_vp],
     "gl_lookahead_set_profiling": [_vp, _i],
     "gl_lookahead_kernel_times": [_vp, _i, ctypes.POINTER(_f), _i, ctypes.POINTER(_i)],
     "gl_lookahead_bootstrap": [_vp, _vp, _i, _i, _i, _i, _i, _vp, _i, _i, _i, _vp],
-    "gl_graphleap_block": [_vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _i, _vp, _vp, _i, _vp, _vp, _i],
+    "gl_graphleap_workspace_bytes": [_i, _i, _i, _i, _i, _i, _i],
+    "gl_graphleap_block": [_vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _i, _vp, _vp, _i, _vp, _vp, _i,
+                           _vp, _sz],
     "gl_graphleap_stack": [_vp, _vp, _i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i), _vp, _vp, _i,
-                           _i, _vp, _vp, _vp, _vp],
+                           _i, _vp, _vp, _vp, _vp, _vp, _sz],
     "gl_linear": [_vp, _i, _i, _vp, _vp, _i, _i, _i, _vp, _i, _vp, _vp],
     "gl_vig_workspace_bytes": [_i, _i, _i, _i, _i],
     "gl_vig_block": [_vp, _vp, _i, _i, _i, _i, _vp, ctypes.POINTER(VigParams), _i, _vp, _sz, _vp,
@@ -63,7 +66,8 @@ SIGNATURES = {
     "gl_version": [],
 }
 RESTYPES = {"gl_status_string": ctypes.c_char_p, "gl_last_error": ctypes.c_char_p,
-            "gl_vig_workspace_bytes": ctypes.c_size_t}
+            "gl_vig_workspace_bytes": ctypes.c_size_t, "gl_mrconv_workspace_bytes": ctypes.c_size_t,
+            "gl_graphleap_workspace_bytes": ctypes.c_size_t}
 
 _lib = None
 
@@ -108,6 +112,8 @@ def _dt(t: torch.Tensor) -> int:
 def _p(t):
     if t is None:
         return None
+    if isinstance(t, Workspace):
+        return ctypes.c_void_p(t.ptr)
     if not t.is_cuda or not t.is_contiguous():
         raise ValueError("tensors must be contiguous device tensors")
     return ctypes.c_void_p(t.data_ptr())
@@ -151,23 +157,47 @@ def max_pool_nodes(x: torch.Tensor, H: int, W: int, r: int = 2, out: torch.Tenso
     return out
 
 
+class Workspace:
+    """A caller-owned device workspace: a torch uint8 buffer (or none when the
+    call needs 0 bytes), passed as pointer and size."""
+
+    def __init__(self, nbytes: int, device):
+        self.nbytes = int(nbytes)
+        self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device) if nbytes else None
+        self.ptr = self.buf.data_ptr() if nbytes else None
+
+    def record_stream(self, s):
+        if self.buf is not None:
+            self.buf.record_stream(s)
+
+
+def mrconv_workspace(B: int, N: int, C: int, k: int, Cout: int, dtype, device) -> Workspace:
+    """Workspace of gl_mrconv / gl_mrconv_heads for this layer (empty when the
+    fused tile needs none)."""
+    dt = GL_BF16 if dtype == torch.bfloat16 else GL_F32
+    return Workspace(lib().gl_mrconv_workspace_bytes(B, N, C, k, Cout, dt), device)
+
+
 def mrconv(x: torch.Tensor, idx: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = None,
            keys: torch.Tensor | None = None, out: torch.Tensor | None = None,
-           stream=None, heads: int = 1) -> torch.Tensor:
+           stream=None, heads: int = 1, ws: Workspace | None = None) -> torch.Tensor:
     """out[B, N, Cout] = [x_i, max_j (keys_j - x_i)] W^T + bias.  heads > 1: the
-    multi-head update (W block-diagonal by heads in each half, Cout == C)."""
+    multi-head update (W block-diagonal by heads in each half, Cout == C).
+    ws: the call's workspace (allocated here when not given)."""
     B, N, C = x.shape
     M = N if keys is None else keys.shape[1]
     k = idx.shape[2]
     Cout = W.shape[0]
     if out is None:
         out = torch.empty((B, N, Cout), dtype=x.dtype, device=x.device)
+    if ws is None:
+        ws = mrconv_workspace(B, N, C, k, Cout, x.dtype, x.device)
     if heads != 1:
         _call("gl_mrconv_heads", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(W), _p(bias), heads,
-              _dt(x), _p(out), _s(stream))
+              _dt(x), _p(out), _p(ws), ws.nbytes, _s(stream))
     else:
         _call("gl_mrconv", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(W), _p(bias), Cout, _dt(x),
-              _p(out), _s(stream))
+              _p(out), _p(ws), ws.nbytes, _s(stream))
     return out
 
 
@@ -249,15 +279,17 @@ class Lookahead:
         return idx0
 
     def block(self, x_in, H, W, idx_use, Wt, bias=None, pool_r=1, keys_ws=None, x_out=None,
-              idx_next=None, dilation_next=1):
+              idx_next=None, dilation_next=1, ws: Workspace | None = None):
         B, N, C = x_in.shape
         k = idx_use.shape[2]
         if x_out is None:
             x_out = torch.empty_like(x_in)
+        if ws is None:
+            ws = graphleap_workspace(x_in, H, W, k, pool_r)
         self._keep(x_in, keys_ws, idx_next)
         _call("gl_graphleap_block", self._h, _p(x_in), B, H, W, C, pool_r, _p(keys_ws),
               _p(idx_use), k, _p(Wt), _p(bias), _dt(x_in), _p(x_out), _p(idx_next),
-              dilation_next)
+              dilation_next, _p(ws), ws.nbytes)
         return x_out
 
     def vig_block(self, x_in, idx_use, params: dict, ws, u_out=None, x_out=None, idx_next=None,
@@ -298,9 +330,17 @@ class Lookahead:
             x_out = torch.empty_like(x0)
         dil = (ctypes.c_int * L)(*dilations)
         self._keep(x0, ws["x"], ws["idx"], ws["keys"])
+        ws["mr"].record_stream(self.s_build)
         _call("gl_graphleap_stack", self._h, _p(x0), B, H, W, C, pool_r, L, k, dil, _p(Ws),
-              _p(bs), _dt(x0), schedule, _p(ws["x"]), _p(ws["idx"]), _p(ws["keys"]), _p(x_out))
+              _p(bs), _dt(x0), schedule, _p(ws["x"]), _p(ws["idx"]), _p(ws["keys"]), _p(x_out),
+              _p(ws["mr"]), ws["mr"].nbytes)
         return x_out
+
+
+def graphleap_workspace(x0: torch.Tensor, H: int, W: int, k: int, pool_r: int = 1) -> Workspace:
+    """The MRConv workspace of gl_graphleap_block / gl_graphleap_stack."""
+    B, N, C = x0.shape
+    return Workspace(lib().gl_graphleap_workspace_bytes(B, H, W, C, pool_r, k, _dt(x0)), x0.device)
 
 
 def make_stack_workspace(x0: torch.Tensor, H: int, W: int, k: int, pool_r: int = 1) -> dict:
@@ -310,6 +350,7 @@ def make_stack_workspace(x0: torch.Tensor, H: int, W: int, k: int, pool_r: int =
         "x": torch.empty((2, B, N, C), dtype=x0.dtype, device=x0.device),
         "idx": torch.empty((2, B, N, k), dtype=torch.int32, device=x0.device),
         "keys": torch.empty((B, M, C), dtype=x0.dtype, device=x0.device) if pool_r > 1 else None,
+        "mr": graphleap_workspace(x0, H, W, k, pool_r),
     }
 
 

@@ -4,6 +4,7 @@
 #include <stdio.h>
 
 #include <climits>
+#include <initializer_list>
 #include <string>
 #include <utility>
 #include <vector>
@@ -87,6 +88,13 @@ gl_status check_pool(const void* x, int B, int H, int W, int C, int r, gl_dtype 
   return GL_OK;
 }
 
+// Row tiles of the fused MRConv tile (0: the tile does not fit LDS).
+int mrconv_rt(int C, int k, gl_dtype dt) {
+  const int dtb = dt == GL_BF16;
+  const int rt = gl::mrconv_row_tiles(C, k, dtb, 65536);
+  return rt ? rt : gl::mrconv_row_tiles(C, k, dtb, 160 * 1024);
+}
+
 gl_status check_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
                        const int32_t* idx, int k, const void* W, const void* bias, int Cout,
                        gl_dtype dt, const void* out, int* rt_out) {
@@ -102,10 +110,8 @@ gl_status check_mrconv(const void* x, int B, int N, int C, const void* keys, int
   // the kernels address a neighbour row by its offset in 16-byte vectors (int32)
   if ((long long)M * (C / vec_width(dt)) > INT_MAX)
     return fail(GL_ERR_BAD_SHAPE, "mrconv: M=%d rows of C=%d exceed 2^31 16-byte vectors per image", M, C);
-  const int dtb = dt == GL_BF16;
   // rt = 0: the fused LDS tile does not fit; the two-pass form is used
-  int rt = gl::mrconv_row_tiles(C, k, dtb, 65536);
-  if (!rt) rt = gl::mrconv_row_tiles(C, k, dtb, 160 * 1024);
+  const int rt = mrconv_rt(C, k, dt);
   if (!aligned(x, 16) || (keys && !aligned(keys, 16)) || !aligned(W, 16) || !aligned(out, 16) ||
       !aligned(idx, 4) || (bias && !aligned(bias, esize(dt))))
     return fail(GL_ERR_ALIGNMENT, "mrconv: x/keys/W/out need 16-byte alignment");
@@ -120,6 +126,28 @@ gl_status check_mrconv(const void* x, int B, int N, int C, const void* keys, int
   return GL_OK;
 }
 
+// Workspace bytes of one MRConv (the [x | m] rows of the two-pass form; 0 for
+// the fused tile).
+size_t mrconv_ws_need(int B, int N, int C, int k, int Cout, gl_dtype dt, int rt) {
+  const int dtb = dt == GL_BF16;
+  return gl::mrconv_use_split(C, Cout, dtb, rt) ? gl::mrconv_split_ws_bytes(B * N, C, dtb) : 0;
+}
+
+// A caller workspace of `need` bytes: present, large enough, 16-byte aligned,
+// and (when given) clear of the call's other buffers.
+gl_status check_ws(const char* who, size_t need, const void* ws, size_t ws_bytes,
+                   std::initializer_list<std::pair<const void*, size_t>> others = {}) {
+  if (need == 0) return GL_OK;
+  if (!ws || ws_bytes < need)
+    return fail(GL_ERR_WORKSPACE, "%s: needs a workspace of %zu bytes (got %zu at %p)", who, need,
+                ws ? ws_bytes : (size_t)0, ws);
+  if (!aligned(ws, 16)) return fail(GL_ERR_WORKSPACE, "%s: workspace must be 16-byte aligned", who);
+  for (const auto& o : others)
+    if (overlap(ws, need, o.first, o.second))
+      return fail(GL_ERR_ALIAS, "%s: workspace overlaps another argument", who);
+  return GL_OK;
+}
+
 constexpr uint32_t kHandleMagic = 0x474c4c41u;  // "GLLA"
 
 }  // namespace
@@ -127,8 +155,6 @@ constexpr uint32_t kHandleMagic = 0x474c4c41u;  // "GLLA"
 struct gl_lookahead {
   uint32_t magic;
   hipStream_t su, sb;
-  void* ws;          // [x | m] rows of the two-pass MRConv (grown on demand, update stream)
-  size_t ws_bytes;
   hipEvent_t ev_ready, ev_built;
   bool pending;
   int prof_max;
@@ -140,28 +166,10 @@ namespace {
 
 bool handle_ok(gl_lookahead_t h) { return h && h->magic == kHandleMagic; }
 
-// The handle's MRConv workspace, at least `bytes` long.  Growing it waits for
-// the update stream, whose kernels are the only users of the old buffer.
-gl_status ensure_ws(gl_lookahead_t h, size_t bytes) {
-  if (bytes <= h->ws_bytes) return GL_OK;
-  hipError_t e = hipStreamSynchronize(h->su);
-  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
-  if (h->ws) (void)hipFree(h->ws);
-  h->ws = nullptr;
-  h->ws_bytes = 0;
-  if ((e = hipMalloc(&h->ws, bytes)) != hipSuccess) return hip_fail(e, "hipMalloc (MRConv workspace)");
-  h->ws_bytes = bytes;
-  return GL_OK;
-}
-
-// Workspace the MRConv of one block needs on this handle (null if none).
-gl_status block_ws(gl_lookahead_t h, int B, int N, int C, gl_dtype dt, int rt, void** ws) {
-  *ws = nullptr;
-  const int dtb = dt == GL_BF16;
-  if (!gl::mrconv_use_split(C, C, dtb, rt)) return GL_OK;
-  gl_status s = ensure_ws(h, gl::mrconv_split_ws_bytes(B * N, C, dtb));
-  if (s == GL_OK) *ws = h->ws;
-  return s;
+// The MRConv workspace of one block of the handle's schedules: the caller's
+// (already checked to be large enough), or null when the fused tile is used.
+void* block_ws(int B, int N, int C, int k, gl_dtype dt, int rt, void* ws) {
+  return mrconv_ws_need(B, N, C, k, C, dt, rt) ? ws : nullptr;
 }
 
 void free_profiling(gl_lookahead_t h) {
@@ -235,6 +243,8 @@ struct BlockArgs {
   void* x_out;
   int32_t* idx_next;
   int dil_next;
+  void* ws;          // MRConv workspace (two-pass form), caller-owned
+  size_t ws_bytes;
 };
 
 gl_status check_block(const BlockArgs& a, int* rt) {
@@ -264,7 +274,10 @@ gl_status check_block(const BlockArgs& a, int* rt) {
     if (overlap(a.idx_next, ib, a.x_out, (size_t)a.B * N * a.C * esize(a.dt)))
       return fail(GL_ERR_ALIAS, "block: idx_next overlaps x_out");
   }
-  return GL_OK;
+  const size_t xb = (size_t)a.B * N * a.C * esize(a.dt), ib = (size_t)a.B * N * a.k * 4;
+  return check_ws("block", mrconv_ws_need(a.B, N, a.C, a.k, a.C, a.dt, *rt), a.ws, a.ws_bytes,
+                  {{a.x_in, xb}, {a.x_out, xb}, {a.idx_use, ib}, {a.idx_next, a.idx_next ? ib : 0},
+                   {a.keys_ws, pooled ? (size_t)a.B * M * a.C * esize(a.dt) : 0}});
 }
 
 // Enqueue one lookahead block whose arguments were checked.
@@ -287,8 +300,7 @@ gl_status enqueue_block(gl_lookahead_t h, const BlockArgs& a, int rt, bool do_po
       return s;
     if ((s = mark_built(h)) != GL_OK) return s;
   }
-  void* ws;
-  if ((s = block_ws(h, a.B, N, a.C, a.dt, rt, &ws)) != GL_OK) return s;
+  void* ws = block_ws(a.B, N, a.C, a.k, a.dt, rt, a.ws);
   return timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {
     return gl::launch_mrconv(a.x_in, keys, a.idx_use, a.Wt, a.bias, a.x_out, a.B, N, M, a.C, a.C,
                              a.k, a.dt == GL_BF16, rt, ws, h->su, e0, e1);
@@ -312,6 +324,7 @@ const char* gl_status_string(gl_status s) {
     case GL_ERR_ALIAS: return "GL_ERR_ALIAS";
     case GL_ERR_HIP: return "GL_ERR_HIP";
     case GL_ERR_BAD_HANDLE: return "GL_ERR_BAD_HANDLE";
+    case GL_ERR_WORKSPACE: return "GL_ERR_WORKSPACE";
   }
   return "GL_ERR_UNKNOWN";
 }
@@ -343,51 +356,57 @@ gl_status gl_max_pool_nodes(const void* x, int B, int H, int W, int C, int r, gl
   return e == hipSuccess ? GL_OK : hip_fail(e, "max pool launch");
 }
 
+size_t gl_mrconv_workspace_bytes(int B, int N, int C, int k, int Cout, gl_dtype dt) {
+  if (B < 1 || N < 1 || C < 1 || Cout < 1 || k < 1 || k > GL_MAX_K || !dtype_ok(dt) ||
+      !size_ok(B, N, C))
+    return 0;
+  return mrconv_ws_need(B, N, C, k, Cout, dt, mrconv_rt(C, k, dt));
+}
+
+namespace {
+
+// Checks of gl_mrconv / gl_mrconv_heads and of the caller's workspace.
+gl_status check_mrconv_call(const char* who, const void* x, int B, int N, int C, const void* keys,
+                            int M, const int32_t* idx, int k, const void* W, const void* bias,
+                            int Cout, gl_dtype dt, const void* out, const void* ws,
+                            size_t ws_bytes, int* rt) {
+  gl_status s = check_mrconv(x, B, N, C, keys, M, idx, k, W, bias, Cout, dt, out, rt);
+  if (s != GL_OK) return s;
+  const size_t es = esize(dt);
+  return check_ws(who, mrconv_ws_need(B, N, C, k, Cout, dt, *rt), ws, ws_bytes,
+                  {{x, (size_t)B * N * C * es}, {keys, keys ? (size_t)B * M * C * es : 0},
+                   {idx, (size_t)B * N * k * 4}, {W, (size_t)Cout * 2 * C * es},
+                   {bias, bias ? (size_t)Cout * es : 0}, {out, (size_t)B * N * Cout * es}});
+}
+
+}  // namespace
+
 gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
                     const int32_t* idx, int k, const void* W, const void* bias, int Cout,
-                    gl_dtype dt, void* out, hipStream_t stream) {
+                    gl_dtype dt, void* out, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
   int rt = 0;
-  gl_status s = check_mrconv(x, B, N, C, keys, M, idx, k, W, bias, Cout, dt, out, &rt);
+  gl_status s = check_mrconv_call("mrconv", x, B, N, C, keys, M, idx, k, W, bias, Cout, dt, out,
+                                  workspace, workspace_bytes, &rt);
   if (s != GL_OK) return s;
-  const int dtb = dt == GL_BF16;
-  void* ws = nullptr;
-  hipError_t e;
-  if (gl::mrconv_use_split(C, Cout, dtb, rt)) {
-    // stream-ordered workspace for the [x | m] rows of the two-pass form
-    if ((e = hipMallocAsync(&ws, gl::mrconv_split_ws_bytes(B * N, C, dtb), stream)) != hipSuccess)
-      return hip_fail(e, "hipMallocAsync (MRConv workspace)");
-  }
-  e = gl::launch_mrconv(x, keys ? keys : x, idx, W, bias, out, B, N, M, C, Cout, k, dtb, rt, ws,
-                        stream);
-  if (ws) {
-    hipError_t f = hipFreeAsync(ws, stream);
-    if (e == hipSuccess) e = f;
-  }
+  hipError_t e = gl::launch_mrconv(x, keys ? keys : x, idx, W, bias, out, B, N, M, C, Cout, k,
+                                   dt == GL_BF16, rt, workspace, stream);
   return e == hipSuccess ? GL_OK : hip_fail(e, "mrconv launch");
 }
 
 gl_status gl_mrconv_heads(const void* x, int B, int N, int C, const void* keys, int M,
                           const int32_t* idx, int k, const void* W, const void* bias, int heads,
-                          gl_dtype dt, void* out, hipStream_t stream) {
+                          gl_dtype dt, void* out, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
   int rt = 0;
-  gl_status s = check_mrconv(x, B, N, C, keys, M, idx, k, W, bias, C, dt, out, &rt);
+  gl_status s = check_mrconv_call("mrconv_heads", x, B, N, C, keys, M, idx, k, W, bias, C, dt, out,
+                                  workspace, workspace_bytes, &rt);
   if (s != GL_OK) return s;
   if (heads < 1 || C % heads)
     return fail(GL_ERR_BAD_SHAPE, "mrconv_heads: heads=%d must divide C=%d", heads, C);
-  const int dtb = dt == GL_BF16;
-  void* ws = nullptr;
-  hipError_t e;
-  if (gl::mrconv_use_split(C, C, dtb, rt)) {
-    if ((e = hipMallocAsync(&ws, gl::mrconv_split_ws_bytes(B * N, C, dtb), stream)) != hipSuccess)
-      return hip_fail(e, "hipMallocAsync (MRConv workspace)");
-  }
   gl::MrArgs a = gl::make_mr_args(x, keys ? keys : x, idx, W, bias, out, B, N, M, C, C, k);
   a.heads = heads;
-  e = gl::launch_mrconv_args(a, dtb, rt, ws, stream);
-  if (ws) {
-    hipError_t f = hipFreeAsync(ws, stream);
-    if (e == hipSuccess) e = f;
-  }
+  hipError_t e = gl::launch_mrconv_args(a, dt == GL_BF16, rt, workspace, stream);
   return e == hipSuccess ? GL_OK : hip_fail(e, "mrconv launch");
 }
 
@@ -398,8 +417,6 @@ gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_look
   h->magic = kHandleMagic;
   h->su = s_update;
   h->sb = s_build;
-  h->ws = nullptr;
-  h->ws_bytes = 0;
   h->pending = false;
   h->prof_max = 0;
   h->prof_n[0] = h->prof_n[1] = h->prof_n[2] = h->prof_n[3] = 0;
@@ -421,10 +438,6 @@ gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_look
 gl_status gl_lookahead_destroy(gl_lookahead_t h) {
   if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "lookahead_destroy: bad handle");
   free_profiling(h);
-  if (h->ws) {
-    (void)hipStreamSynchronize(h->su);
-    (void)hipFree(h->ws);
-  }
   (void)hipEventDestroy(h->ev_ready);
   (void)hipEventDestroy(h->ev_built);
   h->magic = 0;
@@ -502,13 +515,19 @@ gl_status gl_lookahead_bootstrap(gl_lookahead_t h, const void* x0, int B, int H,
   return mark_built(h);
 }
 
+size_t gl_graphleap_workspace_bytes(int B, int H, int W, int C, int pool_r, int k, gl_dtype dt) {
+  if (H < 1 || W < 1 || pool_r < 1 || H % pool_r || W % pool_r) return 0;
+  return gl_mrconv_workspace_bytes(B, H * W, C, k, C, dt);
+}
+
 gl_status gl_graphleap_block(gl_lookahead_t h, const void* x_in, int B, int H, int W, int C,
                              int pool_r, void* keys_ws, const int32_t* idx_use, int k,
                              const void* Wt, const void* bias, gl_dtype dt, void* x_out,
-                             int32_t* idx_next, int dilation_next) {
+                             int32_t* idx_next, int dilation_next, void* workspace,
+                             size_t workspace_bytes) {
   if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "graphleap_block: bad handle");
   BlockArgs a{x_in, B, H, W, C, pool_r, keys_ws, idx_use, k, Wt, bias, dt, x_out, idx_next,
-              dilation_next};
+              dilation_next, workspace, workspace_bytes};
   int rt = 0;
   gl_status s = check_block(a, &rt);
   if (s != GL_OK) return s;
@@ -518,7 +537,8 @@ gl_status gl_graphleap_block(gl_lookahead_t h, const void* x_in, int B, int H, i
 gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int W, int C,
                              int pool_r, int L, int k, const int* dilations, const void* Ws,
                              const void* bs, gl_dtype dt, gl_schedule schedule, void* x_ws,
-                             int32_t* idx_ws, void* keys_ws, void* x_out) {
+                             int32_t* idx_ws, void* keys_ws, void* x_out, void* workspace,
+                             size_t workspace_bytes) {
   if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "graphleap_stack: bad handle");
   if (!x0 || !dilations || !Ws || !x_ws || !idx_ws || !x_out)
     return fail(GL_ERR_NULL_PTR, "graphleap_stack: x0, dilations, Ws, x_ws, idx_ws, x_out required");
@@ -542,6 +562,12 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
       overlap(x_ws, 2 * xbytes, x0, xbytes) || overlap(idx_ws, 2 * ibytes, keys_ws, kbytes) ||
       overlap(idx_ws, 2 * ibytes, x0, xbytes) || overlap(keys_ws, kbytes, x0, xbytes))
     return fail(GL_ERR_ALIAS, "graphleap_stack: workspaces overlap each other or x0");
+  if (overlap(workspace, workspace_bytes, x_out, xbytes) ||
+      overlap(workspace, workspace_bytes, x_ws, 2 * xbytes) ||
+      overlap(workspace, workspace_bytes, idx_ws, 2 * ibytes) ||
+      overlap(workspace, workspace_bytes, keys_ws, kbytes) ||
+      overlap(workspace, workspace_bytes, x0, xbytes))
+    return fail(GL_ERR_ALIAS, "graphleap_stack: workspace overlaps another buffer");
   char* xw[2] = {static_cast<char*>(x_ws), static_cast<char*>(x_ws) + xbytes};
   int32_t* iw[2] = {idx_ws, idx_ws + (size_t)B * N * k};
   const char* Wb = static_cast<const char*>(Ws);
@@ -554,7 +580,8 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
     BlockArgs& a = blocks[l];
     a = BlockArgs{l == 0 ? x0 : xw[(l - 1) & 1], B, H, W, C, pool_r, keys_ws, iw[0], k,
                   Wb + l * wbytes, bb ? bb + l * bbytes : nullptr, dt,
-                  l == L - 1 ? x_out : static_cast<void*>(xw[l & 1]), nullptr, 1};
+                  l == L - 1 ? x_out : static_cast<void*>(xw[l & 1]), nullptr, 1, workspace,
+                  workspace_bytes};
     if (schedule != GL_SCHED_STANDARD && l + 1 < L) {
       a.idx_next = iw[1];
       a.dil_next = dilations[l + 1];
@@ -579,8 +606,7 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
       e = gl::launch_knn(a.x_in, pooled ? keys_ws : a.x_in, B, N, C, M, k, dilations[l],
                          dt == GL_BF16, iw[0], h->su);
       if (e != hipSuccess) return hip_fail(e, "knn launch");
-      void* ws;
-      if ((s = block_ws(h, B, N, C, dt, rts[l], &ws)) != GL_OK) return s;
+      void* ws = block_ws(B, N, C, k, dt, rts[l], workspace);
       e = gl::launch_mrconv(a.x_in, pooled ? keys_ws : a.x_in, iw[0], a.Wt, a.bias, a.x_out, B, N,
                             M, C, C, k, dt == GL_BF16, rts[l], ws, h->su);
       if (e != hipSuccess) return hip_fail(e, "mrconv launch");
@@ -612,8 +638,7 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
       const bool build = l + 1 < L && !(l == 0 && dilations[1] == dilations[0]);
       const gl::MrArgs ma = gl::make_mr_args(a.x_in, keys, iw[cur], a.Wt, a.bias, a.x_out, B, N, M,
                                              C, C, k);
-      void* ws;
-      if ((s = block_ws(h, B, N, C, dt, rts[l], &ws)) != GL_OK) return s;
+      void* ws = block_ws(B, N, C, k, dt, rts[l], workspace);
       if (build && !gl::knn_separate(M, C, dtb) && !ws) {
         next = 1 - cur;
         const gl::KnnArgs ka = gl::make_knn_args(a.x_in, keys, B, N, C, M, k, dilations[l + 1],
@@ -788,8 +813,9 @@ gl_status enqueue_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, in
   if (schedule == GL_SCHED_LOOKAHEAD && (s = join_build(h)) != GL_OK) return s;
   if (!u_ready && (s = lin("linear launch (FC1)", x_in, C, p.W_in, p.b_in, C, 0, 0, nullptr, u)) != GL_OK)
     return s;
-  void* mws;
-  if ((s = block_ws(h, B, N, C, dt, rt, &mws)) != GL_OK) return s;
+  // the two-pass MRConv's [x | m] rows go to the FFN's hidden-row region,
+  // which is free until FFN1 (later on the same stream) overwrites it
+  void* mws = block_ws(B, N, C, k, dt, rt, w.hid);
   const bool fused = schedule == GL_SCHED_LOOKAHEAD_FUSED && idx_next &&
                      !gl::knn_separate(N, C, dtb) && !mws;
   if (fused) {

@@ -75,8 +75,8 @@ def test_knn_validation():
 
 
 def _mr(x=P(0), B=2, N=196, C=192, keys=None, M=196, idx=P(20), k=9, W=P(30), bias=None,
-        Cout=192, dt=1, out=P(40)):
-    st = api.lib().gl_mrconv(x, B, N, C, keys, M, idx, k, W, bias, Cout, dt, out, None)
+        Cout=192, dt=1, out=P(40), ws=None, wsb=0):
+    st = api.lib().gl_mrconv(x, B, N, C, keys, M, idx, k, W, bias, Cout, dt, out, ws, wsb, None)
     return api.STATUS[st]
 
 
@@ -94,9 +94,8 @@ def test_mrconv_validation():
     assert _mr(C=20) == "GL_ERR_UNSUPPORTED"
     # one image's keys beyond 2^31 16-byte vectors (the kernels' row offsets)
     assert _mr(keys=P(10), M=1 << 24, C=1024) == "GL_ERR_BAD_SHAPE"
-    # too wide for one LDS tile: not rejected, the two-pass form takes it (and
-    # fails only at its workspace allocation here, with no GPU)
-    assert _mr(C=8192) == "GL_ERR_HIP"
+    # too wide for one LDS tile: the two-pass form takes it, with a workspace
+    assert _mr(C=8192) == "GL_ERR_WORKSPACE"
     assert _mr(W=ctypes.c_void_p(A * 31 + 4)) == "GL_ERR_ALIGNMENT"
     assert _mr(bias=ctypes.c_void_p(A * 50 + 1)) == "GL_ERR_ALIGNMENT"
     assert _mr(out=ctypes.c_void_p(A + 64)) == "GL_ERR_ALIAS"    # out inside x
@@ -134,12 +133,41 @@ def test_max_pool_validation():
 
 
 @host_only
+def test_mrconv_workspace():
+    """The two-pass form (W beyond 8 KB per node of the fused tile) needs the
+    caller's [B*N, 2C] workspace; the fused tile needs none."""
+    L = api.lib()
+    need = L.gl_mrconv_workspace_bytes(64, 196, 640, 9, 640, 1)
+    assert need == 64 * 196 * 1280 * 2
+    assert L.gl_mrconv_workspace_bytes(32, 196, 192, 9, 192, 1) == 0
+    assert L.gl_mrconv_workspace_bytes(0, 196, 192, 9, 192, 1) == 0
+    assert L.gl_mrconv_workspace_bytes(2, 196, 192, 9, 192, 5) == 0     # bad dtype
+    assert L.gl_graphleap_workspace_bytes(64, 14, 14, 640, 1, 9, 1) == need
+    assert L.gl_graphleap_workspace_bytes(32, 14, 14, 192, 1, 9, 1) == 0
+    assert L.gl_graphleap_workspace_bytes(32, 14, 14, 192, 3, 9, 1) == 0  # 14 % 3 != 0
+    big = dict(B=64, C=640, Cout=640)
+    assert _mr(**big) == "GL_ERR_WORKSPACE"
+    assert _mr(**big, ws=P(60), wsb=need - 1) == "GL_ERR_WORKSPACE"
+    assert _mr(**big, ws=ctypes.c_void_p(A * 61 + 8), wsb=need) == "GL_ERR_WORKSPACE"
+    assert _mr(**big, ws=P(0), wsb=need) == "GL_ERR_ALIAS"              # on top of x
+    assert _mr(**big, ws=ctypes.c_void_p(A * 40), wsb=need) == "GL_ERR_ALIAS"  # ends in out
+    # a workspace is accepted where none is needed
+    assert _mr(ws=P(60), wsb=1) != "GL_ERR_WORKSPACE"
+    # a good workspace passes every check; with no GPU the launch itself fails
+    assert _mr(**big, ws=P(60), wsb=need) == "GL_ERR_HIP"
+    L = api.lib()
+    st = L.gl_mrconv_heads(P(0), 64, 196, 640, None, 196, P(20), 9, P(30), None, 16, 1, P(40),
+                           None, 0, None)
+    assert api.STATUS[st] == "GL_ERR_WORKSPACE"
+
+
+@host_only
 def test_handle_validation():
     L = api.lib()
     assert api.STATUS[L.gl_lookahead_destroy(None)] == "GL_ERR_BAD_HANDLE"
     assert api.STATUS[L.gl_lookahead_set_profiling(None, 4)] == "GL_ERR_BAD_HANDLE"
     assert api.STATUS[L.gl_graphleap_block(None, P(0), 1, 14, 14, 192, 1, None, P(1), 9, P(2),
-                                           None, 1, P(3), None, 1)] == "GL_ERR_BAD_HANDLE"
+                                           None, 1, P(3), None, 1, None, 0)] == "GL_ERR_BAD_HANDLE"
     assert api.STATUS[L.gl_lookahead_create(None, None, None)] == "GL_ERR_NULL_PTR"
 
 
@@ -182,7 +210,9 @@ def test_vig_validation():
 @host_only
 def test_mrconv_heads_validation():
     L = api.lib()
-    st = L.gl_mrconv_heads(P(0), 2, 196, 192, None, 196, P(10), 9, P(20), None, 5, 1, P(30), None)
+    st = L.gl_mrconv_heads(P(0), 2, 196, 192, None, 196, P(10), 9, P(20), None, 5, 1, P(30), None,
+                           0, None)
     assert api.STATUS[st] == "GL_ERR_BAD_SHAPE"          # 5 does not divide 192
-    st = L.gl_mrconv_heads(P(0), 2, 196, 192, None, 196, P(10), 9, P(20), None, 0, 1, P(30), None)
+    st = L.gl_mrconv_heads(P(0), 2, 196, 192, None, 196, P(10), 9, P(20), None, 0, 1, P(30), None,
+                           0, None)
     assert api.STATUS[st] == "GL_ERR_BAD_SHAPE"
