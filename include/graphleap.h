@@ -170,6 +170,25 @@ gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
                     hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * gl_mrconv_noalloc -- gl_mrconv for callers that cannot allocate memory or
+ * pass a workspace: code under HIP graph capture, serving loops and harnesses
+ * that forbid allocation.  Same operation, arguments, layout and errors as
+ * gl_mrconv, without the workspace.  The two-pass form's [x_i, m_i] rows go
+ * to a buffer inside the library, GL_NOALLOC_SCRATCH_BYTES per device, which
+ * a device holds from the library's load until the process ends; a layer
+ * whose gl_mrconv_workspace_bytes() exceeds it fails with GL_ERR_WORKSPACE
+ * before anything is enqueued.  The call itself allocates nothing.  Every
+ * call on one device shares that buffer and it keeps the last call's rows:
+ * calls that can overlap on one device (several streams or threads) race,
+ * and the caller must order them.  `stream` must belong to the current
+ * device (GL_ERR_UNSUPPORTED otherwise).
+ * -------------------------------------------------------------------------*/
+#define GL_NOALLOC_SCRATCH_BYTES (32u << 20)   /* 32 MiB */
+gl_status gl_mrconv_noalloc(const void* x, int B, int N, int C, const void* keys, int M,
+                            const int32_t* idx, int k, const void* W, const void* bias, int Cout,
+                            gl_dtype dt, void* out, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * gl_mrconv_heads -- the multi-head MRConv update (Sec. II-A; per-head
  * W_x,h / W_m,h of Sec. IV-C2): channels split into `heads` equal contiguous
  * heads of hd = C / heads, and output head h sees only head h's channels of

@@ -44,6 +44,7 @@ SIGNATURES = {
     "gl_max_pool_nodes": [_vp, _i, _i, _i, _i, _i, _i, _vp, _vp],
     "gl_mrconv_workspace_bytes": [_i, _i, _i, _i, _i, _i],
     "gl_mrconv": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _sz, _vp],
+    "gl_mrconv_noalloc": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp],
     "gl_mrconv_heads": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _sz, _vp],
     "gl_lookahead_create": [_vp, _vp, ctypes.POINTER(_vp)],
     "gl_lookahead_destroy": [_vp],
@@ -198,6 +199,21 @@ def mrconv(x: torch.Tensor, idx: torch.Tensor, W: torch.Tensor, bias: torch.Tens
     else:
         _call("gl_mrconv", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(W), _p(bias), Cout, _dt(x),
               _p(out), _p(ws), ws.nbytes, _s(stream))
+    return out
+
+
+def mrconv_noalloc(x: torch.Tensor, idx: torch.Tensor, W: torch.Tensor,
+                   bias: torch.Tensor | None = None, keys: torch.Tensor | None = None,
+                   out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """gl_mrconv_noalloc: the update with the library's own scratch buffer (no
+    workspace; calls on one device must not overlap)."""
+    B, N, C = x.shape
+    M = N if keys is None else keys.shape[1]
+    Cout = W.shape[0]
+    if out is None:
+        out = torch.empty((B, N, Cout), dtype=x.dtype, device=x.device)
+    _call("gl_mrconv_noalloc", _p(x), B, N, C, _p(keys), M, _p(idx), idx.shape[2], _p(W), _p(bias),
+          Cout, _dt(x), _p(out), _s(stream))
     return out
 
 

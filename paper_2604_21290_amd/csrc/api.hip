@@ -5,6 +5,7 @@
 
 #include <climits>
 #include <initializer_list>
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -981,3 +982,67 @@ gl_status gl_vig_stack(gl_lookahead_t h, const void* x0, int B, int N, int C, in
 }
 
 }  // extern "C"
+
+// ===========================================================================
+// MRConv that allocates nothing and takes no workspace (gl_mrconv_noalloc).
+// ===========================================================================
+namespace {
+
+// The [x | m] rows of the two-pass MRConv of gl_mrconv_noalloc.  Each device
+// the library runs on holds its own copy until the process ends.  In host code
+// this name stands for a host-side shadow, not device memory: kernels get the
+// device address taken with hipGetSymbolAddress (scratch_ptr below).
+static __device__ __align__(256) char scratch[GL_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, taken once per device
+// (with that device current) and kept.  The stream must belong to it.
+gl_status scratch_ptr(hipStream_t stream, void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (stream) {
+    int sdev = -1;
+    if ((e = hipStreamGetDevice(stream, &sdev)) != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+    if (sdev != dev)
+      return fail(GL_ERR_UNSUPPORTED, "mrconv_noalloc: the stream is on device %d, the current device is %d",
+                  sdev, dev);
+  }
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(GL_ERR_UNSUPPORTED, "mrconv_noalloc: device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess)
+      return hip_fail(e, "hipGetSymbolAddress (scratch)");
+    if (!p) return fail(GL_ERR_HIP, "hipGetSymbolAddress (scratch) returned NULL");
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return GL_OK;
+}
+
+}  // namespace
+
+extern "C" gl_status gl_mrconv_noalloc(const void* x, int B, int N, int C, const void* keys, int M,
+                                       const int32_t* idx, int k, const void* W, const void* bias,
+                                       int Cout, gl_dtype dt, void* out, hipStream_t stream) {
+  int rt = 0;
+  gl_status s = check_mrconv(x, B, N, C, keys, M, idx, k, W, bias, Cout, dt, out, &rt);
+  if (s != GL_OK) return s;
+  const size_t need = mrconv_ws_need(B, N, C, k, Cout, dt, rt);
+  if (need > (size_t)GL_NOALLOC_SCRATCH_BYTES)
+    return fail(GL_ERR_WORKSPACE,
+                "mrconv_noalloc: this layer needs %zu bytes of scratch, beyond the library's %zu "
+                "(use gl_mrconv with a workspace)",
+                need, (size_t)GL_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if (need && (s = scratch_ptr(stream, &ws)) != GL_OK) return s;
+  // the gather writes every [x | m] row the GEMM reads: nothing to clear
+  hipError_t e = gl::launch_mrconv(x, keys ? keys : x, idx, W, bias, out, B, N, M, C, Cout, k,
+                                   dt == GL_BF16, rt, ws, stream);
+  return e == hipSuccess ? GL_OK : hip_fail(e, "mrconv launch");
+}

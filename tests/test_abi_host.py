@@ -162,6 +162,24 @@ def test_mrconv_workspace():
 
 
 @host_only
+def test_mrconv_noalloc_validation():
+    """gl_mrconv_noalloc checks like gl_mrconv and refuses layers whose
+    two-pass rows exceed the library's scratch buffer before any HIP call."""
+    L = api.lib()
+
+    def na(B=2, N=196, C=192, Cout=192, x=P(0), out=P(40)):
+        st = L.gl_mrconv_noalloc(x, B, N, C, None, N, P(20), 9, P(30), None, Cout, 1, out, None)
+        return api.STATUS[st], L.gl_last_error().decode()
+
+    assert na(x=None)[0] == "GL_ERR_NULL_PTR"
+    assert na(out=ctypes.c_void_p(A + 64))[0] == "GL_ERR_ALIAS"
+    st, msg = na(B=64, C=1024, Cout=1024, out=P(200))    # 51 MB of rows > 32 MiB
+    assert st == "GL_ERR_WORKSPACE" and "scratch" in msg, msg
+    text = open(HEADER).read()
+    assert "#define GL_NOALLOC_SCRATCH_BYTES (32u << 20)" in text
+
+
+@host_only
 def test_handle_validation():
     L = api.lib()
     assert api.STATUS[L.gl_lookahead_destroy(None)] == "GL_ERR_BAD_HANDLE"

@@ -1,0 +1,75 @@
+"""gl_mrconv_noalloc (the update for callers that cannot allocate) against
+gl_mrconv with a caller workspace, through the C ABI: two calls in a row, the
+second smaller, on the two-pass form that uses the library's scratch buffer
+and on the fused tile that needs none.  Results must be bit-identical (same
+kernels, same inputs) and within the oracle's tolerance."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from gpu_helpers import check_close, from_dev, mrconv_mag, require_gpu, to_dev
+from paper_2604_21290_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[gpu-test]", *a, flush=True)
+
+
+def _case(g, B, N, C, Cout, k, M=None, dt=I.BF16):
+    x = I.store(g.standard_normal((B, N, C)), dt)
+    keys = None if M is None else I.store(g.standard_normal((B, M, C)), dt)
+    idx = g.integers(0, N if M is None else M, (B, N, k)).astype(np.int32)
+    W = I.store(g.uniform(-0.1, 0.1, (Cout, 2 * C)), dt)
+    b = I.store(g.uniform(-1, 1, Cout), dt)
+    return x, keys, idx, W, b
+
+
+def _run(label, x, keys, idx, W, b):
+    from paper_2604_21290_amd import api
+    B, N, C = x.shape
+    _say("noalloc", label, (B, N, C), "Cout", W.shape[0], "k", idx.shape[2],
+         "workspace bytes", api.lib().gl_mrconv_workspace_bytes(B, N, C, idx.shape[2], W.shape[0],
+                                                                 api.GL_BF16 if x.dtype == I.BF16
+                                                                 else api.GL_F32))
+    xd, idd, Wd, bd = to_dev(x), torch.from_numpy(idx).cuda(), to_dev(W), to_dev(b)
+    kd = None if keys is None else to_dev(keys)
+    ref_gpu = api.mrconv(xd, idd, Wd, bd, keys=kd)
+    got = api.mrconv_noalloc(xd, idd, Wd, bd, keys=kd)
+    torch.cuda.synchronize()
+    assert torch.equal(got, ref_gpu), f"{label}: gl_mrconv_noalloc differs from gl_mrconv"
+    ref, xcat = O.mrconv_ref(x.value, idx, W.value, b.value,
+                             keys=None if keys is None else keys.value, return_concat=True)
+    check_close(from_dev(got).value, ref, x.dtype, label, mag=mrconv_mag(xcat, W.value),
+                n_terms=2 * C)
+
+
+def test_noalloc_two_pass_then_smaller():
+    require_gpu()
+    g = np.random.default_rng(2024)
+    # ViG-B-shaped layer (C = Cout = 640: the two-pass form, 2.5 MB of scratch),
+    # then a smaller one with pooled keys and a ragged node count
+    _run("two-pass 8x196x640", *_case(g, 8, 196, 640, 640, 9))
+    _run("two-pass smaller 3x77x512 pooled", *_case(g, 3, 77, 512, 512, 7, M=49))
+
+
+def test_noalloc_full_scratch_then_fused():
+    require_gpu()
+    g = np.random.default_rng(2025)
+    # the largest ViG-B batch that fits the 32 MiB scratch (B = 64: 32.1 MB),
+    # then a narrow layer on the fused tile (no scratch)
+    _run("two-pass 64x196x640", *_case(g, 64, 196, 640, 640, 9))
+    _run("fused 4x196x192", *_case(g, 4, 196, 192, 192, 9))
+
+
+def test_noalloc_rejects_beyond_scratch():
+    require_gpu()
+    from paper_2604_21290_amd import api
+    x = torch.zeros((64, 196, 1024), dtype=torch.bfloat16, device="cuda")
+    idx = torch.zeros((64, 196, 9), dtype=torch.int32, device="cuda")
+    W = torch.zeros((1024, 2048), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(api.GraphLeapError) as e:
+        api.mrconv_noalloc(x, idx, W)
+    assert e.value.status == 9, e.value
