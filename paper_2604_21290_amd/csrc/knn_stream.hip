@@ -15,10 +15,12 @@
 //      floor), followed by a compare against the row's threshold: the
 //      K'-th packed key's distance bucket plus one, so no candidate that
 //      could enter the list is dropped.
-//   3. Every lane owns kStSlots LDS slots per row of its 4 rows and appends
-//      without branching: it always stores (passing key, or the empty marker
-//      0xffffffff) at its next free slot and advances the slot count by the
-//      pass bit.  When some lane's slots could overflow in the next group of
+//   3. Every lane owns kStSlots LDS slots per row of its 4 rows (empty slots
+//      hold the marker 0xffffffff) and appends the keys that pass at its
+//      next free slot; a group of tiles in which no candidate of the wave
+//      passes skips the packing and stores.  Chunks are visited starting at
+//      the workgroup's own place in the key set, which tightens the
+//      thresholds early on image grids.  When some lane's slots could overflow in the next group of
 //      tiles, and at the end, the wave merges its 16 rows' slots into their
 //      sorted register lists (4 rows at a time, 16 lanes per row, the same
 //      bitonic merge as the in-register kernel), empties the slots and
@@ -170,34 +172,54 @@ __device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], ui
                                          uint32_t* tauL, int KK, int ib, int lane, int g, int t) {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   __builtin_amdgcn_wave_barrier();
+  // The rows of two list registers at a time are merged together: their sorts
+  // and merges are independent dependency chains, which the scheduler
+  // interleaves (one chain alone leaves the VALU waiting on each step).
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const int row = 4 * p + g;
-    uint32_t tk = list_element<R>(L[p], KK - 1, lane);
+  for (int p0 = 0; p0 < 4; p0 += 2) {
+    uint32_t tk[2];
+    uint32_t v4[2][kStSlots];
     int tr = t;
-    asm volatile("" : "+v"(tr));  // keeps the 8 slot addresses out of the caller's loops
-    uint32_t v4[kStSlots];
-    // slot m of lane (t + m) mod 16: a lane's used slots spread over 16 readers
+    asm volatile("" : "+v"(tr));  // keeps the slot addresses out of the caller's loops
 #pragma unroll
-    for (int m = 0; m < kStSlots; ++m) {
-      uint32_t* slot = cand + row * kStRowStride + 16 * m + ((tr + m) & 15);
-      const uint32_t c = *slot;
-      *slot = 0xffffffffu;
-      v4[m] = c < tk ? c : 0xffffffffu;
+    for (int pp = 0; pp < 2; ++pp) {
+      const int row = 4 * (p0 + pp) + g;
+      tk[pp] = list_element<R>(L[p0 + pp], KK - 1, lane);
+      // slot m of lane (t + m) mod 16: a lane's used slots spread over 16 readers
+#pragma unroll
+      for (int m = 0; m < kStSlots; ++m) {
+        uint32_t* slot = cand + row * kStRowStride + 16 * m + ((tr + m) & 15);
+        const uint32_t c = *slot;
+        *slot = 0xffffffffu;
+        v4[pp][m] = c < tk[pp] ? c : 0xffffffffu;
+      }
     }
     bool pass = false;
 #pragma unroll
-    for (int m = 0; m < kStSlots; ++m) pass |= v4[m] != 0xffffffffu;
+    for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+      for (int m = 0; m < kStSlots; ++m) pass |= v4[pp][m] != 0xffffffffu;
     if (__any(pass)) {
-      sort_regs_asc<kStSlots>(v4);
+#pragma unroll
+      for (int pp = 0; pp < 2; ++pp) sort_regs_asc<kStSlots>(v4[pp]);
+      // layer m of both rows, while either still has a key below its
+      // threshold (merging a layer with none changes nothing among a list's
+      // first K' keys: keys are unique)
 #pragma unroll
       for (int m = 0; m < kStSlots; ++m) {
-        if (!__any(v4[m] < tk)) break;
-        merge16_into_list<R>(L[p], sort16_lanes(v4[m], t), t);
-        tk = list_element<R>(L[p], KK - 1, lane);
+        if (!__any(v4[0][m] < tk[0] || v4[1][m] < tk[1])) break;
+        const uint32_t c0 = sort16_lanes(v4[0][m], t);
+        const uint32_t c1 = sort16_lanes(v4[1][m], t);
+        merge16_into_list<R>(L[p0], c0, t);
+        merge16_into_list<R>(L[p0 + 1], c1, t);
+        tk[0] = list_element<R>(L[p0], KK - 1, lane);
+        tk[1] = list_element<R>(L[p0 + 1], KK - 1, lane);
       }
     }
-    if (t == 0) tauL[row] = tk;
+    if (t == 0) {
+      tauL[4 * p0 + g] = tk[0];
+      tauL[4 * (p0 + 1) + g] = tk[1];
+    }
   }
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -298,12 +320,20 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
   // One LDS key buffer; the next chunk waits in registers while this one is used.
   char* kbuf = kbuf0;
   const int nchunks = (M + KC - 1) / KC;
+  // The chunks are visited in a rotated order that starts with the chunk at
+  // the workgroup's own position in the key set (its first query row scaled
+  // by M / N).  The selected lists do not depend on the order; on image
+  // grids a node's nearest keys tend to lie near it, so the thresholds
+  // tighten after the first chunk and fewer candidates pass the filter.
+  const int ch0 = (int)(((long long)q0 * M / N) / KC);
   // A chunk of at most MV vectors per thread is prefetched into registers
   // while the previous one is used; larger chunks are copied piecewise when
   // their turn comes.
   const bool prefetch = nvec <= MV * kStThreads;
-  if (prefetch) st_load_chunk<DT>(regs, kb, 0, M, C, CG, nvec, 0, tid);
-  for (int ch = 0; ch < nchunks; ++ch) {
+  if (prefetch) st_load_chunk<DT>(regs, kb, ch0 * KC, M, C, CG, nvec, 0, tid);
+  for (int c = 0; c < nchunks; ++c) {
+    const int ch = ch0 + c < nchunks ? ch0 + c : ch0 + c - nchunks;
+    const int chn = ch + 1 < nchunks ? ch + 1 : 0;
     const int k0 = ch * KC;
     const int ntl = (min(KC, M - k0) + 15) >> 4;
     if (prefetch) {
@@ -317,7 +347,7 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
     __syncthreads();
     st_chunk_scales<DT, KS>(kbuf, ksc0, KC, kstride, k0, M, C, qscale, tid);
     __syncthreads();
-    if (prefetch && ch + 1 < nchunks) st_load_chunk<DT>(regs, kb, k0 + KC, M, C, CG, nvec, 0, tid);
+    if (prefetch && c + 1 < nchunks) st_load_chunk<DT>(regs, kb, chn * KC, M, C, CG, nvec, 0, tid);
     // Gram tiles of group t0 + 4 are issued before the epilogue of group t0
     // (independent MFMA chains run while the VALU filters).  All KC rows of the
     // key buffer hold finite values (the chunk loader repeats the last key),
@@ -341,18 +371,33 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
       } else {
         st_gram<DT, KS>(acc, af, kbuf, t0, kstride, C, g, t);
       }
+      // The common path per candidate is the distance and one compare; the
+      // packing and the slot store run only for the candidates that pass
+      // (empty slots already hold the empty marker), and not at all in a
+      // group where no lane of the wave has one.
+      float dd[kStGroup][4];
+      bool anyp = false;
 #pragma unroll
       for (int p = 0; p < kStGroup; ++p) {
-        const int tt = t0 + p;
-        const float2 sc = ksc0[tt * 16 + t];
-        const uint32_t j = (uint32_t)(k0 + tt * 16 + t);
+        const float2 sc = ksc0[(t0 + p) * 16 + t];
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const float d1s = fmaf(acc[p][v] * sc.x, qr[v], sc.y);
-          const bool pass = d1s < tS[v];
-          const uint32_t q = (uint32_t)__builtin_amdgcn_fmed3f(d1s, 0.f, qmaxf);
-          mySlots[v * kStRowStride + 16 * nS[v]] = pass ? (q << ib) | j : 0xffffffffu;
-          nS[v] += pass ? 1 : 0;
+          dd[p][v] = fmaf(acc[p][v] * sc.x, qr[v], sc.y);
+          anyp |= dd[p][v] < tS[v];
+        }
+      }
+      if (__any(anyp)) {
+#pragma unroll
+        for (int p = 0; p < kStGroup; ++p) {
+          const uint32_t j = (uint32_t)(k0 + (t0 + p) * 16 + t);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            if (dd[p][v] < tS[v]) {
+              const uint32_t q = (uint32_t)__builtin_amdgcn_fmed3f(dd[p][v], 0.f, qmaxf);
+              mySlots[v * kStRowStride + 16 * nS[v]] = (q << ib) | j;
+              ++nS[v];
+            }
+          }
         }
       }
       if (PIPE) {
