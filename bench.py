@@ -123,6 +123,21 @@ def algorithmic(w, es):
     return knn_flops, knn_bytes, mr_flops, mr_bytes
 
 
+def layer_work(w, es):
+    """Algorithmic work of one layer (one kNN build + one MRConv update), with
+    bytes counted once each at their HBM size: X read by the build, X (and
+    pooled keys) read by the update, the graph written by the build and read
+    by the update, W, the output, and the key pooling's own I/O."""
+    B, N, M, C, k = w.B, w.N, w.M, w.C, w.k
+    pooled = w.pool_r > 1
+    x = B * N * C * es
+    keys = B * M * C * es if pooled else 0
+    idx = B * N * k * 4
+    flops = 2.0 * B * N * M * C + 2.0 * B * N * (2 * C) * C
+    by = (x + keys) + (x + keys) + 2 * idx + 2 * C * C * es + x + ((x + keys) if pooled else 0)
+    return flops, by
+
+
 def _oracle_stack_worker(task) -> float:
     """One process of the CPU baseline: the oracle's stack on a slice of the
     batch, `reps` times, on one thread; returns its seconds."""
@@ -359,6 +374,104 @@ def cold_gather(w, api, torch, x0, idx, W, b, out, mr_bytes, reps: int = 20) -> 
                       f"- median(write alone) over {reps} pairs"}
 
 
+def measure_config(name, w, api, I, dev, torch, steps: int, warmup: int) -> dict:
+    """One workload of the benchmark's configuration set, measured the way the
+    headline is: its L-block stack under the one-launch schedule (layers/s),
+    every launch of a second pass stamped by its own dispatch (the dominant
+    kernel and its roofline), and the two metric components on their own --
+    the standalone kNN build (Gram MFMA fraction) and MRConv update (gather
+    HBM bandwidth) -- averaged over back-to-back launches with HIP events."""
+    import numpy as np
+    es = 2 if w.dtype == I.BF16 else 4
+    peak = PEAK_TFLOPS[w.dtype]
+    x0 = dev(I.make_features(w))
+    Wd = dev(I.Stored(np.stack([I.make_weight(w, l).bits for l in range(w.L)]), None, w.dtype))
+    bd = dev(I.Stored(np.stack([I.make_bias(w, l).bits for l in range(w.L)]), None, w.dtype))
+    s = torch.cuda.current_stream()
+    la = api.Lookahead(s, torch.cuda.Stream())
+    ws = api.make_stack_workspace(x0, w.H, w.W, w.k, w.pool_r)
+    out = torch.empty_like(x0)
+    dil = list(w.dilations)
+
+    def step():
+        la.stack(x0, w.H, w.W, Wd, bd, dil, w.k, w.pool_r, schedule=api.GL_SCHED_LOOKAHEAD_FUSED,
+                 ws=ws, x_out=out)
+
+    def timed(fn, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(s)
+        for _ in range(n):
+            fn()
+        e1.record(s)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    for _ in range(warmup):
+        step()
+    ms = timed(step, steps)
+    value = w.L / (ms / 1e3)
+    # per-launch durations, stamped by each dispatch on its own stream
+    n_rec = steps * w.L + 8
+    la.set_profiling(n_rec)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    times = {key: la.kernel_times_ms(which, n_rec) for key, which in
+             (("knn_graph", api.GL_TIME_BUILD), ("mrconv", api.GL_TIME_UPDATE),
+              ("graphleap_block", api.GL_TIME_FUSED))}
+    la.set_profiling(0)
+    la.close()
+    knn_flops, knn_bytes, mr_flops, mr_bytes = algorithmic(w, es)
+    F, Y = layer_work(w, es)
+    pool_io = (w.B * w.N * w.C + w.B * w.M * w.C) * es if w.pool_r > 1 else 0
+    kern = {}
+    for key, t in times.items():
+        if not t:
+            continue
+        avg = sum(t) / len(t) * 1e-3
+        e = {"launches_per_step": len(t) / steps, "avg_us": avg * 1e6, "us_per_step": sum(t) / steps * 1e3}
+        if key == "knn_graph":
+            e.update(bound="mfma", achieved=knn_flops / avg / 1e12, peak=peak, unit="TFLOP/s")
+        elif key == "mrconv":
+            e.update(bound="hbm", achieved=mr_bytes / avg / 1e9, peak=PEAK_HBM_GBS, unit="GB/s")
+        else:   # one launch = one layer's build and update
+            yb = Y - pool_io
+            if yb / (PEAK_HBM_GBS * 1e9) >= F / (peak * 1e12):
+                e.update(bound="hbm", achieved=yb / avg / 1e9, peak=PEAK_HBM_GBS, unit="GB/s")
+            else:
+                e.update(bound="mfma", achieved=F / avg / 1e12, peak=peak, unit="TFLOP/s")
+        e["frac"] = e["achieved"] / e["peak"]
+        kern[key] = e
+    dom = max(kern, key=lambda k_: kern[k_]["us_per_step"])
+    # the metric's two components, each kernel on its own
+    keys = api.pool_keys(x0, w.H, w.W, w.pool_r) if w.pool_r > 1 else None
+    idx = torch.empty((w.B, w.N, w.k), dtype=torch.int32, device=x0.device)
+    n = max(10, steps // 2)
+    t_knn = timed(lambda: api.knn_graph(x0, w.k, dil[-1], keys=keys, out=idx), n) * 1e-3
+    mws = api.mrconv_workspace(w.B, w.N, w.C, w.k, w.C, x0.dtype, x0.device)
+    t_mr = timed(lambda: api.mrconv(x0, idx, Wd[0], bd[0], keys=keys, out=out, ws=mws), n) * 1e-3
+    t_floor = max(F / (peak * 1e12), Y / (PEAK_HBM_GBS * 1e9))
+    return {
+        "workload": f"{name}: {DESCR[name]}", "dtype": w.dtype, "layers_per_s": value,
+        "ms_per_step": ms, "steps": steps, "schedule": "fused",
+        "dominant_kernel": {"kernel": dom, **{k_: kern[dom][k_] for k_ in
+                                              ("bound", "achieved", "peak", "unit", "frac", "avg_us")}},
+        "kernels": kern,
+        "gram_mfma": {"kernel": "gl_knn_graph", "d": dil[-1], "avg_us": t_knn * 1e6,
+                      "tflops": knn_flops / t_knn / 1e12, "frac": knn_flops / t_knn / 1e12 / peak},
+        "gather_hbm": {"kernel": "gl_mrconv", "avg_us": t_mr * 1e6, "gbs": mr_bytes / t_mr / 1e9,
+                       "frac": mr_bytes / t_mr / 1e9 / PEAK_HBM_GBS,
+                       "effective_gbs": w.B * w.N * w.k * w.C * es / t_mr / 1e9},
+        "layer": {"flop": F, "bytes": Y, "roofline_layers_per_s": 1.0 / t_floor,
+                  "frac": value * t_floor},
+    }
+
+
+# the benchmark's configuration set besides the headline (one GPU each)
+CONFIG_SET = ("single", "vig_b", "pyr_s1", "pyr_s2", "hires")
+
+
 def full_block(args, w, api, I, dev, torch) -> dict:
     """Time the full ViG block stack (gl_vig_stack) under its three schedules
     and profile its launches."""
@@ -433,6 +546,9 @@ def main() -> int:
     ap.add_argument("--cpu-images", type=int, default=32)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other configurations (single, vig_b, pyr_s1, pyr_s2, hires)")
+    ap.add_argument("--config-steps", type=int, default=30)
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -578,16 +694,20 @@ def main() -> int:
             "fc_tflops": mr_flops / t / 1e12, "fc_mfma_frac": mr_flops / t / 1e12 / peak,
             "hbm_gbs": mr_bytes / t / 1e9, "hbm_frac": mr_bytes / t / 1e9 / PEAK_HBM_GBS,
             "gather_effective_gbs": (w.B * w.N * w.k * w.C * es) / t / 1e9}
-    # one-launch block: X read once by both roles, the used graph read, the next
-    # graph written, W read, X^(l+1) written
-    fb_flops = knn_flops + mr_flops
-    fb_bytes = mr_bytes + w.B * w.N * w.k * 4
+    # one-launch block = one layer: the layer's algorithmic bytes (X read by the
+    # build and again by the update, the graph written and read, W, X^(l+1)
+    # written); the block's own floor (X read once by both roles) is reported
+    # beside it
+    fb_flops, fb_bytes = layer_work(w, es)
+    fb_bytes -= (w.B * w.N * w.C + w.B * w.M * w.C) * es if w.pool_r > 1 else 0
+    fb_floor = mr_bytes + w.B * w.N * w.k * 4
     if tf:
         t = sum(tf) / len(tf) * 1e-3
         kernels["graphleap_block"] = {
             "launches_per_step": len(tf) / args.steps, "avg_us": t * 1e6,
             "tflops": fb_flops / t / 1e12, "mfma_frac": fb_flops / t / 1e12 / peak,
-            "hbm_gbs": fb_bytes / t / 1e9, "hbm_frac": fb_bytes / t / 1e9 / PEAK_HBM_GBS}
+            "hbm_gbs": fb_bytes / t / 1e9, "hbm_frac": fb_bytes / t / 1e9 / PEAK_HBM_GBS,
+            "block_floor_bytes": fb_floor, "block_floor_hbm_frac": fb_floor / t / 1e9 / PEAK_HBM_GBS}
     totals = {"knn_graph": sum(tb), "mrconv": sum(tu), "graphleap_block": sum(tf)}
     dom = max(totals, key=totals.get)
     if dom == "knn_graph":
@@ -609,7 +729,11 @@ def main() -> int:
                     "peak": PEAK_HBM_GBS, "unit": "GB/s",
                     "frac": fb_bytes / t / 1e9 / PEAK_HBM_GBS,
                     "traffic": load_traffic("graphleap_block", args.workload),
-                    "per_launch": f"{fb_bytes:.4g} bytes (flop floor {fb_flops:.4g})"}
+                    "per_launch": f"{fb_bytes:.4g} bytes = one layer's algorithmic bytes (X read by "
+                                  f"the build and by the update, graph written and read, W, output); "
+                                  f"flop floor {fb_flops:.4g}",
+                    "block_floor": {"bytes": fb_floor, "frac": fb_floor / t / 1e9 / PEAK_HBM_GBS,
+                                    "note": "X read once by both roles of the one launch"}}
         else:
             roof = {"kernel": "graphleap_block", "bound": "mfma", "achieved": fb_flops / t / 1e12,
                     "peak": peak, "unit": "TFLOP/s", "frac": fb_flops / t / 1e12 / peak,
@@ -623,7 +747,7 @@ def main() -> int:
     # the whole layer against its roofline: F = Gram + FC flop, Y = the block's byte floor
     t_floor = max(fb_flops / (peak * 1e12), fb_bytes / (PEAK_HBM_GBS * 1e9))
     layer_roofline = {"layers_per_s": 1.0 / t_floor, "frac": value * t_floor,
-                      "flop_per_layer": fb_flops, "bytes_per_layer": fb_bytes}
+                      "flop_per_layer": fb_flops, "bytes_per_layer": layer_work(w, es)[1]}
     st = stage_transition(w, api, torch, x0, es)
     if st is not None:
         kernels["stage_transition"] = st
@@ -638,6 +762,18 @@ def main() -> int:
         log("full ViG block stack")
         full = full_block(args, w, api, I, dev, torch)
         log("full block", json.dumps(full))
+
+    configs = None
+    if not args.no_configs and args.workload == "vig_ti":
+        configs = {}
+        for name in CONFIG_SET:
+            log(f"config {name}")
+            configs[name] = measure_config(name, I.WORKLOADS[name], api, I, dev, torch,
+                                           steps=args.config_steps, warmup=max(2, args.config_steps // 5))
+            c = configs[name]
+            log(f"  {c['layers_per_s']:.0f} layers/s; dominant {c['dominant_kernel']['kernel']} "
+                f"{100 * c['dominant_kernel']['frac']:.2f}% of {c['dominant_kernel']['bound']}; "
+                f"Gram {100 * c['gram_mfma']['frac']:.2f}% MFMA; gather {c['gather_hbm']['gbs']:.0f} GB/s")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -657,7 +793,7 @@ def main() -> int:
                    "schedule": args.schedule},
         "roofline": roof, "cpu_baseline": cpu, "kernels": kernels, "schedules": schedules,
         "full_block": full, "per_stack": per_step, "overlap": overlap, "layer_roofline": layer_roofline,
-        "image_layers_per_s": value * w.B, "source_sha": kernel_source_sha(),
+        "image_layers_per_s": value * w.B, "configs": configs, "source_sha": kernel_source_sha(),
     }
     print(json.dumps(line), flush=True)
     la.close()

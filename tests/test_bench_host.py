@@ -43,3 +43,21 @@ def test_cpu_baseline_runs_the_oracle_in_worker_processes():
     assert r["kind"] == "oracle" and r["unit"] == "layers/s"
     assert r["value"] > 0 and r["cores"] == 1
     assert "single-thread processes" in r["sample"]
+
+
+def test_layer_work_matches_the_per_config_table():
+    """One layer's algorithmic flop and bytes (one build + one update) for the
+    five configurations: Gram 2BNMC + FC 4BNC^2 flop; bytes counted once each
+    (X by the build and by the update, pooled keys, the graph written and
+    read, W, the output, the pooling's own I/O)."""
+    from paper_2604_21290_amd import inputs as I
+    want = {  # name: (GFLOP, MB) as the per-config table prints them (3 digits)
+        "single": (0.044, 0.76), "vig_ti": (1.40, 7.8), "vig_b": (23.7, 50.7),
+        "pyr_s1": (5.72, 74.5), "pyr_s2": (4.14, 40.0), "hires": (16.0, 17.7),
+    }
+    for name, (gf, mb) in want.items():
+        w = I.WORKLOADS[name]
+        F, Y = bench.layer_work(w, 2 if w.dtype == I.BF16 else 4)
+        assert abs(F / 1e9 - gf) / gf < 1e-2, (name, F)
+        assert abs(Y / 1e6 - mb) / mb < 1e-2, (name, Y)
+    assert bench.layer_work(I.WORKLOADS["vig_ti"], 2)[1] == 7824384
