@@ -29,6 +29,8 @@ struct MrArgs {
   void* out;          // [B*N, Cout]
   int R, N, M, C, Cout, k;
   int heads;          // > 1: W is block-diagonal by heads (Cout == C); zero blocks are skipped
+  int col_tiles;      // > 0: each workgroup computes col_tiles 16-column output tiles of its
+                      // nodes (small grids: the output columns split over several workgroups)
 };
 
 struct GemmArgs {

@@ -26,6 +26,20 @@ __global__ __launch_bounds__(kMrThreads) __attribute__((amdgpu_waves_per_eu(3, 8
   mrconv_tile<DT, RT, KB>(smem, a, blk * 16 * RT);
 }
 
+// Small grids: workgroup blk computes output-column group blk % ncg (a.col_tiles
+// 16-column tiles) of node tile blk / ncg.  Few workgroups run, so the kernel is
+// not held to three waves per SIMD.
+template <int DT, int RT, int KB>
+__global__ __launch_bounds__(kMrThreads) void mrconv_cols_kernel(MrArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  const int nct = (a.Cout + 15) >> 4;
+  const int ncg = (nct + a.col_tiles - 1) / a.col_tiles;
+  const int blk = blockIdx.x, cg = blk % ncg;
+  const int tile0 = cg * a.col_tiles;
+  mrconv_tile<DT, RT, KB, false, false, true>(smem, a, (blk / ncg) * 16 * RT, tile0,
+                                              min(nct, tile0 + a.col_tiles));
+}
+
 // The multi-head update: the per-tile step tests need registers the
 // three-waves-per-SIMD budget does not leave, so this one is not held to it.
 template <int DT, int RT, int KB>
@@ -35,8 +49,16 @@ __global__ __launch_bounds__(kMrThreads) void mrconv_heads_kernel(MrArgs a) {
   mrconv_tile<DT, RT, KB, true>(smem, a, blk * 16 * RT);
 }
 
-template <int DT, int RT, bool HEADS = false>
+template <int DT, int RT, bool HEADS = false, bool COLS = false>
 const void* mrconv_fn_kb(int KB) {
+  if (COLS) {
+    switch (KB) {
+      case 9: return (const void*)&mrconv_cols_kernel<DT, RT, 9>;
+      case 16: return (const void*)&mrconv_cols_kernel<DT, RT, 16>;
+      case 32: return (const void*)&mrconv_cols_kernel<DT, RT, 32>;
+      default: return (const void*)&mrconv_cols_kernel<DT, RT, 64>;
+    }
+  }
   if (HEADS) {
     switch (KB) {
       case 9: return (const void*)&mrconv_heads_kernel<DT, RT, 9>;
@@ -133,9 +155,21 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
   }
   const int TM = 16 * rt;
   const size_t smem = mrconv_smem_bytes(C, k, dt_bf16, rt);
-  const dim3 grid((a.R + TM - 1) / TM), block(kMrThreads);
+  const int row_tiles = (a.R + TM - 1) / TM;
+  // A grid of a few node tiles (a single image) leaves most CUs idle while each
+  // workgroup streams all of W in batches; there the output columns are split
+  // into groups of four 16-column tiles (one per wave), each group its own
+  // workgroup (the gather is repeated per group, W is read once per group).
+  const int nct = (Cout + 15) >> 4;
+  a.col_tiles = 0;
+  if (a.heads <= 1 && row_tiles <= 64 && nct > 4) a.col_tiles = 4;
+  const int ncg = a.col_tiles ? (nct + a.col_tiles - 1) / a.col_tiles : 1;
+  const dim3 grid(row_tiles * ncg), block(kMrThreads);
   const void* fn;
-  if (a.heads > 1) {
+  if (a.col_tiles > 0) {
+    fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2, false, true>(KB) : mrconv_fn_kb<1, 1, false, true>(KB))
+                 : (rt == 2 ? mrconv_fn_kb<0, 2, false, true>(KB) : mrconv_fn_kb<0, 1, false, true>(KB));
+  } else if (a.heads > 1) {
     fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2, true>(KB) : mrconv_fn_kb<1, 1, true>(KB))
                  : (rt == 2 ? mrconv_fn_kb<0, 2, true>(KB) : mrconv_fn_kb<0, 1, true>(KB));
   } else {

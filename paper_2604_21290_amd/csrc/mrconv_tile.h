@@ -59,18 +59,29 @@ __device__ __forceinline__ bool mr_step_needed(const MrArgs& a, int n0, int s, i
   return (k0 < hi && k1 > lo) || (k0 < a.C + hi && k1 > a.C + lo);
 }
 
-template <int DT, bool HEADS>
-__device__ __forceinline__ void mr_load_w(uint4 (&bw)[kMrKU][4], const MrArgs& a, const char* Wb,
-                                          int w, int p, int s0, int K2, int Cout, int g, int t) {
+// COLS: only output tiles tile0 .. tile_end-1 (a column group of a small grid),
+// one tile per wave and pass, with the W operands of kMrKUCols k-steps per batch.
+constexpr int kMrKUCols = 12;
+template <bool COLS> struct MrBatch {
+  static constexpr int KU = COLS ? kMrKUCols : kMrKU;  // k-steps per batch of W operands
+  static constexpr int NC = COLS ? 1 : 4;              // output tiles per wave and pass
+};
+
+template <int DT, bool HEADS, bool COLS = false>
+__device__ __forceinline__ void mr_load_w(uint4 (&bw)[MrBatch<COLS>::KU][MrBatch<COLS>::NC],
+                                          const MrArgs& a, const char* Wb, int w, int p, int s0,
+                                          int K2, int Cout, int g, int t, int tile0 = 0,
+                                          int tile_end = 0) {
   constexpr int ES = DT ? 2 : 4;
   constexpr int KSTEP = DT ? 32 : 16;
+  constexpr int KU = MrBatch<COLS>::KU, NC = MrBatch<COLS>::NC;
 #pragma unroll
-  for (int c4 = 0; c4 < 4; ++c4) {
-    const int n0 = (w + 4 * (4 * p + c4)) * 16;
-    if (n0 >= Cout) continue;  // wave-uniform
+  for (int c4 = 0; c4 < NC; ++c4) {
+    const int n0 = ((COLS ? tile0 : 0) + w + 4 * (NC * p + c4)) * 16;
+    if (COLS ? n0 >= tile_end * 16 : n0 >= Cout) continue;  // wave-uniform
     const char* wrow = Wb + (size_t)min(n0 + t, Cout - 1) * K2 * ES;
 #pragma unroll
-    for (int u = 0; u < kMrKU; ++u) {
+    for (int u = 0; u < KU; ++u) {
       if (HEADS && !mr_step_needed(a, n0, s0 + u, KSTEP)) continue;  // wave-uniform
       const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
       bw[u][c4] = *reinterpret_cast<const uint4*>(wrow + (size_t)(kk < K2 ? kk : 0) * ES);
@@ -160,8 +171,11 @@ __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM
 // TM = 16*RT nodes starting at flattened node row0.  smem holds
 // mrconv_smem_bytes(C, k, RT) bytes.  Called by all 256 threads.
 // HEADS: the multi-head update (a.heads > 1), which skips the zero blocks of W.
-template <int DT, int RT, int KB, bool HEADS = false, bool T3 = false>
-__device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row0) {
+// COLS: only the 16-column output tiles tile0 .. tile_end-1 (tile_end within
+// the layer's tiles), the column group of a small grid.
+template <int DT, int RT, int KB, bool HEADS = false, bool T3 = false, bool COLS = false>
+__device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row0, int tile0 = 0,
+                                            int tile_end = 0) {
   constexpr int TM = 16 * RT;
   constexpr int ES = DT ? 2 : 4;
   const int C = a.C, k = a.k, M = a.M, R = a.R, Cout = a.Cout;
@@ -189,30 +203,34 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
   const char* Wb = static_cast<const char*>(a.W);
   // output tiles past Cout are never loaded: their operands stay zero (their
   // results are not stored either)
-  uint4 bw[kMrKU][4] = {};
-  if (w < NCT) mr_load_w<DT, HEADS>(bw, a, Wb, w, 0, 0, K2, Cout, g, t);
+  constexpr int KU = MrBatch<COLS>::KU, NC = MrBatch<COLS>::NC;
+  uint4 bw[KU][NC] = {};
+  const int T0 = COLS ? tile0 : 0, TE = COLS ? tile_end : NCT;
+  if (T0 + w < TE) mr_load_w<DT, HEADS, COLS>(bw, a, Wb, w, 0, 0, K2, Cout, g, t, tile0, tile_end);
   __syncthreads();
 
   mr_gather_rows<DT, KB, T3>(a, row0, TM, sIdx, sA, lds_row);
   __syncthreads();
 
   // -- FC on MFMA -----------------------------------------------------------------
-  for (int p = 0; w + 16 * p < NCT; ++p) {
-    f32x4 acc[RT][4];
+  for (int p = 0; T0 + w + 4 * NC * p < TE; ++p) {
+    f32x4 acc[RT][NC];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int c4 = 0; c4 < 4; ++c4) acc[rt][c4] = f32x4{0.f, 0.f, 0.f, 0.f};
-    bool nvalid[4];
+      for (int c4 = 0; c4 < NC; ++c4) acc[rt][c4] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bool nvalid[NC];
 #pragma unroll
-    for (int c4 = 0; c4 < 4; ++c4) nvalid[c4] = (w + 4 * (4 * p + c4)) * 16 < Cout;
-    for (int s0 = 0; s0 < ksteps; s0 += kMrKU) {
-      if (p != 0 || s0 != 0) mr_load_w<DT, HEADS>(bw, a, Wb, w, p, s0, K2, Cout, g, t);
-      bool kin[kMrKU];
+    for (int c4 = 0; c4 < NC; ++c4)
+      nvalid[c4] = COLS ? T0 + w + 4 * (NC * p + c4) < TE : (w + 4 * (NC * p + c4)) * 16 < Cout;
+    for (int s0 = 0; s0 < ksteps; s0 += KU) {
+      if (p != 0 || s0 != 0)
+        mr_load_w<DT, HEADS, COLS>(bw, a, Wb, w, p, s0, K2, Cout, g, t, tile0, tile_end);
+      bool kin[KU];
 #pragma unroll
-      for (int u = 0; u < kMrKU; ++u) kin[u] = (s0 + u) * KSTEP + g * (KSTEP / 4) < K2;
+      for (int u = 0; u < KU; ++u) kin[u] = (s0 + u) * KSTEP + g * (KSTEP / 4) < K2;
 #pragma unroll
-      for (int u = 0; u < kMrKU; ++u) {
+      for (int u = 0; u < KU; ++u) {
         const int kk = (s0 + u) * KSTEP + g * (KSTEP / 4);
         uint4 af[RT];
 #pragma unroll
@@ -220,8 +238,8 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
           af[rt] = kin[u] ? *reinterpret_cast<const uint4*>(sA + (rt * 16 + t) * lds_row + kk * ES)
                           : make_uint4(0, 0, 0, 0);
 #pragma unroll
-        for (int c4 = 0; c4 < 4; ++c4) {
-          if (HEADS && !mr_step_needed(a, (w + 4 * (4 * p + c4)) * 16, s0 + u, KSTEP)) continue;
+        for (int c4 = 0; c4 < NC; ++c4) {
+          if (HEADS && !mr_step_needed(a, (w + 4 * (NC * p + c4)) * 16, s0 + u, KSTEP)) continue;
           // past 2C the A operand is zero and bv a real W element (column 0)
           const uint4 bv = bw[u][c4];
 #pragma unroll
@@ -245,9 +263,9 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
     // stores without per-lane guards
     const bool full = row0 + TM <= R && (Cout & 15) == 0;
 #pragma unroll
-    for (int c4 = 0; c4 < 4; ++c4) {
+    for (int c4 = 0; c4 < NC; ++c4) {
       if (!nvalid[c4]) continue;  // wave-uniform
-      const int n = (w + 4 * (4 * p + c4)) * 16 + t;
+      const int n = (T0 + w + 4 * (NC * p + c4)) * 16 + t;
       const int nc = min(n, Cout - 1);
       float bn = 0.f;
       if (a.bias) {

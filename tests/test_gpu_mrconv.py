@@ -59,6 +59,11 @@ EDGE = [
     ("fp32_vig", 1, 196, None, 192, 192, 9, I.F32, False),
     ("k_max_64", 1, 70, None, 16, 16, 64, I.BF16, True),
     ("wide_C_1024", 1, 40, None, 1024, 64, 9, I.BF16, True),
+    # small grids: output columns split over workgroups (groups of 4 tiles, a
+    # partial last group, ragged node tiles, fp32)
+    ("cols_ragged_bf16", 2, 45, None, 64, 120, 7, I.BF16, True),
+    ("cols_ragged_fp32", 1, 77, None, 48, 200, 9, I.F32, True),
+    ("cols_pooled", 1, 100, 25, 96, 96, 9, I.BF16, False),
     # two-pass form (gather to [x | m], then the tiled GEMM): ragged node and
     # output tiles, a half contraction step at the end, fp32, pooled keys, k > 16
     ("split_ragged_R_Cout", 3, 70, None, 512, 300, 9, I.BF16, True),
