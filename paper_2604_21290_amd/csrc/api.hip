@@ -131,7 +131,7 @@ gl_status check_mrconv(const void* x, int B, int N, int C, const void* keys, int
 // the fused tile).
 size_t mrconv_ws_need(int B, int N, int C, int k, int Cout, gl_dtype dt, int rt) {
   const int dtb = dt == GL_BF16;
-  return gl::mrconv_use_split(C, Cout, dtb, rt) ? gl::mrconv_split_ws_bytes(B * N, C, dtb) : 0;
+  return gl::mrconv_use_split(C, Cout, dtb, rt, B * N) ? gl::mrconv_split_ws_bytes(B * N, C, dtb) : 0;
 }
 
 // A caller workspace of `need` bytes: present, large enough, 16-byte aligned,

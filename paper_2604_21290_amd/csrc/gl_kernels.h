@@ -103,7 +103,8 @@ hipError_t launch_mrconv(const void* x, const void* keys, const int32_t* idx, co
 hipError_t launch_mrconv_args(const MrArgs& a, int dt_bf16, int rt, void* split_ws,
                               hipStream_t stream, hipEvent_t ev0 = nullptr,
                               hipEvent_t ev1 = nullptr);
-bool mrconv_use_split(int C, int Cout, int dt_bf16, int rt);
+bool mrconv_use_split(int C, int Cout, int dt_bf16, int rt, int R);
+int mrconv_col_tiles(int R, int Cout, int rt);
 size_t mrconv_split_ws_bytes(int R, int C, int dt_bf16);
 size_t gemm_smem_bytes();
 hipError_t launch_gemm_nt(const GemmArgs& a, int dt_bf16, hipStream_t stream, hipEvent_t ev0,

@@ -104,12 +104,22 @@ const void* gather_fn_kb(int KB) {
   }
 }
 
-// The fused tile streams all of W through every workgroup of 16*rt nodes;
-// beyond 8 KB of W per node (or when the tile does not fit LDS) the two-pass
-// form, which reads W once per 64 or 128 nodes, is used.
-bool mrconv_use_split(int C, int Cout, int dt_bf16, int rt) {
+// Column groups of a small grid: a layer of at most 64 node tiles with more than
+// four 16-column output tiles runs one workgroup per (node tile, group of four
+// output tiles); 0 = no split.
+int mrconv_col_tiles(int R, int Cout, int rt) {
+  const int row_tiles = (R + 16 * rt - 1) / (16 * rt);
+  return row_tiles <= 64 && (Cout + 15) / 16 > 4 ? 4 : 0;
+}
+
+// The fused tile streams all of W (of its column group) through every workgroup
+// of 16*rt nodes; beyond 8 KB of W per node (or when the tile does not fit LDS)
+// the two-pass form, which reads W once per 64 or 128 nodes, is used.
+bool mrconv_use_split(int C, int Cout, int dt_bf16, int rt, int R) {
   if (rt < 1) return true;
-  const size_t wbytes = (size_t)Cout * 2 * C * (dt_bf16 ? 2 : 4);
+  const int ct = mrconv_col_tiles(R, Cout, rt);
+  const int cols = ct ? (16 * ct < Cout ? 16 * ct : Cout) : Cout;
+  const size_t wbytes = (size_t)cols * 2 * C * (dt_bf16 ? 2 : 4);
   return wbytes / (size_t)(16 * rt) > 8192;
 }
 
@@ -133,7 +143,7 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
   const void* bias = a.bias;
   void* out = a.out;
   const int KB = mrconv_k_bucket(k);
-  if (mrconv_use_split(C, Cout, dt_bf16, rt)) {
+  if (mrconv_use_split(C, Cout, dt_bf16, rt, a.R)) {
     if (!split_ws) return hipErrorInvalidValue;
     const dim3 g1((a.R + kMrGatherRows - 1) / kMrGatherRows), blk(kMrThreads);
     const void* fg = dt_bf16 ? gather_fn_kb<1>(KB) : gather_fn_kb<0>(KB);
@@ -161,8 +171,7 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
   // into groups of four 16-column tiles (one per wave), each group its own
   // workgroup (the gather is repeated per group, W is read once per group).
   const int nct = (Cout + 15) >> 4;
-  a.col_tiles = 0;
-  if (a.heads <= 1 && row_tiles <= 64 && nct > 4) a.col_tiles = 4;
+  a.col_tiles = a.heads <= 1 ? mrconv_col_tiles(a.R, Cout, rt) : 0;
   const int ncg = a.col_tiles ? (nct + a.col_tiles - 1) / a.col_tiles : 1;
   const dim3 grid(row_tiles * ncg), block(kMrThreads);
   const void* fn;

@@ -52,7 +52,7 @@ def test_noalloc_two_pass_then_smaller():
     # ViG-B-shaped layer (C = Cout = 640: the two-pass form, 2.5 MB of scratch),
     # then a smaller one with pooled keys and a ragged node count
     _run("two-pass 8x196x640", *_case(g, 8, 196, 640, 640, 9))
-    _run("two-pass smaller 3x77x512 pooled", *_case(g, 3, 77, 512, 512, 7, M=49))
+    _run("two-pass smaller 3x400x512 pooled", *_case(g, 3, 400, 512, 512, 7, M=49))
 
 
 def test_noalloc_full_scratch_then_fused():
