@@ -250,28 +250,31 @@ def graph_replay(args, w, api, torch, x0, Wd, bd, dil, ws, out):
 
 
 def heads_update(args, w, api, torch, x0, idx, Wdense, H=16) -> dict | None:
-    """The multi-head MRConv update (gl_mrconv_heads, H heads, block-diagonal
-    W) against the dense update with the same W, averaged over launches."""
+    """The multi-head MRConv update (gl_mrconv_heads: H heads, per-head weights
+    Wh [H, hd, 2hd]) against the dense update (gl_mrconv, [C, 2C]) of the same
+    layer, each averaged over launches timed with HIP events."""
     if w.C % H or w.pool_r > 1:
         return None
     hd = w.C // H
-    Wb = torch.zeros_like(Wdense)
-    for h in range(H):
-        Wb[h * hd:(h + 1) * hd, h * hd:(h + 1) * hd] = Wdense[h * hd:(h + 1) * hd, h * hd:(h + 1) * hd]
-        Wb[h * hd:(h + 1) * hd, w.C + h * hd:w.C + (h + 1) * hd] = \
-            Wdense[h * hd:(h + 1) * hd, w.C + h * hd:w.C + (h + 1) * hd]
+    Wh = torch.stack([torch.cat([Wdense[h * hd:(h + 1) * hd, h * hd:(h + 1) * hd],
+                                 Wdense[h * hd:(h + 1) * hd, w.C + h * hd:w.C + (h + 1) * hd]], 1)
+                      for h in range(H)]).contiguous()
     out = torch.empty_like(x0)
     mws = api.mrconv_workspace(w.B, w.N, w.C, w.k, w.C, x0.dtype, x0.device)
-    res = {"heads": H}
+    hws = api.mrconv_heads_workspace(w.B, w.N, w.C, w.k, H, x0.dtype, x0.device)
+    res = {"heads": H, "hd": hd, "weights_bytes": {"dense": Wdense.numel() * Wdense.element_size(),
+                                                   "heads": Wh.numel() * Wh.element_size()}}
     n = max(20, args.steps // 4)
-    for name, hh in (("dense_us", 1), ("heads_us", H)):
+    calls = (("dense_us", lambda: api.mrconv(x0, idx, Wdense, out=out, ws=mws)),
+             ("heads_us", lambda: api.mrconv_heads(x0, idx, Wh, out=out, ws=hws)))
+    for name, fn in calls:
         for _ in range(3):
-            api.mrconv(x0, idx, Wb, out=out, heads=hh, ws=mws)
+            fn()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record()
         for _ in range(n):
-            api.mrconv(x0, idx, Wb, out=out, heads=hh, ws=mws)
+            fn()
         e1.record()
         torch.cuda.synchronize()
         res[name] = e0.elapsed_time(e1) / n * 1e3

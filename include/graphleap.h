@@ -193,18 +193,24 @@ gl_status gl_mrconv_noalloc(const void* x, int B, int N, int C, const void* keys
  * W_x,h / W_m,h of Sec. IV-C2): channels split into `heads` equal contiguous
  * heads of hd = C / heads, and output head h sees only head h's channels of
  * x_i and of m_i:
- *   out[b,i,h*hd + o] = sum_{c<hd} x[b,i,h*hd+c] W[h*hd+o, h*hd+c]
- *                     + sum_{c<hd} m[b,i,h*hd+c] W[h*hd+o, C+h*hd+c] + bias[h*hd+o]
- * W is the dense [C, 2C] = [W_x | W_m] of gl_mrconv and MUST hold zeros
- * outside the heads' diagonal blocks of each half.  The kernel skips the
- * contraction steps a 16-column output tile does not need, but steps that
- * straddle a block edge do multiply the zeros.  Cout == C.  Everything else
- * is as gl_mrconv (workspace: gl_mrconv_workspace_bytes with Cout = C);
- * heads == 1 is gl_mrconv.
+ *   out[b,i,h*hd + o] = sum_{c<hd} x[b,i,h*hd+c] Wh[h,o,c]
+ *                     + sum_{c<hd} m[b,i,h*hd+c] Wh[h,o,hd+c] + bias[h*hd+o]
+ * Wh: [heads, hd, 2*hd] row-major in dt, head h's [W_x,h | W_m,h]; only the
+ * heads' own weights are stored and read.  Cout == C.
+ * hd a multiple of 4, at most 256 (bf16) / 128 (fp32), and the fused tile
+ * fits LDS: the per-head kernel contracts each head's 2*hd channels on MFMA
+ * (fp32 accumulation, one rounding) and needs no workspace.  Other head
+ * widths: Wh is expanded into the dense block-diagonal [C, 2C] in the
+ * workspace and the dense update runs on it.  heads == 1 is gl_mrconv with
+ * W = Wh[0].
+ * workspace: gl_mrconv_heads_workspace_bytes(B, N, C, k, heads, dt) bytes
+ * (0: none needed), 16-byte aligned, disjoint from every other argument.
+ * Everything else is as gl_mrconv.
  * Limits: heads >= 1, C % heads == 0.
  * -------------------------------------------------------------------------*/
+size_t gl_mrconv_heads_workspace_bytes(int B, int N, int C, int k, int heads, gl_dtype dt);
 gl_status gl_mrconv_heads(const void* x, int B, int N, int C, const void* keys, int M,
-                          const int32_t* idx, int k, const void* W, const void* bias, int heads,
+                          const int32_t* idx, int k, const void* Wh, const void* bias, int heads,
                           gl_dtype dt, void* out, void* workspace, size_t workspace_bytes,
                           hipStream_t stream);
 

@@ -46,6 +46,7 @@ SIGNATURES = {
     "gl_mrconv": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _sz, _vp],
     "gl_mrconv_noalloc": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp],
     "gl_mrconv_heads": [_vp, _i, _i, _i, _vp, _i, _vp, _i, _vp, _vp, _i, _i, _vp, _vp, _sz, _vp],
+    "gl_mrconv_heads_workspace_bytes": [_i, _i, _i, _i, _i, _i],
     "gl_lookahead_create": [_vp, _vp, ctypes.POINTER(_vp)],
     "gl_lookahead_destroy": [_vp],
     "gl_lookahead_set_profiling": [_vp, _i],
@@ -68,6 +69,7 @@ SIGNATURES = {
 }
 RESTYPES = {"gl_status_string": ctypes.c_char_p, "gl_last_error": ctypes.c_char_p,
             "gl_vig_workspace_bytes": ctypes.c_size_t, "gl_mrconv_workspace_bytes": ctypes.c_size_t,
+            "gl_mrconv_heads_workspace_bytes": ctypes.c_size_t,
             "gl_graphleap_workspace_bytes": ctypes.c_size_t}
 
 _lib = None
@@ -181,9 +183,8 @@ def mrconv_workspace(B: int, N: int, C: int, k: int, Cout: int, dtype, device) -
 
 def mrconv(x: torch.Tensor, idx: torch.Tensor, W: torch.Tensor, bias: torch.Tensor | None = None,
            keys: torch.Tensor | None = None, out: torch.Tensor | None = None,
-           stream=None, heads: int = 1, ws: Workspace | None = None) -> torch.Tensor:
-    """out[B, N, Cout] = [x_i, max_j (keys_j - x_i)] W^T + bias.  heads > 1: the
-    multi-head update (W block-diagonal by heads in each half, Cout == C).
+           stream=None, ws: Workspace | None = None) -> torch.Tensor:
+    """out[B, N, Cout] = [x_i, max_j (keys_j - x_i)] W^T + bias (gl_mrconv).
     ws: the call's workspace (allocated here when not given)."""
     B, N, C = x.shape
     M = N if keys is None else keys.shape[1]
@@ -193,12 +194,35 @@ def mrconv(x: torch.Tensor, idx: torch.Tensor, W: torch.Tensor, bias: torch.Tens
         out = torch.empty((B, N, Cout), dtype=x.dtype, device=x.device)
     if ws is None:
         ws = mrconv_workspace(B, N, C, k, Cout, x.dtype, x.device)
-    if heads != 1:
-        _call("gl_mrconv_heads", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(W), _p(bias), heads,
-              _dt(x), _p(out), _p(ws), ws.nbytes, _s(stream))
-    else:
-        _call("gl_mrconv", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(W), _p(bias), Cout, _dt(x),
-              _p(out), _p(ws), ws.nbytes, _s(stream))
+    _call("gl_mrconv", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(W), _p(bias), Cout, _dt(x),
+          _p(out), _p(ws), ws.nbytes, _s(stream))
+    return out
+
+
+def mrconv_heads_workspace(B: int, N: int, C: int, k: int, heads: int, dtype, device) -> Workspace:
+    """Workspace of gl_mrconv_heads for this layer (empty for the grouped kernel)."""
+    dt = GL_BF16 if dtype == torch.bfloat16 else GL_F32
+    return Workspace(lib().gl_mrconv_heads_workspace_bytes(B, N, C, k, heads, dt), device)
+
+
+def mrconv_heads(x: torch.Tensor, idx: torch.Tensor, Wh: torch.Tensor,
+                 bias: torch.Tensor | None = None, keys: torch.Tensor | None = None,
+                 out: torch.Tensor | None = None, stream=None,
+                 ws: Workspace | None = None) -> torch.Tensor:
+    """The multi-head update (gl_mrconv_heads): Wh [H, hd, 2hd] holds each head's
+    [W_x,h | W_m,h]; out[B, N, C] with C = H * hd."""
+    B, N, C = x.shape
+    H, hd, two_hd = Wh.shape
+    if H * hd != C or two_hd != 2 * hd:
+        raise ValueError(f"mrconv_heads: Wh {tuple(Wh.shape)} does not match C={C}")
+    M = N if keys is None else keys.shape[1]
+    k = idx.shape[2]
+    if out is None:
+        out = torch.empty((B, N, C), dtype=x.dtype, device=x.device)
+    if ws is None:
+        ws = mrconv_heads_workspace(B, N, C, k, H, x.dtype, x.device)
+    _call("gl_mrconv_heads", _p(x), B, N, C, _p(keys), M, _p(idx), k, _p(Wh), _p(bias), H,
+          _dt(x), _p(out), _p(ws), ws.nbytes, _s(stream))
     return out
 
 

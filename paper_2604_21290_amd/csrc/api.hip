@@ -98,7 +98,7 @@ int mrconv_rt(int C, int k, gl_dtype dt) {
 
 gl_status check_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
                        const int32_t* idx, int k, const void* W, const void* bias, int Cout,
-                       gl_dtype dt, const void* out, int* rt_out) {
+                       gl_dtype dt, const void* out, int* rt_out, size_t w_bytes = 0) {
   if (!x || !idx || !W || !out) return fail(GL_ERR_NULL_PTR, "mrconv: x, idx, W and out are required");
   if (!dtype_ok(dt)) return fail(GL_ERR_UNSUPPORTED, "mrconv: unknown dtype %d", (int)dt);
   if (B < 1 || N < 1 || C < 1 || Cout < 1 || !size_ok(B, N, C) || !size_ok(B, N, Cout))
@@ -118,9 +118,10 @@ gl_status check_mrconv(const void* x, int B, int N, int C, const void* keys, int
     return fail(GL_ERR_ALIGNMENT, "mrconv: x/keys/W/out need 16-byte alignment");
   const size_t es = esize(dt);
   const size_t ob = (size_t)B * N * Cout * es;
+  if (!w_bytes) w_bytes = (size_t)Cout * 2 * C * es;
   if (overlap(out, ob, x, (size_t)B * N * C * es) ||
       overlap(out, ob, keys, keys ? (size_t)B * M * C * es : 0) ||
-      overlap(out, ob, idx, (size_t)B * N * k * 4) || overlap(out, ob, W, (size_t)Cout * 2 * C * es) ||
+      overlap(out, ob, idx, (size_t)B * N * k * 4) || overlap(out, ob, W, w_bytes) ||
       overlap(out, ob, bias, bias ? (size_t)Cout * es : 0))
     return fail(GL_ERR_ALIAS, "mrconv: out overlaps an input");
   if (rt_out) *rt_out = rt;
@@ -357,6 +358,28 @@ gl_status gl_max_pool_nodes(const void* x, int B, int H, int W, int C, int r, gl
   return e == hipSuccess ? GL_OK : hip_fail(e, "max pool launch");
 }
 
+namespace {
+
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// Workspace of gl_mrconv_heads: none for the per-head kernel; else the dense
+// block-diagonal W expanded from Wh (then the two-pass rows when the fused
+// tile does not fit LDS).
+size_t heads_ws_need(int B, int N, int C, int k, int heads, gl_dtype dt, int rt) {
+  if (heads == 1) return mrconv_ws_need(B, N, C, k, C, dt, rt);  // Wh is the dense W
+  if (rt > 0 && gl::mrconv_headw_steps(C / heads, dt == GL_BF16)) return 0;
+  return align256((size_t)C * 2 * C * esize(dt)) + (rt > 0 ? 0 : mrconv_ws_need(B, N, C, k, C, dt, rt));
+}
+
+}  // namespace
+
+size_t gl_mrconv_heads_workspace_bytes(int B, int N, int C, int k, int heads, gl_dtype dt) {
+  if (B < 1 || N < 1 || C < 1 || k < 1 || k > GL_MAX_K || !dtype_ok(dt) || !size_ok(B, N, C) ||
+      heads < 1 || C % heads)
+    return 0;
+  return heads_ws_need(B, N, C, k, heads, dt, mrconv_rt(C, k, dt));
+}
+
 size_t gl_mrconv_workspace_bytes(int B, int N, int C, int k, int Cout, gl_dtype dt) {
   if (B < 1 || N < 1 || C < 1 || Cout < 1 || k < 1 || k > GL_MAX_K || !dtype_ok(dt) ||
       !size_ok(B, N, C))
@@ -396,19 +419,46 @@ gl_status gl_mrconv(const void* x, int B, int N, int C, const void* keys, int M,
 }
 
 gl_status gl_mrconv_heads(const void* x, int B, int N, int C, const void* keys, int M,
-                          const int32_t* idx, int k, const void* W, const void* bias, int heads,
+                          const int32_t* idx, int k, const void* Wh, const void* bias, int heads,
                           gl_dtype dt, void* out, void* workspace, size_t workspace_bytes,
                           hipStream_t stream) {
-  int rt = 0;
-  gl_status s = check_mrconv_call("mrconv_heads", x, B, N, C, keys, M, idx, k, W, bias, C, dt, out,
-                                  workspace, workspace_bytes, &rt);
-  if (s != GL_OK) return s;
-  if (heads < 1 || C % heads)
+  if (heads < 1 || C < 1 || C % heads)
     return fail(GL_ERR_BAD_SHAPE, "mrconv_heads: heads=%d must divide C=%d", heads, C);
-  gl::MrArgs a = gl::make_mr_args(x, keys ? keys : x, idx, W, bias, out, B, N, M, C, C, k);
+  const int hd = C / heads;
+  const size_t es = esize(dt);
+  const size_t whb = (size_t)C * 2 * hd * es;
+  int rt = 0;
+  gl_status s = check_mrconv(x, B, N, C, keys, M, idx, k, Wh, bias, C, dt, out, &rt, whb);
+  if (s != GL_OK) return s;
+  s = check_ws("mrconv_heads", heads_ws_need(B, N, C, k, heads, dt, rt), workspace,
+               workspace_bytes,
+               {{x, (size_t)B * N * C * es}, {keys, keys ? (size_t)B * M * C * es : 0},
+                {idx, (size_t)B * N * k * 4}, {Wh, whb}, {bias, bias ? (size_t)C * es : 0},
+                {out, (size_t)B * N * C * es}});
+  if (s != GL_OK) return s;
+  const int dtb = dt == GL_BF16;
+  gl::MrArgs a = gl::make_mr_args(x, keys ? keys : x, idx, Wh, bias, out, B, N, M, C, C, k);
   a.heads = heads;
-  hipError_t e = gl::launch_mrconv_args(a, dt == GL_BF16, rt, workspace, stream);
-  return e == hipSuccess ? GL_OK : hip_fail(e, "mrconv launch");
+  hipError_t e;
+  if (heads == 1) {
+    // one head: Wh [1, C, 2C] is the dense [W_x | W_m]
+    a.heads = 1;
+    e = gl::launch_mrconv_args(a, dtb, rt, workspace, stream);
+  } else if (rt > 0 && gl::mrconv_headw_steps(hd, dtb)) {
+    e = gl::launch_mrconv_headw(a, dtb, rt, stream);
+  } else {
+    // expand Wh into the dense block-diagonal [C, 2C] in the workspace; the
+    // fused multi-head tile skips its all-zero steps, the two-pass form (the
+    // tile does not fit LDS) runs the dense product
+    char* wd = static_cast<char*>(workspace);
+    e = gl::launch_expand_heads(Wh, wd, C, heads, dtb, stream);
+    if (e == hipSuccess) {
+      a.W = wd;
+      if (rt < 1) a.heads = 1;
+      e = gl::launch_mrconv_args(a, dtb, rt, wd + align256((size_t)C * 2 * C * es), stream);
+    }
+  }
+  return e == hipSuccess ? GL_OK : hip_fail(e, "mrconv_heads launch");
 }
 
 gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_lookahead_t* out) {

@@ -106,6 +106,13 @@ hipError_t launch_mrconv_args(const MrArgs& a, int dt_bf16, int rt, void* split_
 bool mrconv_use_split(int C, int Cout, int dt_bf16, int rt, int R);
 int mrconv_col_tiles(int R, int Cout, int rt);
 size_t mrconv_split_ws_bytes(int R, int C, int dt_bf16);
+// Multi-head update with per-head weights Wh [H, hd, 2hd] on MFMA (hd a
+// multiple of 4; mrconv_headw_steps > 0), or the dense block-diagonal W
+// expanded from Wh (launch_expand_heads) for the others.
+int mrconv_headw_steps(int hd, int dt_bf16);
+hipError_t launch_mrconv_headw(const MrArgs& a, int dt_bf16, int rt, hipStream_t stream);
+hipError_t launch_expand_heads(const void* Wh, void* Wd, int C, int heads, int dt_bf16,
+                               hipStream_t stream);
 size_t gemm_smem_bytes();
 hipError_t launch_gemm_nt(const GemmArgs& a, int dt_bf16, hipStream_t stream, hipEvent_t ev0,
                           hipEvent_t ev1);

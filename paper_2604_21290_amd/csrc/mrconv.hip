@@ -143,7 +143,9 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
   const void* bias = a.bias;
   void* out = a.out;
   const int KB = mrconv_k_bucket(k);
-  if (mrconv_use_split(C, Cout, dt_bf16, rt, a.R)) {
+  // the multi-head update (W = per-head Wh) always takes the fused tile
+  if (a.heads > 1 && rt < 1) return hipErrorInvalidValue;
+  if (a.heads <= 1 && mrconv_use_split(C, Cout, dt_bf16, rt, a.R)) {
     if (!split_ws) return hipErrorInvalidValue;
     const dim3 g1((a.R + kMrGatherRows - 1) / kMrGatherRows), blk(kMrThreads);
     const void* fg = dt_bf16 ? gather_fn_kb<1>(KB) : gather_fn_kb<0>(KB);
@@ -186,6 +188,214 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
                  : (rt == 2 ? mrconv_fn_kb<0, 2>(KB) : mrconv_fn_kb<0, 1>(KB));
   }
   return launch_with_smem(fn, grid, block, smem, stream, ev0, ev1, a);
+}
+
+// ---------------------------------------------------------------------------
+// Multi-head update with per-head weights (Sec. II-A; the per-head W_x,h and
+// W_m,h of Sec. IV-C2): output channel o of head h = o / hd only meets head
+// h's hd channels of x_i and of m_i.  Per workgroup (TM nodes):
+//   1. the gather of the fused tile writes [x_i | m_i] rows into LDS;
+//   2. the FC runs per head on MFMA: a unit is (head h, 16-column tile c of
+//      the head's outputs); its contraction covers only head h's channels,
+//      ceil(hd / KSTEP) steps in the x half and as many in the m half.  A and
+//      B operands past the head's last channel are zero, so nothing of the
+//      neighbouring heads enters.  B comes straight from Wh [H, hd, 2hd]: row
+//      o of Wh viewed as [C, 2hd] is output o's [W_x,h | W_m,h] row, so a
+//      lane's 8 (bf16) or 4 (fp32) k-values are contiguous.
+//   Units are dealt to the 4 waves round-robin; the B operands of a wave's
+//   next unit are requested while the current one finishes, the first ones
+//   ahead of the gather.
+// hd must be a multiple of 4 (operand loads of 4 channels never straddle a
+// head) and at most KSH * KSTEP.
+// ---------------------------------------------------------------------------
+// B operand: Wh row o, k-values kl .. kl+KV-1 of half `half` (zero past hd,
+// and for a column past the head's last output).
+template <int DT>
+__device__ __forceinline__ uint4 mr_wh_operand(const char* Wh, int o, bool ov, int hd, int half,
+                                               int kl) {
+  if (DT) {
+    const char* p = Wh + ((size_t)o * 2 * hd + half * hd + kl) * 2;
+    const uint2 lo = (ov && kl < hd) ? *reinterpret_cast<const uint2*>(p) : make_uint2(0, 0);
+    const uint2 hi = (ov && kl + 4 < hd) ? *reinterpret_cast<const uint2*>(p + 8) : make_uint2(0, 0);
+    return make_uint4(lo.x, lo.y, hi.x, hi.y);
+  } else {
+    const char* p = Wh + ((size_t)o * 2 * hd + half * hd + kl) * 4;
+    return (ov && kl < hd) ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
+  }
+}
+
+// A operand from the LDS row: channels kl .. kl+KV-1 of head h in half `half`
+// (zero past hd).
+template <int DT>
+__device__ __forceinline__ uint4 mr_head_a_operand(const char* rowp, int C, int h, int hd, int half,
+                                                   int kl) {
+  if (DT) {
+    const char* p = rowp + (size_t)(half * C + h * hd + kl) * 2;
+    const uint2 lo = kl < hd ? *reinterpret_cast<const uint2*>(p) : make_uint2(0, 0);
+    const uint2 hi = kl + 4 < hd ? *reinterpret_cast<const uint2*>(p + 8) : make_uint2(0, 0);
+    return make_uint4(lo.x, lo.y, hi.x, hi.y);
+  } else {
+    const char* p = rowp + (size_t)(half * C + h * hd + kl) * 4;
+    return kl < hd ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
+  }
+}
+
+template <int DT, int RT, int KB, int KSH>
+__global__ __launch_bounds__(kMrThreads) void mrconv_headw_kernel(MrArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  constexpr int TM = 16 * RT;
+  constexpr int ES = DT ? 2 : 4;
+  constexpr int KSTEP = DT ? 32 : 16;
+  constexpr int KV = KSTEP / 4;  // k-values per lane and step
+  const int C = a.C, k = a.k, M = a.M, R = a.R, H = a.heads, hd = C / H;
+  const int lds_row = 2 * C * ES + 16;
+  char* sA = smem;
+  int32_t* sIdx = reinterpret_cast<int32_t*>(smem + TM * lds_row);
+  const int row0 = xcd_remap(blockIdx.x, gridDim.x) * TM;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int g = lane >> 4, t = lane & 15;
+
+  for (int e = tid; e < TM * k; e += kMrThreads) {
+    const int r = e / k, tt = e - r * k, row = row0 + r;
+    const int j = row < R ? a.idx[(size_t)row * k + tt] : 0;
+    sIdx[e] = min(max(j, 0), M - 1) * (C * ES / 16);
+  }
+
+  const int nch = (hd + 15) >> 4;  // 16-column tiles per head
+  const int U = H * nch;           // units
+  const char* Wh = static_cast<const char*>(a.W);
+  uint4 bw[2][KSH];
+  auto load_b = [&](int u) {
+    const int h = u / nch, ol = (u - h * nch) * 16 + t;
+    const int o = h * hd + min(ol, hd - 1);
+#pragma unroll
+    for (int half = 0; half < 2; ++half)
+#pragma unroll
+      for (int s = 0; s < KSH; ++s)
+        bw[half][s] = mr_wh_operand<DT>(Wh, o, ol < hd, hd, half, s * KSTEP + g * KV);
+  };
+  if (w < U) load_b(w);
+  __syncthreads();
+  mr_gather_rows<DT, KB>(a, row0, TM, sIdx, sA, lds_row);
+  __syncthreads();
+
+  for (int u = w; u < U; u += 4) {
+    const int h = u / nch, ol = (u - h * nch) * 16 + t;
+    f32x4 acc[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int half = 0; half < 2; ++half)
+#pragma unroll
+      for (int s = 0; s < KSH; ++s) {
+        if (s * KSTEP >= hd) continue;  // uniform
+        const int kl = s * KSTEP + g * KV;
+        const uint4 bv = bw[half][s];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          const uint4 av =
+              mr_head_a_operand<DT>(sA + (size_t)(rt * 16 + t) * lds_row, C, h, hd, half, kl);
+          if (DT) {
+            acc[rt] = mfma_bf16(av, bv, acc[rt]);
+          } else {
+            const float4 x4 = __builtin_bit_cast(float4, av);
+            const float4 w4 = __builtin_bit_cast(float4, bv);
+            acc[rt] = mfma_f32(x4.x, w4.x, acc[rt]);
+            acc[rt] = mfma_f32(x4.y, w4.y, acc[rt]);
+            acc[rt] = mfma_f32(x4.z, w4.z, acc[rt]);
+            acc[rt] = mfma_f32(x4.w, w4.w, acc[rt]);
+          }
+        }
+      }
+    if (u + 4 < U) load_b(u + 4);
+    // epilogue: + bias, round once, store (columns past the head are not)
+    if (ol < hd) {
+      const int o = h * hd + ol;
+      float bn = 0.f;
+      if (a.bias) {
+        bn = DT ? bf16_bits_to_f32(static_cast<const uint16_t*>(a.bias)[o])
+                : static_cast<const float*>(a.bias)[o];
+      }
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = row0 + rt * 16 + 4 * g + v;
+          if (row >= R) continue;
+          const size_t off = (size_t)row * C + o;
+          const float y = acc[rt][v] + bn;
+          if (DT) static_cast<uint16_t*>(a.out)[off] = (uint16_t)f32_to_bf16_bits(y);
+          else static_cast<float*>(a.out)[off] = y;
+        }
+    }
+  }
+}
+
+// k-steps per half the per-head kernel is compiled for (0: hd is not a
+// multiple of 4 or wider than 8 steps).
+int mrconv_headw_steps(int hd, int dt_bf16) {
+  if (hd < 4 || hd % 4) return 0;
+  const int ks = (hd + (dt_bf16 ? 32 : 16) - 1) / (dt_bf16 ? 32 : 16);
+  return ks <= 1 ? 1 : ks <= 2 ? 2 : ks <= 4 ? 4 : ks <= 8 ? 8 : 0;
+}
+
+template <int DT, int RT, int KSH>
+const void* headw_fn_kb(int KB) {
+  switch (KB) {
+    case 9: return (const void*)&mrconv_headw_kernel<DT, RT, 9, KSH>;
+    case 16: return (const void*)&mrconv_headw_kernel<DT, RT, 16, KSH>;
+    case 32: return (const void*)&mrconv_headw_kernel<DT, RT, 32, KSH>;
+    default: return (const void*)&mrconv_headw_kernel<DT, RT, 64, KSH>;
+  }
+}
+
+template <int DT, int RT>
+const void* headw_fn(int KSH, int KB) {
+  return KSH == 1 ? headw_fn_kb<DT, RT, 1>(KB) : KSH == 2 ? headw_fn_kb<DT, RT, 2>(KB)
+       : KSH == 4 ? headw_fn_kb<DT, RT, 4>(KB) : headw_fn_kb<DT, RT, 8>(KB);
+}
+
+hipError_t launch_mrconv_headw(const MrArgs& a, int dt_bf16, int rt, hipStream_t stream) {
+  const int hd = a.C / a.heads;
+  const int KSH = mrconv_headw_steps(hd, dt_bf16);
+  if (!KSH || rt < 1 || a.Cout != a.C) return hipErrorInvalidValue;
+  // few node tiles: 16-node tiles fill more CUs
+  if (rt == 2 && (a.R + 31) / 32 < 256) rt = 1;
+  const int TM = 16 * rt, KB = mrconv_k_bucket(a.k);
+  const void* fn = dt_bf16 ? (rt == 2 ? headw_fn<1, 2>(KSH, KB) : headw_fn<1, 1>(KSH, KB))
+                           : (rt == 2 ? headw_fn<0, 2>(KSH, KB) : headw_fn<0, 1>(KSH, KB));
+  const dim3 grid((a.R + TM - 1) / TM), block(kMrThreads);
+  return launch_with_smem(fn, grid, block, mrconv_smem_bytes(a.C, a.k, dt_bf16, rt), stream,
+                          nullptr, nullptr, a);
+}
+
+// Dense [C, 2C] = [W_x | W_m] from per-head Wh [H, hd, 2hd]: zero outside the
+// heads' diagonal blocks of each half.  One thread per element of the output.
+template <int DT>
+__global__ __launch_bounds__(256) void expand_heads_kernel(const void* __restrict__ Wh,
+                                                           void* __restrict__ Wd, int C, int hd) {
+  constexpr int ES = DT ? 2 : 4;
+  const long e = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (long)C * 2 * C) return;
+  const int o = (int)(e / (2 * C)), jj = (int)(e - (long)o * 2 * C);
+  const int half = jj >= C, j = jj - half * C;
+  const int h = o / hd;
+  const bool in = j / hd == h;
+  const long src = ((long)o * 2 * hd) + half * hd + (j - h * hd);
+  if (ES == 2) {
+    static_cast<uint16_t*>(Wd)[e] = in ? static_cast<const uint16_t*>(Wh)[src] : (uint16_t)0;
+  } else {
+    static_cast<float*>(Wd)[e] = in ? static_cast<const float*>(Wh)[src] : 0.f;
+  }
+}
+
+hipError_t launch_expand_heads(const void* Wh, void* Wd, int C, int heads, int dt_bf16,
+                               hipStream_t stream) {
+  const long n = (long)C * 2 * C;
+  const dim3 grid((unsigned)((n + 255) / 256)), block(256);
+  if (dt_bf16) hipLaunchKernelGGL(expand_heads_kernel<1>, grid, block, 0, stream, Wh, Wd, C, C / heads);
+  else hipLaunchKernelGGL(expand_heads_kernel<0>, grid, block, 0, stream, Wh, Wd, C, C / heads);
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

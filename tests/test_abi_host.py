@@ -156,9 +156,15 @@ def test_mrconv_workspace():
     # a good workspace passes every check; with no GPU the launch itself fails
     assert _mr(**big, ws=P(60), wsb=need) == "GL_ERR_HIP"
     L = api.lib()
-    st = L.gl_mrconv_heads(P(0), 64, 196, 640, None, 196, P(20), 9, P(30), None, 16, 1, P(40),
+    # channels too wide for the fused tile: Wh is expanded into a dense W in
+    # the workspace, ahead of the two-pass rows
+    assert L.gl_mrconv_heads_workspace_bytes(1, 196, 2560, 9, 16, 1) >= 2560 * 5120 * 2
+    st = L.gl_mrconv_heads(P(0), 1, 196, 2560, None, 196, P(20), 9, P(30), None, 16, 1, P(40),
                            None, 0, None)
     assert api.STATUS[st] == "GL_ERR_WORKSPACE"
+    # the fused tile reads Wh directly and needs none
+    assert L.gl_mrconv_heads_workspace_bytes(64, 196, 640, 9, 8, 1) == 0
+    assert L.gl_mrconv_heads_workspace_bytes(2, 196, 192, 9, 5, 1) == 0   # bad heads
 
 
 @host_only
