@@ -15,16 +15,17 @@
 //      floor), followed by a compare against the row's threshold: the
 //      K'-th packed key's distance bucket plus one, so no candidate that
 //      could enter the list is dropped.
-//   3. Every lane owns kStSlots LDS slots per row of its 4 rows (empty slots
-//      hold the marker 0xffffffff) and appends the keys that pass at its
-//      next free slot; a group of tiles in which no candidate of the wave
-//      passes skips the packing and stores.  Chunks are visited starting at
-//      the workgroup's own place in the key set, which tightens the
-//      thresholds early on image grids.  When some lane's slots could overflow in the next group of
-//      tiles, and at the end, the wave merges its 16 rows' slots into their
-//      sorted register lists (4 rows at a time, 16 lanes per row, the same
-//      bitonic merge as the in-register kernel), empties the slots and
-//      refreshes the thresholds.
+//   3. Every row has a buffer of kStCap LDS slots.  The row's passing keys of
+//      a tile are appended densely: a lane's place is the row's count plus
+//      the passing lanes before it in its 16-lane group (a wave ballot); a
+//      group of tiles in which no candidate of the wave passes skips the
+//      packing and stores.  Chunks are visited starting at the workgroup's
+//      own place in the key set, which tightens the thresholds early on image
+//      grids.  When some row's buffer could overflow in the next group of
+//      tiles, and at the end, the wave merges its 16 rows' buffers into their
+//      sorted register lists (ceil(count / 16) layers of 16 per row, 16 lanes
+//      per row, the same bitonic merge as the in-register kernel), empties
+//      them and refreshes the thresholds.
 // Results are identical to the in-register kernel: the same packed keys are
 // ranked, and the threshold only skips keys that cannot enter the list.
 #include "knn_tile.h"
@@ -33,7 +34,7 @@ namespace gl {
 
 constexpr int kStRows = 64;      // query rows per workgroup
 constexpr int kStCap = 128;      // candidate slots per row
-constexpr int kStSlots = kStCap / 16;  // slots per (lane, row)
+constexpr int kStSlots = kStCap / 16;  // layers of 16 in a full row buffer
 constexpr int kStRowStride = kStCap + 2;  // words per row of slots (rows 4 apart change bank)
 constexpr int kStGroup = 4;      // key tiles computed together (independent MFMA chains)
 constexpr int kStThreads = 256;
@@ -163,13 +164,60 @@ __device__ __forceinline__ void st_gram(f32x4 (&acc)[kStGroup], const uint4 (&af
   }
 }
 
+// The same in two halves, for the narrow rows: the B operands of a group are
+// requested (st_gram_load) one epilogue ahead of the MFMAs that use them
+// (st_gram_mma), so no MFMA waits on its own LDS read.
+template <int DT, int KS>
+__device__ __forceinline__ void st_gram_load(uint4 (&bv)[KS][kStGroup], const char* kbuf, int t0,
+                                             int kstride, int g, int t) {
+  constexpr int ES = DT ? 2 : 4;
+  constexpr int KSTEP = DT ? 32 : 16;
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const int c = s * KSTEP + g * (KSTEP / 4);
+#pragma unroll
+    for (int p = 0; p < kStGroup; ++p)
+      bv[s][p] = *reinterpret_cast<const uint4*>(kbuf + ((t0 + p) * 16 + t) * kstride + c * ES);
+  }
+}
+
+template <int DT, int KS>
+__device__ __forceinline__ void st_gram_mma(f32x4 (&acc)[kStGroup], const uint4 (&af)[KS],
+                                            const uint4 (&bv)[KS][kStGroup]) {
+#pragma unroll
+  for (int p = 0; p < kStGroup; ++p) acc[p] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < KS; ++s)
+#pragma unroll
+    for (int p = 0; p < kStGroup; ++p) {
+      if (DT) {
+        acc[p] = mfma_bf16(af[s], bv[s][p], acc[p]);
+      } else {
+        const float4 x4 = __builtin_bit_cast(float4, af[s]);
+        const float4 y4 = __builtin_bit_cast(float4, bv[s][p]);
+        acc[p] = mfma_f32(x4.x, y4.x, acc[p]);
+        acc[p] = mfma_f32(x4.y, y4.y, acc[p]);
+        acc[p] = mfma_f32(x4.z, y4.z, acc[p]);
+        acc[p] = mfma_f32(x4.w, y4.w, acc[p]);
+      }
+    }
+}
+
 // Merge the wave's buffered candidates of its 16 rows into their sorted lists,
-// empty the slots and refresh the filter thresholds.  L[p] holds row 4p + g
-// (16 lanes per row); tS[v] belongs to row 4g + v.  Slot s of lane t in row r
-// is cand[r * kStRowStride + 16 s + t].
+// empty the buffers and refresh the filter thresholds.  L[p] holds row 4p + g
+// (16 lanes per row); tS[v] and cnt[v] belong to row 4g + v.  Row r's buffer
+// is cand[r * kStRowStride + i], i < its count, densely filled, so a row of n
+// candidates is merged in ceil(n / 16) layers of 16.
 template <int R>
-__device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], uint32_t* cand,
-                                         uint32_t* tauL, int KK, int ib, int lane, int g, int t) {
+__device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], int (&cnt)[4],
+                                         uint32_t* cand, uint32_t* tauL, int KK, int ib, int lane,
+                                         int g, int t) {
+  // the counts travel to the lanes that merge the rows (row 4p + g is held by
+  // group g's lanes in the lists, counted by group p's lanes)
+  if (t == 0) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) tauL[4 * g + v] = (uint32_t)cnt[v];
+  }
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   __builtin_amdgcn_wave_barrier();
   // The rows of two list registers at a time are merged together: their sorts
@@ -178,44 +226,35 @@ __device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], ui
 #pragma unroll
   for (int p0 = 0; p0 < 4; p0 += 2) {
     uint32_t tk[2];
-    uint32_t v4[2][kStSlots];
-    int tr = t;
-    asm volatile("" : "+v"(tr));  // keeps the slot addresses out of the caller's loops
+    int n[2];
+    const uint32_t* src[2];
 #pragma unroll
     for (int pp = 0; pp < 2; ++pp) {
       const int row = 4 * (p0 + pp) + g;
+      n[pp] = (int)tauL[row];
       tk[pp] = list_element<R>(L[p0 + pp], KK - 1, lane);
-      // slot m of lane (t + m) mod 16: a lane's used slots spread over 16 readers
-#pragma unroll
-      for (int m = 0; m < kStSlots; ++m) {
-        uint32_t* slot = cand + row * kStRowStride + 16 * m + ((tr + m) & 15);
-        const uint32_t c = *slot;
-        *slot = 0xffffffffu;
-        v4[pp][m] = c < tk[pp] ? c : 0xffffffffu;
-      }
+      src[pp] = cand + row * kStRowStride + t;
     }
-    bool pass = false;
+    for (int m = 0; m < kStSlots; ++m) {
+      if (!__any(16 * m < n[0] || 16 * m < n[1])) break;
+      uint32_t c[2];
 #pragma unroll
-    for (int pp = 0; pp < 2; ++pp)
-#pragma unroll
-      for (int m = 0; m < kStSlots; ++m) pass |= v4[pp][m] != 0xffffffffu;
-    if (__any(pass)) {
-#pragma unroll
-      for (int pp = 0; pp < 2; ++pp) sort_regs_asc<kStSlots>(v4[pp]);
-      // layer m of both rows, while either still has a key below its
-      // threshold (merging a layer with none changes nothing among a list's
-      // first K' keys: keys are unique)
-#pragma unroll
-      for (int m = 0; m < kStSlots; ++m) {
-        if (!__any(v4[0][m] < tk[0] || v4[1][m] < tk[1])) break;
-        const uint32_t c0 = sort16_lanes(v4[0][m], t);
-        const uint32_t c1 = sort16_lanes(v4[1][m], t);
-        merge16_into_list<R>(L[p0], c0, t);
-        merge16_into_list<R>(L[p0 + 1], c1, t);
-        tk[0] = list_element<R>(L[p0], KK - 1, lane);
-        tk[1] = list_element<R>(L[p0 + 1], KK - 1, lane);
+      for (int pp = 0; pp < 2; ++pp) {
+        const uint32_t x = 16 * m + t < n[pp] ? src[pp][16 * m] : 0xffffffffu;
+        c[pp] = x < tk[pp] ? x : 0xffffffffu;
       }
+      // a layer with no key below its row's threshold changes nothing among
+      // the list's first K' keys (keys are unique)
+      if (!__any(c[0] != 0xffffffffu || c[1] != 0xffffffffu)) continue;
+      const uint32_t c0 = sort16_lanes(c[0], t);
+      const uint32_t c1 = sort16_lanes(c[1], t);
+      merge16_into_list<R>(L[p0], c0, t);
+      merge16_into_list<R>(L[p0 + 1], c1, t);
+      tk[0] = list_element<R>(L[p0], KK - 1, lane);
+      tk[1] = list_element<R>(L[p0 + 1], KK - 1, lane);
     }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
     if (t == 0) {
       tauL[4 * p0 + g] = tk[0];
       tauL[4 * (p0 + 1) + g] = tk[1];
@@ -227,6 +266,7 @@ __device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], ui
   for (int v = 0; v < 4; ++v) {
     const uint32_t tk = tauL[4 * g + v];
     tS[v] = tk == 0xffffffffu ? INFINITY : (float)((tk >> ib) + 1u);
+    cnt[v] = 0;
   }
 }
 
@@ -237,6 +277,7 @@ __device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], ui
 template <int DT, int R, int KS>
 __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int kstride, char* smem) {
   constexpr bool PIPE = KS <= 4 || KS >= kStWideKS;
+  constexpr bool SPLIT = KS <= 4;  // B operands one epilogue ahead of their MFMAs
   constexpr int MV = st_max_vec(KS);
   constexpr int ES = DT ? 2 : 4;
   constexpr int VEC = 16 / ES;
@@ -290,22 +331,18 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
 
   // -- selection state ------------------------------------------------------------
   // L[p]: sorted list of row 4p + g (element e = t + 16*a);  tS[v]: filter
-  // threshold of row 4g + v;  nS[v]: this lane's used slots of that row, which
-  // are cand[(4g + v) * kStRowStride + 16 s + t], s < nS[v].
+  // threshold of row 4g + v;  cnt[v]: candidates buffered for that row, at
+  // cand[(4g + v) * kStRowStride + i], i < cnt[v] (the same in the row's 16
+  // lanes).
   uint32_t L[4][R];
 #pragma unroll
   for (int p = 0; p < 4; ++p)
 #pragma unroll
     for (int q = 0; q < R; ++q) L[p][q] = 0xffffffffu;
   float tS[4] = {INFINITY, INFINITY, INFINITY, INFINITY};
-  int nS[4] = {0, 0, 0, 0};
-#pragma unroll
-  for (int m = 0; m < kStSlots; ++m)
-#pragma unroll
-    for (int p = 0; p < 4; ++p) cand[(4 * p + g) * kStRowStride + 16 * m + t] = 0xffffffffu;
-  uint32_t* mySlots = cand + 4 * g * kStRowStride + t;
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
+  int cnt[4] = {0, 0, 0, 0};
+  uint32_t* myRows = cand + 4 * g * kStRowStride;
+  const uint32_t below = (1u << t) - 1u;  // lanes of this lane's 16-lane group before it
 
   // -- zero pad of the key rows (channels C .. 32 KS); chunk stores leave it alone ----
   {
@@ -329,14 +366,18 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
   // A chunk of at most MV vectors per thread is prefetched into registers
   // while the previous one is used; larger chunks are copied piecewise when
   // their turn comes.
+  // The first chunk is loaded inside the loop too: with its loads issued
+  // ahead of the loop, the compiler's wait bookkeeping at the loop head keeps
+  // treating their registers as pending and makes every chunk wait for the
+  // next chunk's prefetch.
   const bool prefetch = nvec <= MV * kStThreads;
-  if (prefetch) st_load_chunk<DT>(regs, kb, ch0 * KC, M, C, CG, nvec, 0, tid);
   for (int c = 0; c < nchunks; ++c) {
     const int ch = ch0 + c < nchunks ? ch0 + c : ch0 + c - nchunks;
     const int chn = ch + 1 < nchunks ? ch + 1 : 0;
     const int k0 = ch * KC;
     const int ntl = (min(KC, M - k0) + 15) >> 4;
     if (prefetch) {
+      if (c == 0) st_load_chunk<DT>(regs, kb, k0, M, C, CG, nvec, 0, tid);
       st_store_chunk(regs, kbuf, kstride, CG, nvec, 0, tid);
     } else {
       for (int e0 = 0; e0 < nvec; e0 += MV * kStThreads) {
@@ -355,59 +396,88 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
     // tiles and keys past the end need no test.  Contraction steps past C
     // multiply a zero A operand.
     f32x4 acc[kStGroup];
-    if (PIPE) st_gram<DT, KS>(acc, af, kbuf, 0, kstride, C, g, t);
+    uint4 bv[SPLIT ? KS : 1][kStGroup];
+    if constexpr (SPLIT) {
+      st_gram_load<DT, KS>(bv, kbuf, 0, kstride, g, t);
+      st_gram_mma<DT, KS>(acc, af, bv);
+    } else if (PIPE) {
+      st_gram<DT, KS>(acc, af, kbuf, 0, kstride, C, g, t);
+    }
     for (int t0 = 0; t0 < ntl; t0 += kStGroup) {
+      // a group adds at most 16 * kStGroup candidates to a row; a row whose
+      // list is not full yet is merged as soon as it holds K' candidates
+      // (its threshold then drops from infinity)
       bool full = false;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) full |= nS[v] > kStSlots - kStGroup;
-      if (__any(full)) {
-        st_flush<R>(L, tS, cand, tauL, KK, ib, lane, g, t);
+      for (int v = 0; v < 4; ++v)
+        full |= cnt[v] > kStCap - 16 * kStGroup || (cnt[v] >= KK && tS[v] == INFINITY);
+      if (__any(full)) st_flush<R>(L, tS, cnt, cand, tauL, KK, ib, lane, g, t);
+      const bool more = t0 + kStGroup < ntl;
+      // this group's key scales, read ahead of the next group's B operands
+      // (LDS reads return in order)
+      float2 sc[kStGroup];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) nS[v] = 0;
-      }
+      for (int p = 0; p < kStGroup; ++p) sc[p] = ksc0[(t0 + p) * 16 + t];
       f32x4 nxt[kStGroup];
-      if (PIPE) {
-        if (t0 + kStGroup < ntl) st_gram<DT, KS>(nxt, af, kbuf, t0 + kStGroup, kstride, C, g, t);
+      if constexpr (SPLIT) {
+        // unconditional (the last group re-reads group 0): a branch here
+        // would make every later LDS wait assume these reads are in flight
+        st_gram_load<DT, KS>(bv, kbuf, more ? t0 + kStGroup : 0, kstride, g, t);
+      } else if (PIPE) {
+        if (more) st_gram<DT, KS>(nxt, af, kbuf, t0 + kStGroup, kstride, C, g, t);
       } else {
         st_gram<DT, KS>(acc, af, kbuf, t0, kstride, C, g, t);
       }
       // The common path per candidate is the distance and one compare; the
-      // packing and the slot store run only for the candidates that pass
-      // (empty slots already hold the empty marker), and not at all in a
-      // group where no lane of the wave has one.
+      // packing and the store run only for the candidates that pass, and not
+      // at all in a group where no lane of the wave has one.  A row's passing
+      // candidates of one tile go to consecutive places of its buffer: a
+      // lane's place is the row's count plus the passing lanes before it in
+      // its 16-lane group (from the wave's ballot).
       float dd[kStGroup][4];
-      bool anyp = false;
 #pragma unroll
-      for (int p = 0; p < kStGroup; ++p) {
-        const float2 sc = ksc0[(t0 + p) * 16 + t];
+      for (int p = 0; p < kStGroup; ++p)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          dd[p][v] = fmaf(acc[p][v] * sc.x, qr[v], sc.y);
-          anyp |= dd[p][v] < tS[v];
-        }
-      }
+        for (int v = 0; v < 4; ++v) dd[p][v] = fmaf(acc[p][v] * sc[p].x, qr[v], sc[p].y);
+      // does any candidate pass: one compare per row, on its group minimum
+      float dmin[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        dmin[v] = fminf(fminf(dd[0][v], dd[1][v]), fminf(dd[2][v], dd[3][v]));
+      const bool anyp = (dmin[0] < tS[0]) | (dmin[1] < tS[1]) | (dmin[2] < tS[2]) | (dmin[3] < tS[3]);
       if (__any(anyp)) {
 #pragma unroll
         for (int p = 0; p < kStGroup; ++p) {
           const uint32_t j = (uint32_t)(k0 + (t0 + p) * 16 + t);
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            if (dd[p][v] < tS[v]) {
+            const bool ps = dd[p][v] < tS[v];
+            const uint32_t gm = (uint32_t)(__ballot(ps) >> (16 * g)) & 0xffffu;
+            if (ps) {
               const uint32_t q = (uint32_t)__builtin_amdgcn_fmed3f(dd[p][v], 0.f, qmaxf);
-              mySlots[v * kStRowStride + 16 * nS[v]] = (q << ib) | j;
-              ++nS[v];
+              myRows[v * kStRowStride + cnt[v] + __popc(gm & below)] = (q << ib) | j;
             }
+            cnt[v] += __popc(gm);
           }
         }
       }
-      if (PIPE) {
+      if constexpr (SPLIT) {
+        if (more) st_gram_mma<DT, KS>(acc, af, bv);
+      } else if (PIPE) {
 #pragma unroll
         for (int p = 0; p < kStGroup; ++p) acc[p] = nxt[p];
       }
     }
+    // Every wave merges what it buffered in this chunk before the barrier: the
+    // waves wait for each other there anyway, so merges at the same place in
+    // every wave overlap instead of adding up, and the next chunk is filtered
+    // with fresh thresholds.
+    bool any = false;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) any |= cnt[v] > 0;
+    if (__any(any)) st_flush<R>(L, tS, cnt, cand, tauL, KK, ib, lane, g, t);
     __syncthreads();  // every wave is done with this chunk before it is overwritten
   }
-  st_flush<R>(L, tS, cand, tauL, KK, ib, lane, g, t);
 
   // -- dilation and output ------------------------------------------------------------
   const uint32_t mask = (1u << ib) - 1u;
