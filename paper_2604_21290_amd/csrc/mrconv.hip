@@ -17,6 +17,14 @@ int mrconv_row_tiles(int C, int k, int dt_bf16, size_t lds_limit) {
   return 0;
 }
 
+// The lean tile: narrow layers (at most 8 output tiles of 16 columns, 8
+// contraction steps) over at least two node tiles per CU, where more
+// workgroups in flight hide the gather's latency better than more work per
+// wave does.
+bool mrconv_use_lean(int C, int Cout, int row_tiles) {
+  return Cout <= 128 && C <= 128 && row_tiles >= 512;
+}
+
 int mrconv_k_bucket(int k) { return k <= 9 ? 9 : k <= 16 ? 16 : k <= 32 ? 32 : 64; }
 
 template <int DT, int RT, int KB>
@@ -24,6 +32,15 @@ __global__ __launch_bounds__(kMrThreads) __attribute__((amdgpu_waves_per_eu(3, 8
   extern __shared__ __align__(16) char smem[];
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
   mrconv_tile<DT, RT, KB>(smem, a, blk * 16 * RT);
+}
+
+// Narrow layers over many node tiles: one output tile per wave and pass and
+// one gather task per thread (78 VGPRs at k <= 9: six waves per SIMD).
+template <int DT, int RT, int KB>
+__global__ __launch_bounds__(kMrThreads) __attribute__((amdgpu_waves_per_eu(4, 8))) void mrconv_lean_kernel(MrArgs a) {
+  extern __shared__ __align__(16) char smem[];
+  const int blk = xcd_remap(blockIdx.x, gridDim.x);
+  mrconv_tile<DT, RT, KB, false, false, false, true>(smem, a, blk * 16 * RT);
 }
 
 // Small grids: workgroup blk computes output-column group blk % ncg (a.col_tiles
@@ -49,8 +66,16 @@ __global__ __launch_bounds__(kMrThreads) void mrconv_heads_kernel(MrArgs a) {
   mrconv_tile<DT, RT, KB, true>(smem, a, blk * 16 * RT);
 }
 
-template <int DT, int RT, bool HEADS = false, bool COLS = false>
+template <int DT, int RT, bool HEADS = false, bool COLS = false, bool LEAN = false>
 const void* mrconv_fn_kb(int KB) {
+  if (LEAN) {
+    switch (KB) {
+      case 9: return (const void*)&mrconv_lean_kernel<DT, RT, 9>;
+      case 16: return (const void*)&mrconv_lean_kernel<DT, RT, 16>;
+      case 32: return (const void*)&mrconv_lean_kernel<DT, RT, 32>;
+      default: return (const void*)&mrconv_lean_kernel<DT, RT, 64>;
+    }
+  }
   if (COLS) {
     switch (KB) {
       case 9: return (const void*)&mrconv_cols_kernel<DT, RT, 9>;
@@ -183,6 +208,9 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
   } else if (a.heads > 1) {
     fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2, true>(KB) : mrconv_fn_kb<1, 1, true>(KB))
                  : (rt == 2 ? mrconv_fn_kb<0, 2, true>(KB) : mrconv_fn_kb<0, 1, true>(KB));
+  } else if (mrconv_use_lean(a.C, Cout, row_tiles)) {
+    fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2, false, false, true>(KB) : mrconv_fn_kb<1, 1, false, false, true>(KB))
+                 : (rt == 2 ? mrconv_fn_kb<0, 2, false, false, true>(KB) : mrconv_fn_kb<0, 1, false, false, true>(KB));
   } else {
     fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2>(KB) : mrconv_fn_kb<1, 1>(KB))
                  : (rt == 2 ? mrconv_fn_kb<0, 2>(KB) : mrconv_fn_kb<0, 1>(KB));

@@ -62,19 +62,22 @@ __device__ __forceinline__ bool mr_step_needed(const MrArgs& a, int n0, int s, i
 // COLS: only output tiles tile0 .. tile_end-1 (a column group of a small grid),
 // one tile per wave and pass, with the W operands of kMrKUCols k-steps per batch.
 constexpr int kMrKUCols = 12;
-template <bool COLS> struct MrBatch {
-  static constexpr int KU = COLS ? kMrKUCols : kMrKU;  // k-steps per batch of W operands
-  static constexpr int NC = COLS ? 1 : 4;              // output tiles per wave and pass
+// LEAN: one output tile per wave and pass and one gather task per thread and
+// round, for narrow layers (few output tiles) that run many node tiles: the
+// registers saved buy more waves per SIMD.
+template <bool COLS, bool LEAN = false> struct MrBatch {
+  static constexpr int KU = COLS ? kMrKUCols : kMrKU;   // k-steps per batch of W operands
+  static constexpr int NC = COLS || LEAN ? 1 : 4;       // output tiles per wave and pass
 };
 
-template <int DT, bool HEADS, bool COLS = false>
-__device__ __forceinline__ void mr_load_w(uint4 (&bw)[MrBatch<COLS>::KU][MrBatch<COLS>::NC],
+template <int DT, bool HEADS, bool COLS = false, bool LEAN = false>
+__device__ __forceinline__ void mr_load_w(uint4 (&bw)[(MrBatch<COLS, LEAN>::KU)][(MrBatch<COLS, LEAN>::NC)],
                                           const MrArgs& a, const char* Wb, int w, int p, int s0,
                                           int K2, int Cout, int g, int t, int tile0 = 0,
                                           int tile_end = 0) {
   constexpr int ES = DT ? 2 : 4;
   constexpr int KSTEP = DT ? 32 : 16;
-  constexpr int KU = MrBatch<COLS>::KU, NC = MrBatch<COLS>::NC;
+  constexpr int KU = MrBatch<COLS, LEAN>::KU, NC = MrBatch<COLS, LEAN>::NC;
 #pragma unroll
   for (int c4 = 0; c4 < NC; ++c4) {
     const int n0 = ((COLS ? tile0 : 0) + w + 4 * (NC * p + c4)) * 16;
@@ -97,7 +100,7 @@ __device__ __forceinline__ void mr_load_w(uint4 (&bw)[MrBatch<COLS>::KU][MrBatch
 // written.  Called by all 256 threads.
 // T3: three tasks per thread in flight instead of two (a caller with registers
 // to spare takes the 32-node tile's 768 tasks of C = 192 in one round).
-template <int DT, int KB, bool T3 = false>
+template <int DT, int KB, bool T3 = false, bool LEAN = false>
 __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM,
                                                const int32_t* sIdx, char* dst, size_t dst_stride) {
   constexpr int ES = DT ? 2 : 4;
@@ -108,7 +111,7 @@ __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM
   // Each task is one (node, 16-byte channel vector); with a small neighbour
   // bucket two tasks keep their loads in flight together.
   constexpr int KG = KB < 16 ? KB : 16;    // neighbour loads in flight per group
-  constexpr int TPT = KB <= 9 ? (T3 ? 3 : 2) : 1;  // tasks per thread per iteration
+  constexpr int TPT = KB <= 9 && !LEAN ? (T3 ? 3 : 2) : 1;  // tasks per thread per iteration
   const int ntask = TM * CG;
   for (int e0 = tid; e0 < ntask; e0 += TPT * kMrThreads) {
     float mx[TPT][VEC];
@@ -173,7 +176,8 @@ __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM
 // HEADS: the multi-head update (a.heads > 1), which skips the zero blocks of W.
 // COLS: only the 16-column output tiles tile0 .. tile_end-1 (tile_end within
 // the layer's tiles), the column group of a small grid.
-template <int DT, int RT, int KB, bool HEADS = false, bool T3 = false, bool COLS = false>
+template <int DT, int RT, int KB, bool HEADS = false, bool T3 = false, bool COLS = false,
+          bool LEAN = false>
 __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row0, int tile0 = 0,
                                             int tile_end = 0) {
   constexpr int TM = 16 * RT;
@@ -203,13 +207,13 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
   const char* Wb = static_cast<const char*>(a.W);
   // output tiles past Cout are never loaded: their operands stay zero (their
   // results are not stored either)
-  constexpr int KU = MrBatch<COLS>::KU, NC = MrBatch<COLS>::NC;
+  constexpr int KU = MrBatch<COLS, LEAN>::KU, NC = MrBatch<COLS, LEAN>::NC;
   uint4 bw[KU][NC] = {};
   const int T0 = COLS ? tile0 : 0, TE = COLS ? tile_end : NCT;
-  if (T0 + w < TE) mr_load_w<DT, HEADS, COLS>(bw, a, Wb, w, 0, 0, K2, Cout, g, t, tile0, tile_end);
+  if (T0 + w < TE) mr_load_w<DT, HEADS, COLS, LEAN>(bw, a, Wb, w, 0, 0, K2, Cout, g, t, tile0, tile_end);
   __syncthreads();
 
-  mr_gather_rows<DT, KB, T3>(a, row0, TM, sIdx, sA, lds_row);
+  mr_gather_rows<DT, KB, T3, LEAN>(a, row0, TM, sIdx, sA, lds_row);
   __syncthreads();
 
   // -- FC on MFMA -----------------------------------------------------------------
@@ -225,7 +229,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
       nvalid[c4] = COLS ? T0 + w + 4 * (NC * p + c4) < TE : (w + 4 * (NC * p + c4)) * 16 < Cout;
     for (int s0 = 0; s0 < ksteps; s0 += KU) {
       if (p != 0 || s0 != 0)
-        mr_load_w<DT, HEADS, COLS>(bw, a, Wb, w, p, s0, K2, Cout, g, t, tile0, tile_end);
+        mr_load_w<DT, HEADS, COLS, LEAN>(bw, a, Wb, w, p, s0, K2, Cout, g, t, tile0, tile_end);
       bool kin[KU];
 #pragma unroll
       for (int u = 0; u < KU; ++u) kin[u] = (s0 + u) * KSTEP + g * (KSTEP / 4) < K2;

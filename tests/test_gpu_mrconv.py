@@ -71,9 +71,9 @@ EDGE = [
     ("split_fp32", 2, 77, None, 320, 136, 7, I.F32, True),
     ("split_pooled", 2, 196, 49, 576, 576, 9, I.BF16, True),
     ("split_k20", 1, 150, None, 512, 512, 20, I.BF16, False),
-    # 16 K nodes and more (hundreds of workgroups per CU): ragged last tile, a
-    # half contraction step (C % 16 == 8), narrow and wide Cout, pooled keys,
-    # k = 1 and k = 16
+    # 16 K nodes and more (at least 512 node tiles; C and Cout <= 128 take the
+    # lean tile): ragged last tile, a half contraction step (C % 16 == 8),
+    # narrow and wide Cout, pooled keys, k = 1 and k = 16, fp32
     ("large_R_ragged", 3, 5471, None, 64, 64, 9, I.BF16, True),
     ("large_R_C72_half_step", 2, 8200, None, 72, 72, 9, I.BF16, True),
     ("large_R_cout_40", 1, 16384, None, 48, 40, 5, I.BF16, False),
@@ -81,6 +81,7 @@ EDGE = [
     ("large_R_k7_pooled", 2, 8250, 100, 32, 32, 7, I.BF16, True),
     ("large_R_k1", 1, 16384, None, 16, 16, 1, I.BF16, False),
     ("large_R_k16", 1, 16384, None, 64, 64, 16, I.BF16, True),
+    ("large_R_fp32_lean", 1, 16400, None, 40, 56, 9, I.F32, True),
 ]
 
 
