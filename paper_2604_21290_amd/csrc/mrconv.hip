@@ -68,35 +68,34 @@ __global__ __launch_bounds__(kMrThreads) void mrconv_heads_kernel(MrArgs a) {
 
 template <int DT, int RT, bool HEADS = false, bool COLS = false, bool LEAN = false>
 const void* mrconv_fn_kb(int KB) {
-  if (LEAN) {
+  if constexpr (LEAN) {
     switch (KB) {
       case 9: return (const void*)&mrconv_lean_kernel<DT, RT, 9>;
       case 16: return (const void*)&mrconv_lean_kernel<DT, RT, 16>;
       case 32: return (const void*)&mrconv_lean_kernel<DT, RT, 32>;
       default: return (const void*)&mrconv_lean_kernel<DT, RT, 64>;
     }
-  }
-  if (COLS) {
+  } else if constexpr (COLS) {
     switch (KB) {
       case 9: return (const void*)&mrconv_cols_kernel<DT, RT, 9>;
       case 16: return (const void*)&mrconv_cols_kernel<DT, RT, 16>;
       case 32: return (const void*)&mrconv_cols_kernel<DT, RT, 32>;
       default: return (const void*)&mrconv_cols_kernel<DT, RT, 64>;
     }
-  }
-  if (HEADS) {
+  } else if constexpr (HEADS) {
     switch (KB) {
       case 9: return (const void*)&mrconv_heads_kernel<DT, RT, 9>;
       case 16: return (const void*)&mrconv_heads_kernel<DT, RT, 16>;
       case 32: return (const void*)&mrconv_heads_kernel<DT, RT, 32>;
       default: return (const void*)&mrconv_heads_kernel<DT, RT, 64>;
     }
-  }
-  switch (KB) {
-    case 9: return (const void*)&mrconv_kernel<DT, RT, 9>;
-    case 16: return (const void*)&mrconv_kernel<DT, RT, 16>;
-    case 32: return (const void*)&mrconv_kernel<DT, RT, 32>;
-    default: return (const void*)&mrconv_kernel<DT, RT, 64>;
+  } else {
+    switch (KB) {
+      case 9: return (const void*)&mrconv_kernel<DT, RT, 9>;
+      case 16: return (const void*)&mrconv_kernel<DT, RT, 16>;
+      case 32: return (const void*)&mrconv_kernel<DT, RT, 32>;
+      default: return (const void*)&mrconv_kernel<DT, RT, 64>;
+    }
   }
 }
 
@@ -209,6 +208,12 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
     fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2, true>(KB) : mrconv_fn_kb<1, 1, true>(KB))
                  : (rt == 2 ? mrconv_fn_kb<0, 2, true>(KB) : mrconv_fn_kb<0, 1, true>(KB));
   } else if (mrconv_use_lean(a.C, Cout, row_tiles)) {
+    // 64-node tiles when they fit 64 KB of LDS (measured 2-3 % faster than 32)
+    if (mrconv_smem_bytes(C, k, dt_bf16, 4) <= 65536) {
+      fn = dt_bf16 ? mrconv_fn_kb<1, 4, false, false, true>(KB) : mrconv_fn_kb<0, 4, false, false, true>(KB);
+      return launch_with_smem(fn, dim3((a.R + 63) / 64), block, mrconv_smem_bytes(C, k, dt_bf16, 4),
+                              stream, ev0, ev1, a);
+    }
     fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2, false, false, true>(KB) : mrconv_fn_kb<1, 1, false, false, true>(KB))
                  : (rt == 2 ? mrconv_fn_kb<0, 2, false, false, true>(KB) : mrconv_fn_kb<0, 1, false, false, true>(KB));
   } else {
