@@ -17,12 +17,12 @@ int mrconv_row_tiles(int C, int k, int dt_bf16, size_t lds_limit) {
   return 0;
 }
 
-// The lean tile: narrow layers (at most 8 output tiles of 16 columns, 8
-// contraction steps) over at least two node tiles per CU, where more
-// workgroups in flight hide the gather's latency better than more work per
-// wave does.
+// The lean tile: layers of at most 16 output tiles of 16 columns over at least
+// one node tile of 32 per CU.  There more workgroups in flight hide the
+// gather's latency better than more work per wave does, and (on 64-node
+// tiles) each workgroup's pass over W serves twice the nodes.
 bool mrconv_use_lean(int C, int Cout, int row_tiles) {
-  return Cout <= 128 && C <= 128 && row_tiles >= 512;
+  return Cout <= 256 && C <= 256 && row_tiles >= 256;
 }
 
 int mrconv_k_bucket(int k) { return k <= 9 ? 9 : k <= 16 ? 16 : k <= 32 ? 32 : 64; }

@@ -63,7 +63,7 @@ __device__ __forceinline__ bool mr_step_needed(const MrArgs& a, int n0, int s, i
 // one tile per wave and pass, with the W operands of kMrKUCols k-steps per batch.
 constexpr int kMrKUCols = 12;
 // LEAN: one output tile per wave and pass and one gather task per thread and
-// round, for narrow layers (few output tiles) that run many node tiles: the
+// round, for layers of few output tiles that run many node tiles: the
 // registers saved buy more waves per SIMD.
 template <bool COLS, bool LEAN = false> struct MrBatch {
   static constexpr int KU = COLS ? kMrKUCols : kMrKU;   // k-steps per batch of W operands

@@ -71,9 +71,10 @@ EDGE = [
     ("split_fp32", 2, 77, None, 320, 136, 7, I.F32, True),
     ("split_pooled", 2, 196, 49, 576, 576, 9, I.BF16, True),
     ("split_k20", 1, 150, None, 512, 512, 20, I.BF16, False),
-    # 16 K nodes and more (at least 512 node tiles; C and Cout <= 128 take the
-    # lean tile): ragged last tile, a half contraction step (C % 16 == 8),
-    # narrow and wide Cout, pooled keys, k = 1 and k = 16, fp32
+    # 8 K nodes and more (at least 256 node tiles; C and Cout <= 256 take the
+    # lean tile, on 64-node tiles when they fit 64 KB of LDS): ragged last
+    # tile, a half contraction step (C % 16 == 8), narrow and wide Cout,
+    # pooled keys, k = 1 and k = 16, fp32
     ("large_R_ragged", 3, 5471, None, 64, 64, 9, I.BF16, True),
     ("large_R_C72_half_step", 2, 8200, None, 72, 72, 9, I.BF16, True),
     ("large_R_cout_40", 1, 16384, None, 48, 40, 5, I.BF16, False),
@@ -82,6 +83,10 @@ EDGE = [
     ("large_R_k1", 1, 16384, None, 16, 16, 1, I.BF16, False),
     ("large_R_k16", 1, 16384, None, 64, 64, 16, I.BF16, True),
     ("large_R_fp32_lean", 1, 16400, None, 40, 56, 9, I.F32, True),
+    ("large_R_C192_lean64", 1, 8200, None, 192, 192, 9, I.BF16, True),
+    ("large_R_C256_lean32_cout200", 1, 8300, None, 256, 200, 9, I.BF16, False),
+    ("large_R_fp32_C160_lean32", 1, 8300, None, 160, 96, 7, I.F32, True),
+    ("large_R_C264_not_lean", 1, 8300, None, 264, 64, 9, I.BF16, True),
 ]
 
 
