@@ -17,11 +17,8 @@
  *     library allocates no device memory on any call that enqueues work: the
  *     calls that need scratch memory take a caller-owned workspace, whose size
  *     a *_workspace_bytes query gives, and fail with GL_ERR_WORKSPACE when it
- *     is missing or short.  (gl_lookahead_create creates two HIP events and,
- *     where the device supports stream wait-value operations, allocates 16
- *     bytes of device memory for its hand-off sequence numbers, freed by
- *     gl_lookahead_destroy; gl_lookahead_set_profiling creates HIP events;
- *     nothing else is created.)
+ *     is missing or short.  (gl_lookahead_create and
+ *     gl_lookahead_set_profiling create HIP events; nothing else is created.)
  *     The library keeps no pointer after a call returns.  Buffers must stay
  *     alive until the streams the work was enqueued on have finished it.
  *   Layout.  Row-major, channels last: features [B, N, C], keys [B, M, C],
@@ -219,15 +216,10 @@ gl_status gl_mrconv_heads(const void* x, int B, int N, int C, const void* keys, 
 
 /* ---------------------------------------------------------------------------
  * Lookahead handle (Sec. IV-A, IV-F; the look-ahead buffer of Sec. IV-G).
- * Orders the build stream against the update stream with two monotonically
- * growing 64-bit sequence numbers in device memory, written and waited on by
- * stream memory operations (hipStreamWriteValue64 / hipStreamWaitValue64),
- * or with two HIP events where the device lacks those.  The caller owns both
- * streams, every tensor and the workspace of the layers that take the
- * two-pass MRConv (see gl_mrconv).  Streams must be distinct for the build to
- * overlap the update; they may be equal.  Destroy a handle only after the
- * work enqueued through it has finished (gl_lookahead_destroy frees the
- * sequence numbers, which synchronises the device).
+ * Holds two HIP events that order the build stream against the update
+ * stream; the caller owns both streams, every tensor and the workspace of
+ * the layers that take the two-pass MRConv (see gl_mrconv).  Streams must be
+ * distinct for the build to overlap the update; they may be equal.
  * -------------------------------------------------------------------------*/
 typedef struct gl_lookahead* gl_lookahead_t;
 

@@ -157,12 +157,6 @@ constexpr uint32_t kHandleMagic = 0x474c4c41u;  // "GLLA"
 struct gl_lookahead {
   uint32_t magic;
   hipStream_t su, sb;
-  // Hand-offs between the streams: two 64-bit sequence numbers in device
-  // memory, written and waited on by stream memory operations (a hand-off
-  // measured about 4.5 us, against about 13 us for an event record + wait),
-  // or, where the device does not support those, two events.
-  uint64_t* seq;             // [0] x ready (update -> build), [1] built (build -> update)
-  uint64_t n_ready, n_built;
   hipEvent_t ev_ready, ev_built;
   bool pending;
   int prof_max;
@@ -218,14 +212,6 @@ gl_status enqueue_build(gl_lookahead_t h, const void* x, int B, int N, int C, co
 // Order the build stream after the update stream's work so far.
 gl_status fork_build(gl_lookahead_t h) {
   hipError_t e;
-  if (h->seq) {
-    const uint64_t n = ++h->n_ready;
-    if ((e = hipStreamWriteValue64(h->su, h->seq, n, 0)) != hipSuccess)
-      return hip_fail(e, "hipStreamWriteValue64");
-    if ((e = hipStreamWaitValue64(h->sb, h->seq, n, hipStreamWaitValueGte, ~0ull)) != hipSuccess)
-      return hip_fail(e, "hipStreamWaitValue64");
-    return GL_OK;
-  }
   if ((e = hipEventRecord(h->ev_ready, h->su)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if ((e = hipStreamWaitEvent(h->sb, h->ev_ready, 0)) != hipSuccess)
     return hip_fail(e, "hipStreamWaitEvent");
@@ -233,18 +219,16 @@ gl_status fork_build(gl_lookahead_t h) {
 }
 
 gl_status mark_built(gl_lookahead_t h) {
-  hipError_t e = h->seq ? hipStreamWriteValue64(h->sb, h->seq + 1, ++h->n_built, 0)
-                        : hipEventRecord(h->ev_built, h->sb);
-  if (e != hipSuccess) return hip_fail(e, "mark built");
+  hipError_t e = hipEventRecord(h->ev_built, h->sb);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
   h->pending = true;
   return GL_OK;
 }
 
 gl_status join_build(gl_lookahead_t h) {
   if (!h->pending) return GL_OK;
-  hipError_t e = h->seq ? hipStreamWaitValue64(h->su, h->seq + 1, h->n_built, hipStreamWaitValueGte, ~0ull)
-                        : hipStreamWaitEvent(h->su, h->ev_built, 0);
-  if (e != hipSuccess) return hip_fail(e, "join build");
+  hipError_t e = hipStreamWaitEvent(h->su, h->ev_built, 0);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
   h->pending = false;
   return GL_OK;
 }
@@ -487,36 +471,14 @@ gl_status gl_lookahead_create(hipStream_t s_update, hipStream_t s_build, gl_look
   h->pending = false;
   h->prof_max = 0;
   h->prof_n[0] = h->prof_n[1] = h->prof_n[2] = h->prof_n[3] = 0;
-  h->seq = nullptr;
-  h->n_ready = h->n_built = 0;
-  int dev = 0, can_wait = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e == hipSuccess)
-    e = hipDeviceGetAttribute(&can_wait, hipDeviceAttributeCanUseStreamWaitValue, dev);
+  hipError_t e = hipEventCreateWithFlags(&h->ev_ready, hipEventDisableTiming);
   if (e != hipSuccess) {
-    delete h;
-    return hip_fail(e, "hipDeviceGetAttribute");
-  }
-  if (can_wait) {
-    // the sequence numbers start at 0 and only grow (64 bits never wrap)
-    if ((e = hipMalloc((void**)&h->seq, 2 * sizeof(uint64_t))) == hipSuccess)
-      e = hipMemset(h->seq, 0, 2 * sizeof(uint64_t));
-    if (e != hipSuccess) {
-      if (h->seq) (void)hipFree(h->seq);
-      delete h;
-      return hip_fail(e, "lookahead sequence numbers");
-    }
-  }
-  e = hipEventCreateWithFlags(&h->ev_ready, hipEventDisableTiming);
-  if (e != hipSuccess) {
-    if (h->seq) (void)hipFree(h->seq);
     delete h;
     return hip_fail(e, "hipEventCreate");
   }
   e = hipEventCreateWithFlags(&h->ev_built, hipEventDisableTiming);
   if (e != hipSuccess) {
     (void)hipEventDestroy(h->ev_ready);
-    if (h->seq) (void)hipFree(h->seq);
     delete h;
     return hip_fail(e, "hipEventCreate");
   }
@@ -529,7 +491,6 @@ gl_status gl_lookahead_destroy(gl_lookahead_t h) {
   free_profiling(h);
   (void)hipEventDestroy(h->ev_ready);
   (void)hipEventDestroy(h->ev_built);
-  if (h->seq) (void)hipFree(h->seq);  // synchronises the device first
   h->magic = 0;
   delete h;
   return GL_OK;
