@@ -113,6 +113,51 @@ def test_knn_edges(case):
     _say(label, _knn_case(x, k, d, keys, label=label))
 
 
+# Keys resident in LDS, 64 query rows per workgroup (bf16, M <= 256, 32 < C <=
+# 128, at least 512 workgroups): every key-tile bucket (4 / 8 / 13 / 16 tiles),
+# one to four contraction steps' worth of channels with partial last steps,
+# K' up to 64, ragged last row tiles.  Sampled rows keep the oracle fast.
+RESIDENT = [
+    # label, B, N, M, C, k, d
+    ("res_pyr_like_ragged", 16, 2049, 196, 80, 9, 1),
+    ("res_C40_M100_KK18", 32, 1000, 100, 40, 9, 2),
+    ("res_C128_M256_KK64", 8, 4100, 256, 128, 16, 4),
+    ("res_C72_M64", 16, 2048, 64, 72, 9, 3),
+    ("res_C56_M209", 16, 2048, 209, 56, 9, 1),
+    ("res_C96_M17_k1", 16, 2047, 17, 96, 1, 1),
+]
+
+
+@pytest.mark.parametrize("case", RESIDENT, ids=[c[0] for c in RESIDENT])
+def test_knn_resident(case):
+    require_gpu()
+    label, B, N, M, C, k, d = case
+    seed = zlib.crc32(label.encode()) % 10000
+    x = I.random_features(seed, B, N, C, I.BF16, unit=False)
+    keys = I.random_features(seed + 1, B, M, C, I.BF16, unit=False)
+    rows = np.sort(np.random.default_rng(seed).choice(N, 256, replace=False))
+    _say(label, _knn_case(x, k, d, keys, rows=rows, label=label))
+
+
+def test_knn_resident_duplicates_and_zero_rows():
+    """Zero query rows, zero key rows and duplicated key rows on the
+    resident-key kernel: ties resolve to the lower key index."""
+    require_gpu()
+    g = np.random.default_rng(11)
+    B, N, M, C = 8, 4096, 150, 64
+    a = g.standard_normal((B, N, C))
+    kv = g.standard_normal((B, M, C))
+    a[:, ::7] = 0.0
+    kv[:, 10] = 0.0
+    kv[:, 20:40] = kv[:, 0:20]
+    x = I.store(a, I.BF16)
+    keys = I.store(kv, I.BF16)
+    rows = np.sort(np.concatenate([np.arange(0, 70, 7), g.choice(N, 246, replace=False)]))
+    rows = np.unique(rows)
+    for d in (1, 3):
+        _say("resident dup/zero", _knn_case(x, 9, d, keys, rows=rows, label=f"res dup d={d}"))
+
+
 @pytest.mark.parametrize("C", [32, 512])
 def test_knn_duplicates_and_zero_rows(C):
     require_gpu()

@@ -152,6 +152,35 @@ def test_stack_entry_matches_blocks_and_serial(name):
     assert torch.equal(fused, out), "one-launch blocks differ from the two-stream schedule"
 
 
+def test_pooled_builds_agree_across_kernels():
+    """At the pyramid's first stage the standalone build keeps the keys
+    resident in LDS, while the one-launch block builds with the in-register
+    tile.  Both must rank the same packed keys.  With the dilation changing
+    from block to block, the fused schedule builds every next graph inside
+    the block and the two-stream schedule builds it standalone; the two
+    stacks must be equal bit for bit, and the graphs are teacher-forced."""
+    require_gpu()
+    import dataclasses
+    from paper_2604_21290_amd import api
+    w = dataclasses.replace(I.WORKLOADS["pyr_s1"], dilations=(1, 2, 3, 1))
+    x0 = I.make_features(w)
+    Wst, bst = _weights(w, w.L)
+    x0d, Wd, bd = to_dev(x0), to_dev(Wst), to_dev(bst)
+    _say("pooled builds", w.name, "dilations", w.dilations)
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    two = la.stack(x0d, w.H, w.W, Wd, bd, list(w.dilations), w.k, w.pool_r)
+    ws = api.make_stack_workspace(x0d, w.H, w.W, w.k, w.pool_r)
+    fused = la.stack(x0d, w.H, w.W, Wd, bd, list(w.dilations), w.k, w.pool_r,
+                     schedule=api.GL_SCHED_LOOKAHEAD_FUSED, ws=ws)
+    torch.cuda.synchronize()
+    la.close()
+    assert torch.equal(fused, two), "block-built graphs differ from standalone-built graphs"
+    xs, graphs = run_blocks(w, x0d, Wd, bd)
+    assert torch.equal(xs[-1], two)
+    rows = np.sort(np.random.default_rng(8).choice(w.N, 256, replace=False))
+    teacher_forced_checks(w, xs, graphs, Wst, bst, n_img=2, rows=rows)
+
+
 def _fused_graph_buffer(dil, Lp):
     """Which of the two graph buffers holds the graph the last block of an
     Lp-block fused-schedule stack used (the stack's own buffer rotation)."""

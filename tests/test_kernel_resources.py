@@ -1,7 +1,7 @@
 """Register budget of the latency-bound kernels (CPU; compiles for gfx950).
 
 The one-launch block kernel, the fused MRConv and the in-register kNN run at
-three waves per SIMD, the lean MRConv at four or more, the wide kNN at two; if the register allocator has to spill to scratch
+three waves per SIMD, the lean MRConv and the resident-key kNN at four or more, the wide kNN at two; if the register allocator has to spill to scratch
 memory to meet that, they slow down without failing any parity test.  This
 test compiles their sources with the resource-usage remarks and requires no
 scratch for every instantiation of them."""
@@ -17,7 +17,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2604_21290_amd", "csrc")
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 KERNELS = {"block.hip": "block_kernel", "mrconv.hip": r"13mrconv_kernel|18mrconv_lean_kernel",
-           "knn.hip": "knn_kernel", "knn_wide.hip": "knn_wide_kernel"}
+           "knn.hip": "knn_kernel", "knn_wide.hip": "knn_wide_kernel",
+           "knn_resident.hip": "knn_resident_kernel"}
 
 
 def _usage(src: str, tmp) -> list:
