@@ -434,12 +434,15 @@ hipError_t launch_expand_heads(const void* Wh, void* Wd, int C, int heads, int d
 // ---------------------------------------------------------------------------
 // r x r pooling of the node grid, stride r: the average (key nodes of pyramid
 // stages) or the maximum (node reduction between pyramid stages, Sec. IV-E).
-// One thread per (image, output node, 16-byte channel vector); the window's
-// r*r loads of a thread are independent.  The maximum of stored values is
-// exact; the average is accumulated in fp32 and rounded once.
+// One thread per (image, output node, 16-byte channel vector).  For the
+// window sizes the pyramids use (RR = 2, 4) all r*r loads of a thread are
+// issued before any is summed, so the window costs one memory round trip;
+// other r (RR = 0) loop.  The window is summed in row-major order either way.
+// The maximum of stored values is exact; the average is accumulated in fp32
+// and rounded once.
 // ---------------------------------------------------------------------------
-template <int DT, bool MAX>
-__global__ __launch_bounds__(256) void pool_kernel(const void* __restrict__ x,
+template <int DT, bool MAX, int RR>
+__global__ __launch_bounds__(128) void pool_kernel(const void* __restrict__ x,
                                                    void* __restrict__ keys, int B, int H, int W,
                                                    int C, int r) {
   constexpr int ES = DT ? 2 : 4;
@@ -457,12 +460,31 @@ __global__ __launch_bounds__(256) void pool_kernel(const void* __restrict__ x,
 #pragma unroll
   for (int i = 0; i < VEC; ++i) acc[i] = MAX ? -INFINITY : 0.f;
   const char* xb = static_cast<const char*>(x) + ((size_t)b * H * W * C + cg * VEC) * ES;
-  for (int u = 0; u < r; ++u) {
-    for (int v = 0; v < r; ++v) {
-      float f[VEC];
-      load_vec<DT>(xb + (size_t)((p * r + u) * W + (q * r + v)) * C * ES, f);
+  auto add = [&](const float* f) {
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) acc[i] = MAX ? fmaxf(acc[i], f[i]) : acc[i] + f[i];
+    for (int i = 0; i < VEC; ++i) acc[i] = MAX ? fmaxf(acc[i], f[i]) : acc[i] + f[i];
+  };
+  if constexpr (RR > 0) {
+    uint4 raw[RR * RR];
+#pragma unroll
+    for (int u = 0; u < RR; ++u)
+#pragma unroll
+      for (int v = 0; v < RR; ++v)
+        raw[u * RR + v] = *reinterpret_cast<const uint4*>(
+            xb + (size_t)((p * RR + u) * W + (q * RR + v)) * C * ES);
+#pragma unroll
+    for (int i = 0; i < RR * RR; ++i) {
+      float f[VEC];
+      load_vec<DT>(reinterpret_cast<const char*>(&raw[i]), f);
+      add(f);
+    }
+  } else {
+    for (int u = 0; u < r; ++u) {
+      for (int v = 0; v < r; ++v) {
+        float f[VEC];
+        load_vec<DT>(xb + (size_t)((p * r + u) * W + (q * r + v)) * C * ES, f);
+        add(f);
+      }
     }
   }
   if (!MAX) {
@@ -473,19 +495,21 @@ __global__ __launch_bounds__(256) void pool_kernel(const void* __restrict__ x,
   store_vec<DT>(static_cast<char*>(keys) + ((size_t)(b * Mo + o) * C + cg * VEC) * ES, acc);
 }
 
+template <int DT, bool MAX>
+const void* pool_fn(int r) {
+  return r == 2 ? (const void*)&pool_kernel<DT, MAX, 2>
+         : r == 4 ? (const void*)&pool_kernel<DT, MAX, 4> : (const void*)&pool_kernel<DT, MAX, 0>;
+}
+
 hipError_t launch_pool(const void* x, void* keys, int B, int H, int W, int C, int r, int dt_bf16,
                        hipStream_t stream, bool max_pool) {
   const int VEC = dt_bf16 ? 8 : 4;
   const long total = (long)B * (H / r) * (W / r) * (C / VEC);
-  dim3 grid((unsigned)((total + 255) / 256)), block(256);
-  if (max_pool) {
-    if (dt_bf16) hipLaunchKernelGGL((pool_kernel<1, true>), grid, block, 0, stream, x, keys, B, H, W, C, r);
-    else hipLaunchKernelGGL((pool_kernel<0, true>), grid, block, 0, stream, x, keys, B, H, W, C, r);
-  } else {
-    if (dt_bf16) hipLaunchKernelGGL((pool_kernel<1, false>), grid, block, 0, stream, x, keys, B, H, W, C, r);
-    else hipLaunchKernelGGL((pool_kernel<0, false>), grid, block, 0, stream, x, keys, B, H, W, C, r);
-  }
-  return hipGetLastError();
+  const void* fn = max_pool ? (dt_bf16 ? pool_fn<1, true>(r) : pool_fn<0, true>(r))
+                            : (dt_bf16 ? pool_fn<1, false>(r) : pool_fn<0, false>(r));
+  dim3 grid((unsigned)((total + 127) / 128)), block(128);
+  void* argv[] = {&x, &keys, &B, &H, &W, &C, &r};
+  return hipLaunchKernel(fn, grid, block, argv, 0, stream);
 }
 
 }  // namespace gl
