@@ -83,6 +83,33 @@ __device__ __forceinline__ uint32_t list_element(const uint32_t* L, int e, int l
   return row_broadcast16(v, e & 15, lane);
 }
 
+// The 4 smallest of a lane's 16 values, ascending, in v[0..3]; v[4..15] hold
+// the other 12 in no order.  Four sorted groups of 4 (five comparators each),
+// then three merges that keep the 4 smallest of two sorted groups sorted
+// (a half-cleaner against the reversed second group, then a 4-element
+// bitonic sort): 44 compare-exchanges against the full bitonic sort's 80.
+__device__ __forceinline__ void top4_regs_asc(uint32_t (&v)[16]) {
+#pragma unroll
+  for (int q = 0; q < 16; q += 4) {
+    cas_asc(v[q], v[q + 1]);
+    cas_asc(v[q + 2], v[q + 3]);
+    cas_asc(v[q], v[q + 2]);
+    cas_asc(v[q + 1], v[q + 3]);
+    cas_asc(v[q + 1], v[q + 2]);
+  }
+  auto merge4 = [&](int a, int b) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) cas_asc(v[a + i], v[b + 3 - i]);
+    cas_asc(v[a], v[a + 2]);
+    cas_asc(v[a + 1], v[a + 3]);
+    cas_asc(v[a], v[a + 1]);
+    cas_asc(v[a + 2], v[a + 3]);
+  };
+  merge4(0, 4);
+  merge4(8, 12);
+  merge4(0, 8);
+}
+
 // Merge this lane's 16 candidates v (one row per 16 lanes) into the row's
 // sorted list L of the KK smallest keys; tau is the list's KK-th key (all ones
 // while the list is not full).  Candidates not below tau are dropped first; the
@@ -96,6 +123,36 @@ __device__ __forceinline__ void select_chunk(uint32_t* L, uint32_t& tau, uint32_
   if (__any(pass)) {
 #pragma unroll
     for (int m = 0; m < 16; ++m) v[m] = v[m] < tau ? v[m] : 0xffffffffu;
+    if constexpr (R == 1) {
+      // A list of at most 16 rarely takes more than each lane's 4 smallest:
+      // those are ordered first, and the rest only when some lane's fifth
+      // smallest is still below the threshold after them.
+      top4_regs_asc(v);
+#pragma unroll
+      for (int m = 0; m < 4; m += 2) {
+        if (!__any(v[m] < tau)) return;
+        const uint32_t c0 = sort16_lanes(v[m], t);
+        const uint32_t c1 = sort16_lanes(v[m + 1], t);
+        merge16_into_list<R>(L, c0, t);
+        merge16_into_list<R>(L, c1, t);
+        tau = list_element<R>(L, KK - 1, lane);
+      }
+      uint32_t fifth = v[4];
+#pragma unroll
+      for (int m = 5; m < 16; ++m) fifth = min(fifth, v[m]);
+      if (!__any(fifth < tau)) return;
+      sort_regs_asc<16>(v);  // v[0..3] are already the smallest four, in order
+#pragma unroll
+      for (int m = 4; m < 16; m += 2) {
+        if (!__any(v[m] < tau)) break;
+        const uint32_t c0 = sort16_lanes(v[m], t);
+        const uint32_t c1 = sort16_lanes(v[m + 1], t);
+        merge16_into_list<R>(L, c0, t);
+        merge16_into_list<R>(L, c1, t);
+        tau = list_element<R>(L, KK - 1, lane);
+      }
+      return;
+    }
     sort_regs_asc<16>(v);
     // Two layers per pass: their 16-lane sorts are independent chains that
     // the scheduler interleaves.  The second layer may hold no key below the
