@@ -71,7 +71,7 @@ __device__ __forceinline__ u32x4 gelu_vec(u32x4 v) {
 }
 
 template <int DT, int ACT_IN, int ACT_OUT, int BM, int STEP, int NW = 4>
-__global__ __launch_bounds__(64 * NW) void gemm_nt_kernel(GemmArgs a) {
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BM == 128 ? 4 : 1, 8))) void gemm_nt_kernel(GemmArgs a) {
   extern __shared__ __align__(16) char smem[];
   using G = GemmCfg<BM, STEP, NW>;
   constexpr int kGmBM = BM, kGmBN = BM, kGmStep = STEP, kGmRow = G::kRow, kGmTile = G::kTile;
@@ -102,23 +102,38 @@ __global__ __launch_bounds__(64 * NW) void gemm_nt_kernel(GemmArgs a) {
     bg[i] = Wb + (size_t)min(n0 + r, Cout - 1) * rowb + slot[i];
     lo[i] = r * kGmRow + slot[i];
   }
-  u32x4 ra[kGmVec], rb[kGmVec];
-  auto gload = [&](int s) {
+  // staging register sets: one for the 64 x 64 tiles (the next stage is in
+  // flight while one is multiplied), three for the 128 x 128 tiles (two stages
+  // ahead: their long contractions are otherwise bound by the latency of each
+  // stage's global loads).  A GELU on A (act_in) keeps one: its staging is
+  // VALU work that measured slower with the deeper pipeline.
+  constexpr int NSET = BM == 128 && !ACT_IN ? 3 : 1;
+  u32x4 ra[NSET][kGmVec], rb[NSET][kGmVec];
+  // Slots past the contraction load column 0 and are zeroed when they are
+  // stored, not when they arrive: touching a loaded register right after its
+  // load makes the wave wait for it there.
+  auto gload = [&](int q, int s) {
 #pragma unroll
     for (int i = 0; i < kGmVec; ++i) {
-      const bool in = s * kGmStep + slot[i] < rowb;
-      const int off = in ? s * kGmStep : 0;
-      ra[i] = *reinterpret_cast<const u32x4*>(ag[i] + off);
-      rb[i] = *reinterpret_cast<const u32x4*>(bg[i] + off);
-      if (!in) ra[i] = rb[i] = u32x4{0, 0, 0, 0};
+      const int off = s * kGmStep + slot[i] < rowb ? s * kGmStep : 0;
+      ra[q][i] = *reinterpret_cast<const u32x4*>(ag[i] + off);
+      rb[q][i] = *reinterpret_cast<const u32x4*>(bg[i] + off);
     }
   };
-  auto sstore = [&](int buf) {
+  auto sstore = [&](int q, int buf, int s) {
     char* sa = smem + buf * 2 * kGmTile;
 #pragma unroll
     for (int i = 0; i < kGmVec; ++i) {
-      *reinterpret_cast<u32x4*>(sa + lo[i]) = ACT_IN ? gelu_vec<DT>(ra[i]) : ra[i];
-      *reinterpret_cast<u32x4*>(sa + kGmTile + lo[i]) = rb[i];
+      // an empty asm that uses the loaded registers pins their first use here:
+      // otherwise the scheduler hoists the zeroing selects (whose condition is
+      // known early) to just after the loads, and the wave waits for loads
+      // meant to stay in flight for two more stages
+      asm volatile("" : "+v"(ra[q][i]), "+v"(rb[q][i]));
+      const bool in = s * kGmStep + slot[i] < rowb;
+      const u32x4 va = in ? ra[q][i] : u32x4{0, 0, 0, 0};
+      const u32x4 vb = in ? rb[q][i] : u32x4{0, 0, 0, 0};
+      *reinterpret_cast<u32x4*>(sa + lo[i]) = ACT_IN ? gelu_vec<DT>(va) : va;
+      *reinterpret_cast<u32x4*>(sa + kGmTile + lo[i]) = vb;
     }
   };
 
@@ -151,11 +166,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_nt_kernel(GemmArgs a) {
     }
   }
 
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int s = 0; s < nstages; ++s) {
-    if (s + 1 < nstages) gload(s + 1);
+  auto multiply = [&](int s) {
     const char* sa = smem + (s & 1) * 2 * kGmTile;
 #pragma unroll
     for (int kk = 0; kk < kGmStep / 64; ++kk) {
@@ -184,8 +195,41 @@ __global__ __launch_bounds__(64 * NW) void gemm_nt_kernel(GemmArgs a) {
           }
         }
     }
-    if (s + 1 < nstages) sstore((s + 1) & 1);
+  };
+
+  if constexpr (NSET == 3) {
+    // Stage s is multiplied out of LDS buffer s & 1 while stage s+1 waits in
+    // register set (s+1) % 3 and stage s+2 is on its way into set (s+2) % 3;
+    // set s % 3, stored to LDS one iteration earlier, then takes stage s+3.
+    // The loop runs whole groups of three stages, so each register set keeps
+    // its role and no load's wait is merged with another's: stages past the
+    // contraction (at most two) load in-range addresses, are stored as zeros
+    // and are not multiplied.
+    gload(0, 0);
+    gload(1, 1);
+    gload(2, 2);
+    sstore(0, 0, 0);
     __syncthreads();
+    for (int s0 = 0; s0 < nstages; s0 += 3) {
+#pragma unroll
+      for (int u = 0; u < 3; ++u) {
+        const int s = s0 + u;
+        if (s < nstages) multiply(s);
+        sstore((u + 1) % 3, (s + 1) & 1, s + 1);
+        gload(u, s + 3);
+        __syncthreads();
+      }
+    }
+  } else {
+    gload(0, 0);
+    sstore(0, 0, 0);
+    __syncthreads();
+    for (int s = 0; s < nstages; ++s) {
+      if (s + 1 < nstages) gload(0, s + 1);
+      multiply(s);
+      if (s + 1 < nstages) sstore(0, (s + 1) & 1, s + 1);
+      __syncthreads();
+    }
   }
 
   // -- epilogue: lane (g, t) of tile (i, j) holds rows 4g..4g+3, column t --------
