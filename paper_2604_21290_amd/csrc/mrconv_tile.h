@@ -217,6 +217,11 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
   __syncthreads();
 
   // -- FC on MFMA -----------------------------------------------------------------
+  // PIPE (the one-launch block's update role, which has the registers): the W
+  // operands of the next batch of k-steps are requested before the current
+  // batch is multiplied, so no batch after the first waits on its own loads.
+  constexpr bool PIPE = T3 && !HEADS && !COLS && !LEAN;
+  uint4 bw2[KU][NC] = {};
   for (int p = 0; T0 + w + 4 * NC * p < TE; ++p) {
     f32x4 acc[RT][NC];
 #pragma unroll
@@ -227,9 +232,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
 #pragma unroll
     for (int c4 = 0; c4 < NC; ++c4)
       nvalid[c4] = COLS ? T0 + w + 4 * (NC * p + c4) < TE : (w + 4 * (NC * p + c4)) * 16 < Cout;
-    for (int s0 = 0; s0 < ksteps; s0 += KU) {
-      if (p != 0 || s0 != 0)
-        mr_load_w<DT, HEADS, COLS, LEAN>(bw, a, Wb, w, p, s0, K2, Cout, g, t, tile0, tile_end);
+    auto batch = [&](const uint4 (&bv4)[KU][NC], int s0) {
       bool kin[KU];
 #pragma unroll
       for (int u = 0; u < KU; ++u) kin[u] = (s0 + u) * KSTEP + g * (KSTEP / 4) < K2;
@@ -245,7 +248,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
         for (int c4 = 0; c4 < NC; ++c4) {
           if (HEADS && !mr_step_needed(a, (w + 4 * (NC * p + c4)) * 16, s0 + u, KSTEP)) continue;
           // past 2C the A operand is zero and bv a real W element (column 0)
-          const uint4 bv = bw[u][c4];
+          const uint4 bv = bv4[u][c4];
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt) {
             if (DT) {
@@ -260,6 +263,26 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
             }
           }
         }
+      }
+    };
+    if constexpr (PIPE) {
+      // batches in pairs: bw holds batch s0 (for the first pass, requested
+      // before the gather), bw2 batch s0 + KU; each set is refilled while
+      // the other is multiplied.  Past the contraction nothing is multiplied.
+      if (p != 0) mr_load_w<DT, HEADS, COLS, LEAN>(bw, a, Wb, w, p, 0, K2, Cout, g, t, tile0, tile_end);
+      for (int s0 = 0; s0 < ksteps; s0 += 2 * KU) {
+        if (s0 + KU < ksteps)
+          mr_load_w<DT, HEADS, COLS, LEAN>(bw2, a, Wb, w, p, s0 + KU, K2, Cout, g, t, tile0, tile_end);
+        batch(bw, s0);
+        if (s0 + 2 * KU < ksteps)
+          mr_load_w<DT, HEADS, COLS, LEAN>(bw, a, Wb, w, p, s0 + 2 * KU, K2, Cout, g, t, tile0, tile_end);
+        if (s0 + KU < ksteps) batch(bw2, s0 + KU);
+      }
+    } else {
+      for (int s0 = 0; s0 < ksteps; s0 += KU) {
+        if (p != 0 || s0 != 0)
+          mr_load_w<DT, HEADS, COLS, LEAN>(bw, a, Wb, w, p, s0, K2, Cout, g, t, tile0, tile_end);
+        batch(bw, s0);
       }
     }
     // -- epilogue: + bias, round once, store ------------------------------------
