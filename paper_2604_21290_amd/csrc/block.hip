@@ -50,7 +50,7 @@ __device__ __forceinline__ void block_body(char* smem, const KnnArgs& ka, const 
   if (block_role_is_build(blockIdx.x, nb, nu, &j)) {
     j = xcd_remap(j, nb);
     if constexpr (WK > 0) {
-      knn_wide_tile<R, kWdQW, WK, kBlockWideDB>(smem, ka, j);
+      knn_wide_tile<R, kWdQW, WK, kBlockWideDB, true>(smem, ka, j);
     } else {
       const int nt = (ka.N + kKnnRows - 1) / kKnnRows;
       const int b = j / nt, tile = j - b * nt;

@@ -65,7 +65,10 @@ constexpr int kWdQW = 2;
 // One workgroup's tile: blk is its index among the B * ceil(N / QR) tiles.
 // smem holds WideGeom<QW, KROWS>::kSmem bytes.  Called by all 256 threads.
 // DB: two staging register sets (else one, for a caller with fewer registers).
-template <int R, int QW, int KROWS, bool DB = true>
+// SKIP: the padding stage of an odd stage count is not multiplied (measured
+// faster in the one-launch block, slower standalone; the result is the same,
+// since a zero stage adds nothing).
+template <int R, int QW, int KROWS, bool DB = true, bool SKIP = false>
 __device__ __forceinline__ void knn_wide_tile(char* smem, const KnnArgs& a, int blk) {
   using G = WideGeom<QW, KROWS>;
   constexpr int NV = G::kNV, NKT = G::kNKT, QR = G::kQR, SPLIT = G::kSplit;
@@ -151,10 +154,10 @@ __device__ __forceinline__ void knn_wide_tile(char* smem, const KnnArgs& a, int 
 
   // At the top of step s, stage s is in LDS buffer s & 1 and stage s + 1 is in
   // flight into st1 (even s) or st0 (odd s).  The loop runs whole pairs of
-  // steps with no conditions, so that each register set keeps its role and no
-  // branch surrounds the MFMAs: stages past the last (at most two, plus one
-  // when the count is odd) load in-range addresses and are stored as zeros,
-  // which add nothing to the accumulators or the norms.
+  // steps, so that each register set keeps its role: stages past the last (at
+  // most two, plus one when the count is odd) load in-range addresses and are
+  // stored as zeros, which add nothing to the accumulators or the norms.  With
+  // SKIP the one padding stage of an odd count is not multiplied.
   if constexpr (DB) {
     const int npair = (nstage + 1) >> 1;
     gload(st0, 0);
@@ -168,7 +171,7 @@ __device__ __forceinline__ void knn_wide_tile(char* smem, const KnnArgs& a, int 
       sstore(st1, s + 1, 1);
       __syncthreads();
       gload(st1, s + 3);
-      multiply(s + 1);
+      if (!SKIP || s + 1 < nstage) multiply(s + 1);  // an odd count's last pair has one stage
       sstore(st0, s + 2, 0);
       __syncthreads();
     }
