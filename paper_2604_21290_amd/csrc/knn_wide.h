@@ -65,9 +65,10 @@ constexpr int kWdQW = 2;
 // One workgroup's tile: blk is its index among the B * ceil(N / QR) tiles.
 // smem holds WideGeom<QW, KROWS>::kSmem bytes.  Called by all 256 threads.
 // DB: two staging register sets (else one, for a caller with fewer registers).
-// SKIP: the padding stage of an odd stage count is not multiplied (measured
-// faster in the one-launch block, slower standalone; the result is the same,
-// since a zero stage adds nothing).
+// SKIP: the padding stage of an odd stage count, and a wave's last key tile
+// when it lies wholly past M, are not multiplied (measured faster in the
+// one-launch block, slower standalone; the result is the same: a zero stage
+// adds nothing, and tiles past M are masked in the epilogue).
 template <int R, int QW, int KROWS, bool DB = true, bool SKIP = false>
 __device__ __forceinline__ void knn_wide_tile(char* smem, const KnnArgs& a, int blk) {
   using G = WideGeom<QW, KROWS>;
@@ -140,11 +141,13 @@ __device__ __forceinline__ void knn_wide_tile(char* smem, const KnnArgs& a, int 
     for (int kk = 0; kk < kWdStep / 64; ++kk) {
       const uint4 af = *reinterpret_cast<const uint4*>(sa + (16 * wr + t) * kWdRow + kk * 64 + g * 16);
       // every staged key tile is multiplied (tiles past M hold repeated rows and
-      // are masked in the epilogue): a branch here would make the compiler copy
-      // the accumulators around it
+      // are masked in the epilogue): standalone, a branch here made the compiler
+      // copy the accumulators around it.  With SKIP (accumulators in VGPRs)
+      // the wave's last tile is skipped when it lies wholly past M.
 #pragma unroll
       for (int j = 0; j < NKT; ++j) {
         const int kt = wk + SPLIT * j;
+        if (SKIP && j == NKT - 1 && kt >= nkt) continue;
         const uint4 bf =
             *reinterpret_cast<const uint4*>(sa + (QR + 16 * kt + t) * kWdRow + kk * 64 + g * 16);
         acc[j] = mfma_bf16(af, bf, acc[j]);
