@@ -19,7 +19,7 @@
 //      a tile are appended densely: a lane's place is the row's count plus
 //      the passing lanes before it in its 16-lane group (a wave ballot); a
 //      group of tiles in which no candidate of the wave passes skips the
-//      packing and stores.  Chunks are visited starting at the workgroup's
+//      packing and stores.  Chunks are visited outwards from the workgroup's
 //      own place in the key set, which tightens the thresholds early on image
 //      grids.  When some row's buffer could overflow in the next group of
 //      tiles, and at the end, the wave merges its 16 rows' buffers into their
@@ -357,12 +357,19 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
   // One LDS key buffer; the next chunk waits in registers while this one is used.
   char* kbuf = kbuf0;
   const int nchunks = (M + KC - 1) / KC;
-  // The chunks are visited in a rotated order that starts with the chunk at
-  // the workgroup's own position in the key set (its first query row scaled
-  // by M / N).  The selected lists do not depend on the order; on image
-  // grids a node's nearest keys tend to lie near it, so the thresholds
-  // tighten after the first chunk and fewer candidates pass the filter.
+  // The chunks are visited outwards from the chunk at the workgroup's own
+  // position in the key set (its first query row scaled by M / N): ch0,
+  // ch0 + 1, ch0 - 1, ch0 + 2, ... (mod nchunks, each chunk once).  The
+  // selected lists do not depend on the order; on image grids a node's
+  // nearest keys tend to lie near it, above as well as below in row-major
+  // order, so the thresholds tighten within the first few chunks and fewer
+  // candidates pass the filter.
   const int ch0 = (int)(((long long)q0 * M / N) / KC);
+  auto chunk_at = [&](int c) {
+    const int off = (c & 1) ? (c + 1) >> 1 : -(c >> 1);
+    const int ch = (ch0 + off) % nchunks;
+    return ch < 0 ? ch + nchunks : ch;
+  };
   // A chunk of at most MV vectors per thread is prefetched into registers
   // while the previous one is used; larger chunks are copied piecewise when
   // their turn comes.
@@ -372,8 +379,8 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
   // next chunk's prefetch.
   const bool prefetch = nvec <= MV * kStThreads;
   for (int c = 0; c < nchunks; ++c) {
-    const int ch = ch0 + c < nchunks ? ch0 + c : ch0 + c - nchunks;
-    const int chn = ch + 1 < nchunks ? ch + 1 : 0;
+    const int ch = chunk_at(c);
+    const int chn = chunk_at(c + 1 < nchunks ? c + 1 : c);
     const int k0 = ch * KC;
     const int ntl = (min(KC, M - k0) + 15) >> 4;
     if (prefetch) {
