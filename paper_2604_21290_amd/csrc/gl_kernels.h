@@ -81,9 +81,10 @@ hipError_t launch_knn_stream(const KnnArgs& a, int dt_bf16, hipStream_t stream, 
 // bf16 rows of C >= 128 against at most 256 keys use the LDS-staged kernel.
 bool knn_use_wide(int M, int C, int dt_bf16);
 hipError_t launch_knn_wide(const KnnArgs& a, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
-// Many query rows (B * ceil(N / 64) >= 512 workgroups) of 33..128 bf16
+// Many query rows (B * ceil(N / 64) >= 384 workgroups) of 33..160 bf16
 // channels against at most 256 keys: keys resident in LDS, 64 rows per
-// workgroup; its packed keys equal the in-register kernel's.
+// workgroup; its packed keys equal those of the one-launch block's build
+// role for the same shape (in-register tile below C = 128, wide tile above).
 bool knn_use_resident(int B, int N, int M, int C, int dt_bf16);
 hipError_t launch_knn_resident(const KnnArgs& a, hipStream_t stream, hipEvent_t ev0,
                                hipEvent_t ev1);

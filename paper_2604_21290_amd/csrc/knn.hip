@@ -49,8 +49,8 @@ hipError_t launch_knn(const void* x, const void* keys, int B, int N, int C, int 
                       hipEvent_t ev0, hipEvent_t ev1) {
   const KnnArgs a = make_knn_args(x, keys, B, N, C, M, k, dil, idx_out);
   if (knn_use_stream(M, C, dt_bf16)) return launch_knn_stream(a, dt_bf16, stream, ev0, ev1);
-  if (knn_use_wide(M, C, dt_bf16)) return launch_knn_wide(a, stream, ev0, ev1);
   if (knn_use_resident(B, N, M, C, dt_bf16)) return launch_knn_resident(a, stream, ev0, ev1);
+  if (knn_use_wide(M, C, dt_bf16)) return launch_knn_wide(a, stream, ev0, ev1);
   const size_t smem = knn_smem_bytes(C, dt_bf16);
   const dim3 grid(B * ((N + kKnnRows - 1) / kKnnRows)), block(kKnnThreads);
   const int R = knn_list_regs(a.KK);

@@ -17,12 +17,14 @@
 //      register per row.  So each of a wave's four row groups is selected
 //      straight from registers with the filtered sort-and-merge, and no
 //      candidate strip goes through LDS.
-// The packed keys are bit-identical to the in-register kernel's. Both use
-// the same norm summation order (per 8-channel slice, chained over the
-// contraction steps, then (s0 + s1) + (s2 + s3)), the same MFMA contraction
-// order and the same epilogue.  So the graph is the same whichever kernel
-// builds it, which the one-launch block relies on: its build role is the
-// in-register tile.
+// The packed keys are bit-identical to those of the kernel the one-launch
+// block uses as its build role for the same shape: the in-register tile below
+// C = 128, the LDS-staged wide tile from C = 128 on.  The MFMA contraction
+// order and the epilogue are the same as both; the norms are summed in the
+// order of the kernel matched (per 8-channel slice of each 32-channel step,
+// chained over the steps, then (s0 + s1) + (s2 + s3); or per 16-byte slot of
+// each 128-byte stage, chained over the stages, then reduced over the eight
+// slots as a tree).  So the graph is the same whichever kernel builds it.
 #include "knn_tile.h"
 
 namespace gl {
@@ -46,15 +48,18 @@ inline size_t resident_smem(int C) {
 // Key tiles compiled for M keys: 4, 8, 13 (M <= 208) or 16.
 inline int knn_resident_tiles(int M) { return M <= 64 ? 4 : M <= 128 ? 8 : M <= 208 ? 13 : 16; }
 
-// bf16, at most 256 keys of 33..128 channels, and enough query rows that
-// 64-row workgroups still give the chip at least two each per CU.
+// bf16, at most 256 keys of 33..160 channels, and enough query rows to give
+// the chip at least 384 workgroups of 64 (about 1.5 per CU; past 128 channels
+// the LDS holds two workgroups per CU).
 bool knn_use_resident(int B, int N, int M, int C, int dt_bf16) {
-  return dt_bf16 && M <= 256 && C > 32 && C <= 128 && C % 8 == 0 &&
-         (long long)B * ((N + kRsRows - 1) / kRsRows) >= 512;
+  return dt_bf16 && M <= 256 && C > 32 && C <= 160 && C % 8 == 0 &&
+         (long long)B * ((N + kRsRows - 1) / kRsRows) >= 384;
 }
 
+// Five contraction steps (C > 128) stage 70 KB of keys, two workgroups per CU,
+// so that variant is compiled for two waves per SIMD.
 template <int R, int KS, int KT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void knn_resident_kernel(KnnArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KS > 4 ? 2 : 4, 8))) void knn_resident_kernel(KnnArgs a) {
   extern __shared__ __align__(16) char smem[];
   constexpr int NK = KT * 16;  // key rows staged
   // key tiles that are whole for every M of this bucket (M > 0, 64, 128, 208)
@@ -109,36 +114,72 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   if (tid < 4) *reinterpret_cast<uint4*>(sZero + 16 * tid) = make_uint4(0, 0, 0, 0);
   __syncthreads();
 
-  // -- key scale pairs, one thread per key row.  Slice p (channels s*32 + 8p
-  //    .. +7 of every step s) is chained over s exactly as a lane of the
-  //    in-register kernel chains it (its slices past C add zero there), and
-  //    the slices are combined in that kernel's shuffle order.
+  // -- key scale pairs, one thread per key row, summed in the order of the
+  //    block's build role for this shape (slices past C add zero there).
+  //    Below C = 128 (the in-register tile): slice p, channels s*32 + 8p .. +7
+  //    of every step s, chained over s, then (s0 + s1) + (s2 + s3), that
+  //    kernel's shuffle order.  From C = 128 (the wide tile): slot p, channels
+  //    64 S + 8p .. +7 of every 128-byte stage S, chained over S, then the
+  //    xor tree over the eight slots.
+  const bool wide = C >= 128;
   const float qscale = a.qscale;
   if (tid < NK) {
-    float sl[4];
+    const char* row = smem + tid * stride;
+    float sj;
+    if (wide) {
+      float sl[8];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      float acc = 0.f;
+      for (int p = 0; p < 8; ++p) {
+        float acc = 0.f;
 #pragma unroll
-      for (int s = 0; s < KS; ++s)
-        if (s * 32 + p * 8 < C)
-          acc = sumsq_bf16x8(*reinterpret_cast<const uint4*>(smem + tid * stride + s * 64 + p * 16), acc);
-      sl[p] = acc;
+        for (int S = 0; S < (KS + 1) / 2; ++S)
+          if (S * 64 + p * 8 < C)
+            acc = sumsq_bf16x8(*reinterpret_cast<const uint4*>(row + S * 128 + p * 16), acc);
+        sl[p] = acc;
+      }
+      sj = ((sl[0] + sl[1]) + (sl[2] + sl[3])) + ((sl[4] + sl[5]) + (sl[6] + sl[7]));
+    } else {
+      float sl[4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        float acc = 0.f;
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+          if (s * 32 + p * 8 < C)
+            acc = sumsq_bf16x8(*reinterpret_cast<const uint4*>(row + s * 64 + p * 16), acc);
+        sl[p] = acc;
+      }
+      sj = (sl[0] + sl[1]) + (sl[2] + sl[3]);
     }
-    const float sj = (sl[0] + sl[1]) + (sl[2] + sl[3]);
     sScale[tid] = make_float2(-2.f * key_rnorm(sj) * qscale, (sj > 0.f ? 2.f : 1.f) * qscale);
   }
 
-  // -- query norms (the in-register kernel's order) and the Gram ------------
-  float qss = 0.f;
+  // -- query norms in the same order (lane g holds channels 32 s + 8 g of
+  //    step s: slice g of the step, or slot g (even s) / g + 4 (odd s) of
+  //    stage s / 2), and the Gram
 #pragma unroll
-  for (int s = 0; s < KS; ++s) {
-    const int c = s * 32 + g * 8;
-    if (c >= C) af[s] = make_uint4(0, 0, 0, 0);
-    qss = sumsq_bf16x8(af[s], qss);
+  for (int s = 0; s < KS; ++s)
+    if (s * 32 + g * 8 >= C) af[s] = make_uint4(0, 0, 0, 0);
+  float qss;
+  if (wide) {
+    float qa = 0.f, qb = 0.f;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      if (s & 1) qb = sumsq_bf16x8(af[s], qb);
+      else qa = sumsq_bf16x8(af[s], qa);
+    }
+    qa += __shfl_xor(qa, 16);
+    qa += __shfl_xor(qa, 32);
+    qb += __shfl_xor(qb, 16);
+    qb += __shfl_xor(qb, 32);
+    qss = qa + qb;
+  } else {
+    qss = 0.f;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qss = sumsq_bf16x8(af[s], qss);
+    qss += __shfl_xor(qss, 16);
+    qss += __shfl_xor(qss, 32);
   }
-  qss += __shfl_xor(qss, 16);
-  qss += __shfl_xor(qss, 32);
   const float rq = 1.f / fmaxf(sqrtf(qss), 1e-12f);
   float qr[4];
 #pragma unroll
@@ -210,7 +251,8 @@ const void* resident_fn_steps(int KS, int KT) {
   switch (KS) {
     case 2: return resident_fn_tiles<R, 2>(KT);
     case 3: return resident_fn_tiles<R, 3>(KT);
-    default: return resident_fn_tiles<R, 4>(KT);
+    case 4: return resident_fn_tiles<R, 4>(KT);
+    default: return resident_fn_tiles<R, 5>(KT);
   }
 }
 

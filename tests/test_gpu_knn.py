@@ -114,9 +114,10 @@ def test_knn_edges(case):
 
 
 # Keys resident in LDS, 64 query rows per workgroup (bf16, M <= 256, 32 < C <=
-# 128, at least 512 workgroups): every key-tile bucket (4 / 8 / 13 / 16 tiles),
-# one to four contraction steps' worth of channels with partial last steps,
-# K' up to 64, ragged last row tiles.  Sampled rows keep the oracle fast.
+# 160, at least 384 workgroups): every key-tile bucket (4 / 8 / 13 / 16 tiles),
+# two to five contraction steps' worth of channels with partial last steps,
+# both norm orders (below and from C = 128), K' up to 64, ragged last row
+# tiles.  Sampled rows keep the oracle fast.
 RESIDENT = [
     # label, B, N, M, C, k, d
     ("res_pyr_like_ragged", 16, 2049, 196, 80, 9, 1),
@@ -125,6 +126,9 @@ RESIDENT = [
     ("res_C72_M64", 16, 2048, 64, 72, 9, 3),
     ("res_C56_M209", 16, 2048, 209, 56, 9, 1),
     ("res_C96_M17_k1", 16, 2047, 17, 96, 1, 1),
+    ("res_C128_wide_order", 16, 1600, 196, 128, 9, 1),
+    ("res_C136_M150_KK18", 32, 800, 150, 136, 9, 2),
+    ("res_C160_M256_KK64", 8, 3100, 256, 160, 16, 4),
 ]
 
 

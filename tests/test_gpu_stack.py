@@ -152,17 +152,19 @@ def test_stack_entry_matches_blocks_and_serial(name):
     assert torch.equal(fused, out), "one-launch blocks differ from the two-stream schedule"
 
 
-def test_pooled_builds_agree_across_kernels():
-    """At the pyramid's first stage the standalone build keeps the keys
+@pytest.mark.parametrize("name", ["pyr_s1", "pyr_s2"])
+def test_pooled_builds_agree_across_kernels(name):
+    """At the pyramid's first two stages the standalone build keeps the keys
     resident in LDS, while the one-launch block builds with the in-register
-    tile.  Both must rank the same packed keys.  With the dilation changing
-    from block to block, the fused schedule builds every next graph inside
-    the block and the two-stream schedule builds it standalone; the two
-    stacks must be equal bit for bit, and the graphs are teacher-forced."""
+    tile (stage 1, C = 80) or the LDS-staged wide tile (stage 2, C = 160).
+    Both must rank the same packed keys.  With the dilation changing from
+    block to block, the fused schedule builds every next graph inside the
+    block and the two-stream schedule builds it standalone; the two stacks
+    must be equal bit for bit, and the graphs are teacher-forced."""
     require_gpu()
     import dataclasses
     from paper_2604_21290_amd import api
-    w = dataclasses.replace(I.WORKLOADS["pyr_s1"], dilations=(1, 2, 3, 1))
+    w = dataclasses.replace(I.WORKLOADS[name], dilations=(1, 2, 3, 1))
     x0 = I.make_features(w)
     Wst, bst = _weights(w, w.L)
     x0d, Wd, bd = to_dev(x0), to_dev(Wst), to_dev(bst)
