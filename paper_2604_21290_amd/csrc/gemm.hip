@@ -11,14 +11,14 @@
 // 64 or 128 rows and A once per 64 or 128 output channels.
 //   - 4 waves in a 2 x 2 layout, or 8 in a 4 x 2 layout; each wave holds its
 //     block of the tile (2 x 2 ... 2 x 4 MFMA tiles of 16 x 16) in registers.
-//   - The contraction runs in stages of 256 bytes per row (4 MFMA k-steps:
-//     128 bf16 or 64 fp32 channels), so the short contractions of the ViG
-//     layers (K = 192 .. 1280) take 1 .. 10 stages, each one global round
-//     trip.  Both operands are K-contiguous, so one 16-byte vector per lane is
-//     exactly an MFMA operand slice.  A stage's A and B tiles (64 rows x 256
-//     bytes each) pass through LDS, double-buffered: the global loads of stage
-//     s+1 are in flight while stage s is multiplied, and one barrier per stage
-//     separates the buffers.
+//   - The contraction runs in stages of 256 bytes per row on the 64 x 64
+//     tiles (4 MFMA k-steps: 128 bf16 or 64 fp32 channels) and of 128 bytes
+//     on the 128 x 128 tiles.  Both operands are K-contiguous, so one 16-byte
+//     vector per lane is exactly an MFMA operand slice.  A stage's A and B
+//     tiles pass through LDS, double-buffered, with one barrier per stage.
+//     The global loads of stage s+1 are in flight while stage s is multiplied;
+//     the 128 x 128 tiles keep three staging register sets, so their loads
+//     are issued two stages ahead.
 //   - act_in is applied to A's elements as they are staged (fp32, rounded back
 //     to the storage type, as if the caller had stored sigma(A)).
 //   - Epilogue in fp32: + bias, act_out, + residual, rounded once.
