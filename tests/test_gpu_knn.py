@@ -201,8 +201,11 @@ def test_knn_deterministic():
 def test_pool_edges():
     require_gpu()
     from paper_2604_21290_amd import api
+    # windows of r = 2 and 4 take the kernels that issue the whole window at
+    # once (both storage types); r = 1 and 3 take the loop
     for (B, H, W, C, r, dt) in [(2, 8, 12, 16, 4, I.BF16), (1, 6, 6, 8, 3, I.F32),
-                                (3, 10, 10, 24, 1, I.BF16), (1, 28, 28, 160, 2, I.F32)]:
+                                (3, 10, 10, 24, 1, I.BF16), (1, 28, 28, 160, 2, I.F32),
+                                (2, 8, 16, 12, 4, I.F32), (3, 6, 10, 40, 2, I.BF16)]:
         x = I.random_features(H * W + C, B, H * W, C, dt, unit=False)
         _say("pool", B, H, W, C, r, dt)
         k = api.pool_keys(to_dev(x), H, W, r)
