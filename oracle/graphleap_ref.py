@@ -36,7 +36,8 @@ notes):
     x Phi(x); fully connected layers are x W^T + b with W[out, in] and an
     optional bias; there is no normalisation layer (the equations have none);
     MRConv is single-head; the FFN is C -> 4C -> C.  Its lookahead graph comes
-    from the projected features U^(l-1) (U^0 for blocks 0 and 1).
+    from the projected features U^(l-1) (U^0 for blocks 0 and 1).  At pyramid
+    stages its keys are pooled from U, as the reduced block's are from X.
 """
 from __future__ import annotations
 
@@ -289,16 +290,21 @@ def linear_ref(x: np.ndarray, W: np.ndarray, b: np.ndarray | None = None) -> np.
     return out
 
 
-def vig_block_ref(x: np.ndarray, idx: np.ndarray, p: dict, return_all: bool = False):
-    """Block l of Alg. 1 given the graph it uses (idx into U's rows):
+def vig_block_ref(x: np.ndarray, idx: np.ndarray, p: dict, return_all: bool = False,
+                  H: int | None = None, W: int | None = None, pool_r: int = 1):
+    """Block l of Alg. 1 given the graph it uses:
         U  = X W_in^T + b_in                        (FC1, Eq. 11)
         Ut = MRConv(U; idx)  with W_upd [C, 2C]     (Eq. 13)
         Y  = sigma(Ut) W_out^T + b_out + X          (FC2 + residual, Eq. 14)
         X' = sigma(Y W_1^T + b_1) W_2^T + b_2 + Y   (FFN + residual, Eq. 15)
-    Missing biases are zero.  Returns X' (or X', U, Ut, Y)."""
+    idx indexes U's rows, or with pool_r > 1 the rows of U's r x r key
+    pooling over the H x W grid, which MRConv then gathers (the pyramid
+    stages' pooled keys).  Missing biases are zero.  Returns X' (or X', U,
+    Ut, Y)."""
     x = np.asarray(x, dtype=np.float64)
     u = linear_ref(x, p["W_in"], p.get("b_in"))
-    ut = mrconv_ref(u, idx, p["W_upd"], p.get("b_upd"))
+    keys = pool_keys_ref(u, H, W, pool_r) if pool_r > 1 else None
+    ut = mrconv_ref(u, idx, p["W_upd"], p.get("b_upd"), keys=keys)
     y = linear_ref(gelu_ref(ut), p["W_out"], p.get("b_out")) + x
     h = gelu_ref(linear_ref(y, p["W_1"], p.get("b_1")))
     xn = linear_ref(h, p["W_2"], p.get("b_2")) + y
@@ -306,11 +312,14 @@ def vig_block_ref(x: np.ndarray, idx: np.ndarray, p: dict, return_all: bool = Fa
 
 
 def vig_stack_ref(x0: np.ndarray, params: list, dilations, k: int,
-                  schedule: str = "lookahead", return_all: bool = False):
+                  schedule: str = "lookahead", return_all: bool = False,
+                  H: int | None = None, W: int | None = None, pool_r: int = 1):
     """L full blocks.  Lookahead (Eq. 12 and the bootstrap of Alg. 1): block 0
     uses G(U^0) and block l >= 1 uses G(U^(l-1)); standard (Eq. 6): block l
     uses G(U^l).  Each graph gets the dilation of the block that consumes it.
-    Returns X^L, or (xs, us, graphs) with return_all."""
+    With pool_r > 1 every graph ranks the r x r pooled keys of the U it is
+    built from, and each block's MRConv gathers the keys pooled from its own
+    U.  Returns X^L, or (xs, us, graphs) with return_all."""
     if schedule not in ("lookahead", "standard"):
         raise ValueError(schedule)
     L = len(dilations)
@@ -320,9 +329,10 @@ def vig_stack_ref(x0: np.ndarray, params: list, dilations, k: int,
         u = linear_ref(xs[l], params[l]["W_in"], params[l].get("b_in"))
         us.append(u)
         src = u if (schedule == "standard" or l == 0) else us[l - 1]
-        idx = knn_ref(src, k, dilations[l])
+        keys = pool_keys_ref(src, H, W, pool_r) if pool_r > 1 else None
+        idx = knn_ref(src, k, dilations[l], keys=keys)
         graphs.append(idx)
-        xs.append(vig_block_ref(xs[l], idx, params[l]))
+        xs.append(vig_block_ref(xs[l], idx, params[l], H=H, W=W, pool_r=pool_r))
     if return_all:
         return xs, us, graphs
     return xs[-1]

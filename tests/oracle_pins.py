@@ -525,10 +525,25 @@ def bf_linear(x, W, b=None):
     return out
 
 
-def bf_vig_block(x, idx, p):
+def bf_pool(x, H, W, r):
+    """Pure-Python means over the r x r windows of the row-major H x W grid."""
+    xl = np.asarray(x).tolist()
+    B, C, Wr = len(xl), len(xl[0][0]), W // r
+    out = np.zeros((B, (H // r) * Wr, C))
+    for b in range(B):
+        for p in range(H // r):
+            for q in range(Wr):
+                for c in range(C):
+                    vals = [xl[b][(p * r + u) * W + q * r + v][c] for u in range(r) for v in range(r)]
+                    out[b, p * Wr + q, c] = math.fsum(vals) / (r * r)
+    return out
+
+
+def bf_vig_block(x, idx, p, H=None, W=None, r=1):
     gel = np.vectorize(_bf_gelu)
     u = bf_linear(x, p["W_in"], p.get("b_in"))
-    ut = bf_mrconv(u, idx, p["W_upd"], p.get("b_upd"))
+    keys = bf_pool(u, H, W, r) if r > 1 else None
+    ut = bf_mrconv(u, idx, p["W_upd"], p.get("b_upd"), keys=keys)
     y = bf_linear(gel(ut), p["W_out"], p.get("b_out")) + np.asarray(x)
     h = gel(bf_linear(y, p["W_1"], p.get("b_1")))
     return bf_linear(h, p["W_2"], p.get("b_2")) + y
@@ -631,6 +646,72 @@ def pin_vig_stack_graph_source(ref):
         assert np.array_equal(graphs[l], ref.knn_ref(ul, 3, dil[l]))
 
 
+def pin_vig_block_pooled_bruteforce(ref):
+    """Pyramid stages: the keys are U pooled 2 x 2 on a 4 x 6 grid, and MRConv
+    gathers those pooled rows."""
+    rng = np.random.default_rng(45)
+    H, W, r = 4, 6, 2
+    x = rng.standard_normal((2, H * W, 3))
+    idx = rng.integers(0, 6, (2, H * W, 3))
+    p = _vig_params(rng, 3)
+    got = ref.vig_block_ref(x, idx, p, H=H, W=W, pool_r=r)
+    assert np.allclose(got, bf_vig_block(x, idx, p, H, W, r), atol=1e-10)
+
+
+def pin_vig_block_single_key(ref):
+    """One pooled key (2 x 2 grid, r = 2): m_i = mean(U) - u_i, worked by hand
+    with W_in = I, W_upd = [0 | I], W_out = I, W_1 = 0 and no biases, so
+    X' = X + sigma(mean(X) - X)."""
+    C = 2
+    I2 = np.eye(C)
+    x = np.array([[[1.0, -1.0], [3.0, 0.0], [-1.0, 2.0], [1.0, 3.0]]])   # mean (1, 1)
+    p = {"W_in": I2, "W_upd": np.hstack([np.zeros((C, C)), I2]), "W_out": I2,
+         "W_1": np.zeros((4 * C, C)), "W_2": np.ones((C, 4 * C))}
+    idx = np.zeros((1, 4, 1), dtype=np.int64)
+    g = {0.0: 0.0, 1.0: PHI1, -1.0: -(1 - PHI1), 2.0: 2 * PHI2, -2.0: -2 * (1 - PHI2)}
+    m = np.array([1.0, 1.0]) - x[0]
+    want = x[0] + np.array([[g[v] for v in row] for row in m])
+    got = ref.vig_block_ref(x, idx, p, H=2, W=2, pool_r=2)
+    assert np.allclose(got[0], want, rtol=0, atol=1e-14), got
+
+
+def pin_vig_stack_pooled_graph_source(ref):
+    """Pooled lookahead stack: graph l ranks the keys pooled from its source U
+    (U^0 for blocks 0 and 1, U^(l-1) after), and block l gathers keys pooled
+    from its own U."""
+    rng = np.random.default_rng(46)
+    H, W, r = 4, 4, 2
+    x = rng.standard_normal((1, H * W, 3))
+    ps = [_vig_params(rng, 3) for _ in range(3)]
+    for p in ps:
+        p["W_2"] = p["W_2"] * 0.1
+    dil = (1, 2, 1)
+    xs, us, graphs = ref.vig_stack_ref(x, ps, dil, 2, schedule="lookahead", return_all=True,
+                                       H=H, W=W, pool_r=r)
+    u = [bf_linear(xs[l], ps[l]["W_in"], ps[l]["b_in"]) for l in range(3)]
+    for l, s in enumerate((0, 0, 1)):
+        assert np.array_equal(graphs[l], ref.knn_ref(u[s], 2, dil[l], keys=bf_pool(u[s], H, W, r)))
+    assert np.allclose(xs[3], bf_vig_block(xs[2], graphs[2], ps[2], H, W, r), atol=1e-10)
+
+
+def pin_vig_stack_pooled_all_keys(ref):
+    """k equal to the number of pooled keys (d = 1): every graph row holds all
+    of them, so the max-relative part ignores which U built the graph and the
+    lookahead and standard schedules give the same X^L."""
+    rng = np.random.default_rng(47)
+    H, W, r = 4, 4, 2
+    x = rng.standard_normal((2, H * W, 3))
+    ps = [_vig_params(rng, 3) for _ in range(3)]
+    for p in ps:
+        p["W_2"] = p["W_2"] * 0.1
+    la, _, g = ref.vig_stack_ref(x, ps, (1, 1, 1), 4, schedule="lookahead", return_all=True,
+                                 H=H, W=W, pool_r=r)
+    st = ref.vig_stack_ref(x, ps, (1, 1, 1), 4, schedule="standard", H=H, W=W, pool_r=r)
+    for gl in g:
+        assert np.array_equal(np.sort(gl, axis=-1), np.broadcast_to(np.arange(4), gl.shape))
+    assert np.allclose(la[-1], st, rtol=0, atol=1e-12)
+
+
 # ---------------------------------------------------------------------------
 # inter-stage max pooling pins
 # ---------------------------------------------------------------------------
@@ -691,7 +772,9 @@ PINS = [
     pin_stack_single_layer, pin_stack_identity_weights, pin_stack_circle_two_blocks,
     pin_stack_pooled_graph_source, pin_gelu_closed_form, pin_linear_bruteforce,
     pin_vig_block_bruteforce, pin_vig_block_residual_identity, pin_vig_block_hand,
-    pin_vig_stack_graph_source, pin_mrconv_heads_bruteforce, pin_mrconv_heads_one_head_is_dense,
+    pin_vig_stack_graph_source, pin_vig_block_pooled_bruteforce, pin_vig_block_single_key,
+    pin_vig_stack_pooled_graph_source, pin_vig_stack_pooled_all_keys,
+    pin_mrconv_heads_bruteforce, pin_mrconv_heads_one_head_is_dense,
     pin_mrconv_heads_locality, pin_max_pool_closed_form, pin_max_pool_bruteforce,
     pin_max_pool_dominates_mean, pin_knn_distances_bruteforce, pin_knn_distances_circle,
     pin_dilated_lists_bruteforce, pin_distance_lists_are_knn_ref,

@@ -128,13 +128,16 @@ def _linear_untransposed(x, W, b=None):
 
 
 def _block_factory(fc2_residual=True, ffn_residual="y", gelu_after_wout=False,
-                   drop_b1=False, linear=None):
+                   drop_b1=False, linear=None, pool_from="u"):
     lin = linear or R.linear_ref
 
-    def block(x, idx, p, return_all=False):
+    def block(x, idx, p, return_all=False, H=None, W=None, pool_r=1):
         x = np.asarray(x, dtype=np.float64)
         u = lin(x, p["W_in"], p.get("b_in"))
-        ut = R.mrconv_ref(u, idx, p["W_upd"], p.get("b_upd"))
+        keys = None
+        if pool_r > 1 and pool_from != "none":
+            keys = R.pool_keys_ref(u if pool_from == "u" else x, H, W, pool_r)
+        ut = R.mrconv_ref(u, idx, p["W_upd"], p.get("b_upd"), keys=keys)
         if gelu_after_wout:
             y = R.gelu_ref(lin(ut, p["W_out"], p.get("b_out")))
         else:
@@ -147,10 +150,11 @@ def _block_factory(fc2_residual=True, ffn_residual="y", gelu_after_wout=False,
     return block
 
 
-def _vig_stack_factory(graph_from="u", lag=1, block=None):
+def _vig_stack_factory(graph_from="u", lag=1, block=None, graph_keys="pooled"):
     blk = block or R.vig_block_ref
 
-    def stack(x0, params, dilations, k, schedule="lookahead", return_all=False):
+    def stack(x0, params, dilations, k, schedule="lookahead", return_all=False, H=None,
+              W=None, pool_r=1):
         L = len(dilations)
         xs = [np.asarray(x0, dtype=np.float64)]
         us, graphs = [], []
@@ -159,9 +163,13 @@ def _vig_stack_factory(graph_from="u", lag=1, block=None):
             us.append(u)
             feats = us if graph_from == "u" else xs
             j = l if (schedule == "standard" or l == 0) else max(l - lag, 0)
-            idx = R.knn_ref(feats[j], k, dilations[l])
+            keys = None
+            if pool_r > 1 and graph_keys != "unpooled":
+                # "own": keys pooled from the consuming block's U, not the source's
+                keys = R.pool_keys_ref(us[l] if graph_keys == "own" else feats[j], H, W, pool_r)
+            idx = R.knn_ref(feats[j], k, dilations[l], keys=keys)
             graphs.append(idx)
-            xs.append(blk(xs[l], idx, params[l]))
+            xs.append(blk(xs[l], idx, params[l], H=H, W=W, pool_r=pool_r))
         return (xs, us, graphs) if return_all else xs[-1]
     return stack
 
@@ -253,6 +261,10 @@ MUTANTS = {
     "block_ffn_bias_dropped": dict(vig_block_ref=_block_factory(drop_b1=True)),
     "vig_stack_graph_from_x": dict(vig_stack_ref=_vig_stack_factory(graph_from="x")),
     "vig_stack_no_lookahead": dict(vig_stack_ref=_vig_stack_factory(lag=0)),
+    "block_keys_pooled_from_x": dict(vig_block_ref=_block_factory(pool_from="x")),
+    "block_gathers_unpooled_rows": dict(vig_block_ref=_block_factory(pool_from="none")),
+    "vig_stack_graph_keys_unpooled": dict(vig_stack_ref=_vig_stack_factory(graph_keys="unpooled")),
+    "vig_stack_graph_keys_from_own_u": dict(vig_stack_ref=_vig_stack_factory(graph_keys="own")),
     "heads_m_from_next_head": dict(mrconv_heads_ref=_heads_factory(shift_m=True)),
     "heads_halves_swapped": dict(mrconv_heads_ref=_heads_factory(swap=True)),
     "max_pool_window_shifted": dict(max_pool_nodes_ref=_max_pool_factory(offset=1)),
