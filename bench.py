@@ -200,7 +200,7 @@ def cpu_full_block(w, images: int, blocks: int) -> dict:
     ps = [{n: v.value for n, v in I.make_vig_params(ws, l).items()} for l in range(blocks)]
     with threadpool_limits(1):
         t0 = time.perf_counter()
-        O.vig_stack_ref(x.value, ps, w.dilations[:blocks], w.k)
+        O.vig_stack_ref(x.value, ps, w.dilations[:blocks], w.k, H=w.H, W=w.W, pool_r=w.pool_r)
         dt = time.perf_counter() - t0
     scale = w.B / S
     return {"value": blocks / (dt * scale), "unit": "layers/s", "cores": 1, "kind": "oracle",
@@ -484,13 +484,14 @@ def full_block(args, w, api, I, dev, torch) -> dict:
     params = [{n: dev(v) for n, v in I.make_vig_params(w, l).items()} for l in range(L)]
     s_up = torch.cuda.current_stream()
     la = api.Lookahead(s_up, torch.cuda.Stream())
-    ws = api.vig_workspace(x0, w.k)
+    ws = api.vig_workspace(x0, w.k, w.H, w.W, w.pool_r)
     out = torch.empty_like(x0)
     dil = list(w.dilations)
     steps = max(10, args.steps // 4)
 
     def run(sc):
-        la.vig_stack(x0, params, dil, w.k, schedule=sc, ws=ws, x_out=out)
+        la.vig_stack(x0, params, dil, w.k, schedule=sc, ws=ws, x_out=out, H=w.H, W=w.W,
+                     pool_r=w.pool_r)
 
     def timed(sc, n):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

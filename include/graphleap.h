@@ -364,30 +364,38 @@ typedef struct {
   const void* b_2;    /* [C] */
 } gl_vig_params;
 
-/* Bytes of the workspace gl_vig_block and gl_vig_stack need (they carve
- * sigma-input, Y and the FFN's hidden rows out of it -- the hidden rows'
- * region also serves the two-pass MRConv -- and the stack also U, two
- * feature buffers and two graphs). */
-size_t gl_vig_workspace_bytes(int B, int N, int C, int k, gl_dtype dt);
+/* Bytes of the workspace gl_vig_block and gl_vig_stack need for an H x W
+ * node grid (N = H*W) whose keys are pooled pool_r x pool_r (1: none).  They
+ * carve sigma-input, Y, the FFN's hidden rows (that region also serves the
+ * two-pass MRConv) and the pooled keys of U out of it, and the stack also U,
+ * two feature buffers and two graphs.  0 when the shape is invalid. */
+size_t gl_vig_workspace_bytes(int B, int H, int W, int C, int pool_r, int k, gl_dtype dt);
 
 /* ---------------------------------------------------------------------------
  * gl_vig_block -- one full block on the lookahead handle's streams, given the
  * graph it uses (Alg. 1):
  *   U = x_in W_in^T + b_in -> u_out           (cached for the next graph)
- *   [build idx_next = G(U, dilation_next) on the build stream, overlapping
- *    everything below; skipped when idx_next is NULL]
- *   Ut = MRConv(U; idx_use)  (W_upd, b_upd)
+ *   [pool_r > 1: keys = U pooled pool_r x pool_r over the H x W grid
+ *    (M = (H/pool_r)*(W/pool_r) rows, in ws); else keys = U, M = N]
+ *   [build idx_next = G(U, keys, dilation_next) on the build stream,
+ *    overlapping everything below; skipped when idx_next is NULL]
+ *   Ut = MRConv(U; keys, idx_use)  (W_upd, b_upd)
  *   Y = GELU(Ut) W_out^T + b_out + x_in
  *   x_out = GELU(Y W_1^T + b_1) W_2^T + b_2 + Y
+ * Key pooling is the pyramid stages' (Sec. IV-E), as in gl_graphleap_block.
  * Enqueues on the update stream after waiting for the handle's previous
- * build.  x_in, x_out, u_out [B, N, C]; idx_use, idx_next [B, N, k] int32;
- * ws of at least gl_vig_workspace_bytes().  x_out must not overlap x_in,
- * u_out, ws or the graphs.
+ * build.  x_in, x_out, u_out [B, N, C]; idx_use, idx_next [B, N, k] int32
+ * indexing the M keys; ws of at least gl_vig_workspace_bytes(), 256-byte
+ * aligned.  The build of idx_next reads u_out and the keys in ws; the next
+ * block enqueued through the handle waits for it before it writes either.
+ * x_out must not overlap x_in, u_out, ws or the graphs.
+ * Limits: H % pool_r == 0 and W % pool_r == 0, k <= M; the kNN and MRConv
+ * limits of gl_knn_graph and gl_mrconv.
  * -------------------------------------------------------------------------*/
-gl_status gl_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, int C, int k,
-                       const int32_t* idx_use, const gl_vig_params* p, gl_dtype dt, void* ws,
-                       size_t ws_bytes, void* u_out, int32_t* idx_next, int dilation_next,
-                       void* x_out);
+gl_status gl_vig_block(gl_lookahead_t h, const void* x_in, int B, int H, int W, int C, int pool_r,
+                       int k, const int32_t* idx_use, const gl_vig_params* p, gl_dtype dt,
+                       void* ws, size_t ws_bytes, void* u_out, int32_t* idx_next,
+                       int dilation_next, void* x_out);
 
 /* ---------------------------------------------------------------------------
  * gl_vig_stack -- L full blocks, natively enqueued.
@@ -397,12 +405,16 @@ gl_status gl_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, int C, 
  *   GL_SCHED_LOOKAHEAD_FUSED: the same graphs; one stream, each build in one
  *     launch with its block's MRConv (both read only U^l).
  *   GL_SCHED_STANDARD: Ghat^l = G(U^l, d_l) (Eq. 6), serial.
- * params: L blocks' weights.  x0, x_out [B, N, C]; ws of at least
- * gl_vig_workspace_bytes(); x_out must not overlap x0 or ws.
+ * With pool_r > 1 each graph ranks the keys pooled from the U it is built
+ * from and each MRConv gathers the keys pooled from its own U (as
+ * gl_vig_block).  params: L blocks' weights.  x0, x_out [B, H*W, C]; ws of
+ * at least gl_vig_workspace_bytes(), 256-byte aligned; x_out must not overlap
+ * x0 or ws.  Every block is checked before anything is enqueued.
  * -------------------------------------------------------------------------*/
-gl_status gl_vig_stack(gl_lookahead_t h, const void* x0, int B, int N, int C, int L, int k,
-                       const int* dilations, const gl_vig_params* params, gl_dtype dt,
-                       gl_schedule schedule, void* ws, size_t ws_bytes, void* x_out);
+gl_status gl_vig_stack(gl_lookahead_t h, const void* x0, int B, int H, int W, int C, int pool_r,
+                       int L, int k, const int* dilations, const gl_vig_params* params,
+                       gl_dtype dt, gl_schedule schedule, void* ws, size_t ws_bytes,
+                       void* x_out);
 
 #ifdef __cplusplus
 }

@@ -58,11 +58,11 @@ SIGNATURES = {
     "gl_graphleap_stack": [_vp, _vp, _i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i), _vp, _vp, _i,
                            _i, _vp, _vp, _vp, _vp, _vp, _sz],
     "gl_linear": [_vp, _i, _i, _vp, _vp, _i, _i, _i, _vp, _i, _vp, _vp],
-    "gl_vig_workspace_bytes": [_i, _i, _i, _i, _i],
-    "gl_vig_block": [_vp, _vp, _i, _i, _i, _i, _vp, ctypes.POINTER(VigParams), _i, _vp, _sz, _vp,
-                     _vp, _i, _vp],
-    "gl_vig_stack": [_vp, _vp, _i, _i, _i, _i, _i, ctypes.POINTER(_i), ctypes.POINTER(VigParams),
-                     _i, _i, _vp, _sz, _vp],
+    "gl_vig_workspace_bytes": [_i, _i, _i, _i, _i, _i, _i],
+    "gl_vig_block": [_vp, _vp, _i, _i, _i, _i, _i, _i, _vp, ctypes.POINTER(VigParams), _i, _vp,
+                     _sz, _vp, _vp, _i, _vp],
+    "gl_vig_stack": [_vp, _vp, _i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i),
+                     ctypes.POINTER(VigParams), _i, _i, _vp, _sz, _vp],
     "gl_status_string": [_i],
     "gl_last_error": [],
     "gl_version": [],
@@ -261,9 +261,19 @@ def vig_params(p: dict) -> VigParams:
     return VigParams(*[(p[n].data_ptr() if p.get(n) is not None else None) for n in VIG_PARAMS])
 
 
-def vig_workspace(x0: torch.Tensor, k: int) -> torch.Tensor:
+def _grid(N, H, W):
+    """The node grid (H, W); a plain N-node set is the N x 1 grid."""
+    if H is None:
+        return N, 1
+    if H * W != N:
+        raise GraphLeapError("grid", 2, f"H*W={H * W} != N={N}")
+    return H, W
+
+
+def vig_workspace(x0: torch.Tensor, k: int, H=None, W=None, pool_r: int = 1) -> torch.Tensor:
     B, N, C = x0.shape
-    n = lib().gl_vig_workspace_bytes(B, N, C, k, _dt(x0))
+    H, W = _grid(N, H, W)
+    n = lib().gl_vig_workspace_bytes(B, H, W, C, pool_r, k, _dt(x0))
     if not n:
         raise GraphLeapError("gl_vig_workspace_bytes", 2, "bad shape")
     return torch.empty(n, dtype=torch.uint8, device=x0.device)
@@ -333,30 +343,35 @@ class Lookahead:
         return x_out
 
     def vig_block(self, x_in, idx_use, params: dict, ws, u_out=None, x_out=None, idx_next=None,
-                  dilation_next=1):
-        """One full ViG block; returns (x_out, u_out)."""
+                  dilation_next=1, H=None, W=None, pool_r=1):
+        """One full ViG block; returns (x_out, u_out).  With pool_r > 1 the
+        graphs index U's keys pooled pool_r x pool_r over the H x W grid."""
         B, N, C = x_in.shape
+        H, W = _grid(N, H, W)
         k = idx_use.shape[2]
         x_out = torch.empty_like(x_in) if x_out is None else x_out
         u_out = torch.empty_like(x_in) if u_out is None else u_out
         self._keep(x_in, ws, u_out, idx_use, idx_next)
         pp = vig_params(params)
-        _call("gl_vig_block", self._h, _p(x_in), B, N, C, k, _p(idx_use), ctypes.byref(pp),
-              _dt(x_in), _p(ws), ws.numel(), _p(u_out), _p(idx_next), dilation_next, _p(x_out))
+        _call("gl_vig_block", self._h, _p(x_in), B, H, W, C, pool_r, k, _p(idx_use),
+              ctypes.byref(pp), _dt(x_in), _p(ws), ws.numel(), _p(u_out), _p(idx_next),
+              dilation_next, _p(x_out))
         return x_out, u_out
 
     def vig_stack(self, x0, params: list, dilations, k, schedule=GL_SCHED_LOOKAHEAD_FUSED,
-                  ws=None, x_out=None):
-        """len(dilations) full ViG blocks; params: list of dicts of device tensors."""
+                  ws=None, x_out=None, H=None, W=None, pool_r=1):
+        """len(dilations) full ViG blocks; params: list of dicts of device tensors.
+        With pool_r > 1 keys are pooled pool_r x pool_r over the H x W grid."""
         B, N, C = x0.shape
+        H, W = _grid(N, H, W)
         L = len(dilations)
-        ws = vig_workspace(x0, k) if ws is None else ws
+        ws = vig_workspace(x0, k, H, W, pool_r) if ws is None else ws
         x_out = torch.empty_like(x0) if x_out is None else x_out
         dil = (ctypes.c_int * L)(*dilations)
         arr = (VigParams * L)(*[vig_params(p) for p in params])
         self._keep(x0, ws)
-        _call("gl_vig_stack", self._h, _p(x0), B, N, C, L, k, dil, arr, _dt(x0), schedule, _p(ws),
-              ws.numel(), _p(x_out))
+        _call("gl_vig_stack", self._h, _p(x0), B, H, W, C, pool_r, L, k, dil, arr, _dt(x0),
+              schedule, _p(ws), ws.numel(), _p(x_out))
         return x_out
 
     def stack(self, x0, H, W, Ws, bs, dilations, k, pool_r=1, schedule=GL_SCHED_LOOKAHEAD,

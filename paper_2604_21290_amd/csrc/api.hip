@@ -798,14 +798,16 @@ hipError_t run_linear(const void* x, int R, int K, const void* W, const void* bi
 
 size_t round256(size_t v) { return (v + 255) & ~size_t(255); }
 
-// Workspace carve-up: sigma-input Ut, Y, FFN hidden H (block and stack), then
-// U, two feature buffers and two graphs (stack only).
+// Workspace carve-up: sigma-input Ut, Y, FFN hidden H (block and stack), the
+// pooled keys of U (pyramid stages), then U, two feature buffers and two
+// graphs (stack only).
 struct VigWs {
   char* ut;
   char* y;
   char* hid;
   char* u;
   char* x[2];
+  char* keys;
   int32_t* idx[2];
   size_t bytes;
 };
@@ -826,10 +828,32 @@ VigWs vig_ws(void* base, int B, int N, int C, int k, gl_dtype dt) {
   w.u = p + 6 * fb;
   w.x[0] = p + 7 * fb;
   w.x[1] = p + 8 * fb;
+  w.keys = p + 9 * fb;    // [B, M, C], M <= N
   w.idx[0] = reinterpret_cast<int32_t*>(p + 10 * fb);
   w.idx[1] = reinterpret_cast<int32_t*>(p + 10 * fb + ib);
   w.bytes = vig_ws_bytes(B, N, C, k, dt);
   return w;
+}
+
+// The node grid of a full block: N = H*W queries; with r > 1 the graph and
+// MRConv use the M = (H/r)*(W/r) keys pooled from U, else M = N and keys = U.
+struct VigGrid {
+  int B, H, W, C, r;
+  int N() const { return H * W; }
+  int M() const { return r > 1 ? (H / r) * (W / r) : H * W; }
+  bool pooled() const { return r > 1; }
+};
+
+bool grid_ok(const VigGrid& g, int k, gl_dtype dt) {
+  return g.B >= 1 && g.H >= 1 && g.W >= 1 && g.C >= 1 && g.r >= 1 && k >= 1 && dtype_ok(dt) &&
+         g.H % g.r == 0 && g.W % g.r == 0 && size_ok(g.B, (long long)g.H * g.W, g.C);
+}
+
+gl_status check_grid(const char* who, const VigGrid& g, int k, gl_dtype dt) {
+  if (!grid_ok(g, k, dt))
+    return fail(GL_ERR_BAD_SHAPE, "%s: bad shape B=%d H=%d W=%d C=%d pool_r=%d k=%d", who, g.B,
+                g.H, g.W, g.C, g.r, k);
+  return GL_OK;
 }
 
 gl_status check_vig_params(const gl_vig_params* p, int C, gl_dtype dt) {
@@ -847,13 +871,15 @@ gl_status check_vig_params(const gl_vig_params* p, int C, gl_dtype dt) {
   return GL_OK;
 }
 
-// One full block on the handle's streams.  u holds U^l (computed here unless
-// u_ready); idx_next (if any) receives G(U^l, dil_next).
-gl_status enqueue_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, int C, int k,
+// One full block on the handle's streams.  u holds U^l (computed here, and
+// pooled into w.keys at pyramid stages, unless u_ready); idx_next (if any)
+// receives G(U^l, dil_next).
+gl_status enqueue_vig_block(gl_lookahead_t h, const void* x_in, const VigGrid& g, int k,
                             const int32_t* idx_use, const gl_vig_params& p, gl_dtype dt,
                             const VigWs& w, void* u, bool u_ready, int32_t* idx_next,
                             int dil_next, gl_schedule schedule, int rt, void* x_out) {
-  const int R = B * N, dtb = dt == GL_BF16;
+  const int B = g.B, N = g.N(), M = g.M(), C = g.C, R = B * N, dtb = dt == GL_BF16;
+  const void* keys = g.pooled() ? static_cast<const void*>(w.keys) : u;
   gl_status s;
   auto lin = [&](const char* what, const void* xi, int K, const void* W, const void* b, int Co,
                  int ai, int ao, const void* res, void* o) {
@@ -862,16 +888,22 @@ gl_status enqueue_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, in
     });
   };
   if (schedule == GL_SCHED_LOOKAHEAD && (s = join_build(h)) != GL_OK) return s;
-  if (!u_ready && (s = lin("linear launch (FC1)", x_in, C, p.W_in, p.b_in, C, 0, 0, nullptr, u)) != GL_OK)
-    return s;
+  if (!u_ready) {
+    if ((s = lin("linear launch (FC1)", x_in, C, p.W_in, p.b_in, C, 0, 0, nullptr, u)) != GL_OK)
+      return s;
+    if (g.pooled()) {
+      hipError_t e = gl::launch_pool(u, w.keys, B, g.H, g.W, C, g.r, dtb, h->su);
+      if (e != hipSuccess) return hip_fail(e, "pool launch");
+    }
+  }
   // the two-pass MRConv's [x | m] rows go to the FFN's hidden-row region,
   // which is free until FFN1 (later on the same stream) overwrites it
   void* mws = block_ws(B, N, C, k, dt, rt, w.hid);
   const bool fused = schedule == GL_SCHED_LOOKAHEAD_FUSED && idx_next &&
-                     !gl::knn_separate(N, C, dtb) && !mws;
+                     !gl::knn_separate(M, C, dtb) && !mws;
   if (fused) {
-    const gl::KnnArgs ka = gl::make_knn_args(u, u, B, N, C, N, k, dil_next, idx_next);
-    const gl::MrArgs ma = gl::make_mr_args(u, u, idx_use, p.W_upd, p.b_upd, w.ut, B, N, N, C, C, k);
+    const gl::KnnArgs ka = gl::make_knn_args(u, keys, B, N, C, M, k, dil_next, idx_next);
+    const gl::MrArgs ma = gl::make_mr_args(u, keys, idx_use, p.W_upd, p.b_upd, w.ut, B, N, M, C, C, k);
     s = timed_launch(h, GL_TIME_FUSED, "block launch", [&](hipEvent_t e0, hipEvent_t e1) {
       return gl::launch_block(ka, ma, dtb, rt, h->su, e0, e1);
     });
@@ -880,18 +912,19 @@ gl_status enqueue_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, in
     if (idx_next) {
       if (schedule == GL_SCHED_LOOKAHEAD) {
         if ((s = fork_build(h)) != GL_OK) return s;
-        if ((s = enqueue_build(h, u, B, N, C, nullptr, N, k, dil_next, dt, idx_next)) != GL_OK)
+        if ((s = enqueue_build(h, u, B, N, C, g.pooled() ? w.keys : nullptr, M, k, dil_next, dt,
+                               idx_next)) != GL_OK)
           return s;
         if ((s = mark_built(h)) != GL_OK) return s;
       } else {
         s = timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
-          return gl::launch_knn(u, u, B, N, C, N, k, dil_next, dtb, idx_next, h->su, e0, e1);
+          return gl::launch_knn(u, keys, B, N, C, M, k, dil_next, dtb, idx_next, h->su, e0, e1);
         });
         if (s != GL_OK) return s;
       }
     }
     s = timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {
-      return gl::launch_mrconv(u, u, idx_use, p.W_upd, p.b_upd, w.ut, B, N, N, C, C, k, dtb, rt,
+      return gl::launch_mrconv(u, keys, idx_use, p.W_upd, p.b_upd, w.ut, B, N, M, C, C, k, dtb, rt,
                                mws, h->su, e0, e1);
     });
     if (s != GL_OK) return s;
@@ -916,33 +949,38 @@ gl_status gl_linear(const void* x, int R, int K, const void* W, const void* bias
   return e == hipSuccess ? GL_OK : hip_fail(e, "linear launch");
 }
 
-size_t gl_vig_workspace_bytes(int B, int N, int C, int k, gl_dtype dt) {
-  if (B < 1 || N < 1 || C < 1 || k < 1 || !dtype_ok(dt)) return 0;
-  return vig_ws_bytes(B, N, C, k, dt);
+size_t gl_vig_workspace_bytes(int B, int H, int W, int C, int pool_r, int k, gl_dtype dt) {
+  const VigGrid g{B, H, W, C, pool_r};
+  return grid_ok(g, k, dt) ? vig_ws_bytes(B, g.N(), C, k, dt) : 0;
 }
 
-gl_status gl_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, int C, int k,
-                       const int32_t* idx_use, const gl_vig_params* p, gl_dtype dt, void* ws,
-                       size_t ws_bytes, void* u_out, int32_t* idx_next, int dilation_next,
-                       void* x_out) {
+gl_status gl_vig_block(gl_lookahead_t h, const void* x_in, int B, int H, int W, int C, int pool_r,
+                       int k, const int32_t* idx_use, const gl_vig_params* p, gl_dtype dt,
+                       void* ws, size_t ws_bytes, void* u_out, int32_t* idx_next,
+                       int dilation_next, void* x_out) {
   if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "vig_block: bad handle");
+  const VigGrid g{B, H, W, C, pool_r};
   gl_status s;
+  if ((s = check_grid("vig_block", g, k, dt)) != GL_OK) return s;
   if ((s = check_vig_params(p, C, dt)) != GL_OK) return s;
   if (!x_in || !idx_use || !ws || !u_out || !x_out)
     return fail(GL_ERR_NULL_PTR, "vig_block: x_in, idx_use, ws, u_out and x_out are required");
-  int rt = 0;
-  // shapes of every layer: FC1 [C->C], MRConv [2C->C], FC2 [C->C], FFN [C->4C->C]
-  if ((s = check_mrconv(u_out, B, N, C, nullptr, N, idx_use, k, p->W_upd, p->b_upd, C, dt, x_out,
-                        &rt)) != GL_OK)
-    return s;
-  if (idx_next && (s = check_knn(u_out, B, N, C, nullptr, N, k, dilation_next, dt, idx_next)) != GL_OK)
-    return s;
+  const int N = g.N(), M = g.M();
   const VigWs w = vig_ws(ws, B, N, C, k, dt);
   if (ws_bytes < w.bytes)
     return fail(GL_ERR_BAD_SHAPE, "vig_block: ws_bytes=%zu < %zu", ws_bytes, w.bytes);
-  const size_t xb = (size_t)B * N * C * esize(dt), ib = (size_t)B * N * k * 4;
   if (!aligned(x_in, 16) || !aligned(u_out, 16) || !aligned(ws, 256) || !aligned(x_out, 16))
     return fail(GL_ERR_ALIGNMENT, "vig_block: x_in, u_out, x_out need 16 bytes, ws 256");
+  const void* keys = g.pooled() ? w.keys : nullptr;
+  int rt = 0;
+  // shapes of every layer: FC1 [C->C], MRConv [2C->C], FC2 [C->C], FFN [C->4C->C]
+  if (g.pooled() && (s = check_pool(u_out, B, H, W, C, pool_r, dt, w.keys)) != GL_OK) return s;
+  if ((s = check_mrconv(u_out, B, N, C, keys, M, idx_use, k, p->W_upd, p->b_upd, C, dt, x_out,
+                        &rt)) != GL_OK)
+    return s;
+  if (idx_next && (s = check_knn(u_out, B, N, C, keys, M, k, dilation_next, dt, idx_next)) != GL_OK)
+    return s;
+  const size_t xb = (size_t)B * N * C * esize(dt), ib = (size_t)B * N * k * 4;
   if (overlap(x_out, xb, x_in, xb) || overlap(x_out, xb, u_out, xb) ||
       overlap(x_out, xb, ws, ws_bytes) || overlap(x_out, xb, idx_use, ib) ||
       overlap(x_out, xb, idx_next, idx_next ? ib : 0) || overlap(u_out, xb, x_in, xb) ||
@@ -950,13 +988,14 @@ gl_status gl_vig_block(gl_lookahead_t h, const void* x_in, int B, int N, int C, 
       overlap(idx_use, ib, ws, ws_bytes) || overlap(idx_next, idx_next ? ib : 0, ws, ws_bytes) ||
       overlap(idx_next, idx_next ? ib : 0, idx_use, ib))
     return fail(GL_ERR_ALIAS, "vig_block: buffers overlap");
-  return enqueue_vig_block(h, x_in, B, N, C, k, idx_use, *p, dt, w, u_out, false, idx_next,
+  return enqueue_vig_block(h, x_in, g, k, idx_use, *p, dt, w, u_out, false, idx_next,
                            dilation_next, GL_SCHED_LOOKAHEAD, rt, x_out);
 }
 
-gl_status gl_vig_stack(gl_lookahead_t h, const void* x0, int B, int N, int C, int L, int k,
-                       const int* dilations, const gl_vig_params* params, gl_dtype dt,
-                       gl_schedule schedule, void* ws, size_t ws_bytes, void* x_out) {
+gl_status gl_vig_stack(gl_lookahead_t h, const void* x0, int B, int H, int W, int C, int pool_r,
+                       int L, int k, const int* dilations, const gl_vig_params* params,
+                       gl_dtype dt, gl_schedule schedule, void* ws, size_t ws_bytes,
+                       void* x_out) {
   if (!handle_ok(h)) return fail(GL_ERR_BAD_HANDLE, "vig_stack: bad handle");
   if (!x0 || !dilations || !params || !ws || !x_out)
     return fail(GL_ERR_NULL_PTR, "vig_stack: x0, dilations, params, ws and x_out are required");
@@ -964,6 +1003,10 @@ gl_status gl_vig_stack(gl_lookahead_t h, const void* x0, int B, int N, int C, in
   if (schedule != GL_SCHED_LOOKAHEAD && schedule != GL_SCHED_STANDARD &&
       schedule != GL_SCHED_LOOKAHEAD_FUSED)
     return fail(GL_ERR_UNSUPPORTED, "vig_stack: schedule=%d", (int)schedule);
+  const VigGrid g{B, H, W, C, pool_r};
+  gl_status s;
+  if ((s = check_grid("vig_stack", g, k, dt)) != GL_OK) return s;
+  const int N = g.N(), M = g.M();
   const VigWs w = vig_ws(ws, B, N, C, k, dt);
   if (ws_bytes < w.bytes)
     return fail(GL_ERR_BAD_SHAPE, "vig_stack: ws_bytes=%zu < %zu", ws_bytes, w.bytes);
@@ -972,47 +1015,50 @@ gl_status gl_vig_stack(gl_lookahead_t h, const void* x0, int B, int N, int C, in
   const size_t xb = (size_t)B * N * C * esize(dt);
   if (overlap(x_out, xb, x0, xb) || overlap(x_out, xb, ws, ws_bytes) || overlap(x0, xb, ws, ws_bytes))
     return fail(GL_ERR_ALIAS, "vig_stack: x_out, x0 and ws must not overlap");
-  gl_status s;
+  const void* keys = g.pooled() ? static_cast<const void*>(w.keys) : w.u;
+  const void* keys_arg = g.pooled() ? w.keys : nullptr;
   int rt = 0;
+  if (g.pooled() && (s = check_pool(w.u, B, H, W, C, pool_r, dt, w.keys)) != GL_OK) return s;
   for (int l = 0; l < L; ++l) {
     if ((s = check_vig_params(&params[l], C, dt)) != GL_OK) return s;
-    if ((s = check_knn(w.u, B, N, C, nullptr, N, k, dilations[l], dt, w.idx[0])) != GL_OK) return s;
-    if ((s = check_mrconv(w.u, B, N, C, nullptr, N, w.idx[0], k, params[l].W_upd, params[l].b_upd,
+    if ((s = check_knn(w.u, B, N, C, keys_arg, M, k, dilations[l], dt, w.idx[0])) != GL_OK) return s;
+    if ((s = check_mrconv(w.u, B, N, C, keys_arg, M, w.idx[0], k, params[l].W_upd, params[l].b_upd,
                           C, dt, w.ut, &rt)) != GL_OK)
       return s;
   }
   const int dtb = dt == GL_BF16;
+  // U^l = FC1(X^l) into w.u, pooled into w.keys at pyramid stages
+  auto project = [&](const void* xi, int l) -> gl_status {
+    gl_status st = timed_launch(h, GL_TIME_LINEAR, "linear launch (FC1)",
+                                [&](hipEvent_t e0, hipEvent_t e1) {
+      return run_linear(xi, B * N, C, params[l].W_in, params[l].b_in, C, 0, 0, nullptr, dt, w.u,
+                        h->su, e0, e1);
+    });
+    if (st != GL_OK || !g.pooled()) return st;
+    hipError_t e = gl::launch_pool(w.u, w.keys, B, H, W, C, pool_r, dtb, h->su);
+    return e == hipSuccess ? GL_OK : hip_fail(e, "pool launch");
+  };
+  auto build = [&](int dil, int32_t* idx) {
+    return timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
+      return gl::launch_knn(w.u, keys, B, N, C, M, k, dil, dtb, idx, h->su, e0, e1);
+    });
+  };
   if ((s = join_build(h)) != GL_OK) return s;
   if (schedule == GL_SCHED_STANDARD) {
     for (int l = 0; l < L; ++l) {
       const void* xi = l == 0 ? x0 : w.x[(l - 1) & 1];
       void* xo = l == L - 1 ? x_out : w.x[l & 1];
-      if ((s = timed_launch(h, GL_TIME_LINEAR, "linear launch (FC1)", [&](hipEvent_t e0, hipEvent_t e1) {
-             return run_linear(xi, B * N, C, params[l].W_in, params[l].b_in, C, 0, 0, nullptr, dt,
-                               w.u, h->su, e0, e1);
-           })) != GL_OK)
-        return s;
-      if ((s = timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
-             return gl::launch_knn(w.u, w.u, B, N, C, N, k, dilations[l], dtb, w.idx[0], h->su, e0,
-                                   e1);
-           })) != GL_OK)
-        return s;
-      if ((s = enqueue_vig_block(h, xi, B, N, C, k, w.idx[0], params[l], dt, w, w.u, true, nullptr,
-                                 0, schedule, rt, xo)) != GL_OK)
+      if ((s = project(xi, l)) != GL_OK) return s;
+      if ((s = build(dilations[l], w.idx[0])) != GL_OK) return s;
+      if ((s = enqueue_vig_block(h, xi, g, k, w.idx[0], params[l], dt, w, w.u, true, nullptr, 0,
+                                 schedule, rt, xo)) != GL_OK)
         return s;
     }
     return GL_OK;
   }
   // lookahead: U^0, then Ghat^0 = G(U^0, d_0)
-  if ((s = timed_launch(h, GL_TIME_LINEAR, "linear launch (FC1)", [&](hipEvent_t e0, hipEvent_t e1) {
-         return run_linear(x0, B * N, C, params[0].W_in, params[0].b_in, C, 0, 0, nullptr, dt, w.u,
-                           h->su, e0, e1);
-       })) != GL_OK)
-    return s;
-  if ((s = timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
-         return gl::launch_knn(w.u, w.u, B, N, C, N, k, dilations[0], dtb, w.idx[0], h->su, e0, e1);
-       })) != GL_OK)
-    return s;
+  if ((s = project(x0, 0)) != GL_OK) return s;
+  if ((s = build(dilations[0], w.idx[0])) != GL_OK) return s;
   int cur = 0;
   for (int l = 0; l < L; ++l) {
     const void* xi = l == 0 ? x0 : w.x[(l - 1) & 1];
@@ -1023,8 +1069,8 @@ gl_status gl_vig_stack(gl_lookahead_t h, const void* x0, int B, int N, int C, in
       next = 1 - cur;
       idx_next = w.idx[next];
     }
-    if ((s = enqueue_vig_block(h, xi, B, N, C, k, w.idx[cur], params[l], dt, w, w.u, l == 0,
-                               idx_next, idx_next ? dilations[l + 1] : 0, schedule, rt, xo)) != GL_OK)
+    if ((s = enqueue_vig_block(h, xi, g, k, w.idx[cur], params[l], dt, w, w.u, l == 0, idx_next,
+                               idx_next ? dilations[l + 1] : 0, schedule, rt, xo)) != GL_OK)
       return s;
     cur = next;
   }

@@ -223,11 +223,20 @@ def test_linear_validation():
 @host_only
 def test_vig_validation():
     L = api.lib()
-    assert L.gl_vig_workspace_bytes(2, 196, 192, 9, 1) > 0
-    assert L.gl_vig_workspace_bytes(0, 196, 192, 9, 1) == 0
+    n = L.gl_vig_workspace_bytes(2, 14, 14, 192, 1, 9, 1)
+    assert n > 0
+    assert L.gl_vig_workspace_bytes(2, 196, 1, 192, 1, 9, 1) == n     # same N, same carve-up
+    assert L.gl_vig_workspace_bytes(2, 14, 14, 192, 2, 9, 1) == n     # keys fit its own region
+    assert L.gl_vig_workspace_bytes(0, 14, 14, 192, 1, 9, 1) == 0
+    assert L.gl_vig_workspace_bytes(2, 14, 14, 192, 3, 9, 1) == 0     # 3 does not divide 14
+    assert L.gl_vig_workspace_bytes(2, 14, 14, 192, 0, 9, 1) == 0
+    assert L.gl_vig_workspace_bytes(2, 14, 14, 192, 1, 0, 1) == 0
     pp = api.VigParams()
-    st = L.gl_vig_stack(None, P(0), 2, 196, 192, 2, 9, (ctypes.c_int * 2)(1, 1),
+    st = L.gl_vig_stack(None, P(0), 2, 14, 14, 192, 1, 2, 9, (ctypes.c_int * 2)(1, 1),
                         ctypes.byref(pp), 1, 2, P(5), 1 << 30, P(9))
+    assert api.STATUS[st] == "GL_ERR_BAD_HANDLE"
+    st = L.gl_vig_block(None, P(0), 2, 14, 14, 192, 2, 9, P(10), ctypes.byref(pp), 1, P(5),
+                        1 << 30, P(7), None, 1, P(9))
     assert api.STATUS[st] == "GL_ERR_BAD_HANDLE"
 
 

@@ -5,6 +5,8 @@ Blocks are teacher-forced: each block's projected features U, the graph built
 from them and its output are checked against the oracle evaluated on the exact
 stored tensors the GPU saw; the stack entry must then reproduce the
 block-by-block run bit for bit."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -90,9 +92,20 @@ def test_linear_residual_in_place():
 
 
 # -- full blocks ------------------------------------------------------------------
+# pyramid stages run three blocks with dilations (1, 2, 1), so that both graphs
+# built inside blocks (from U^0 with d = 2, from U^1 with d = 1) rank pooled keys
+PYR_DIL = (1, 2, 1)
+
+
 def _workload(name, B):
     w = I.with_batch(I.WORKLOADS[name], B)
+    if w.pool_r > 1:
+        w = dataclasses.replace(w, dilations=PYR_DIL)
     return w
+
+
+def _grid(w):
+    return dict(H=w.H, W=w.W, pool_r=w.pool_r)
 
 
 def _run_blocks(w, L, x0d, params_d, same_stream=False):
@@ -102,10 +115,11 @@ def _run_blocks(w, L, x0d, params_d, same_stream=False):
     dil = w.dilations
     s_up = torch.cuda.current_stream()
     la = api.Lookahead(s_up, s_up if same_stream else torch.cuda.Stream())
-    ws = api.vig_workspace(x0d, w.k)
+    ws = api.vig_workspace(x0d, w.k, **_grid(w))
     bufs = [torch.empty((B, N, w.k), dtype=torch.int32, device="cuda") for _ in range(2)]
     u0 = api.linear(x0d, params_d[0]["W_in"], params_d[0].get("b_in"))
-    api.knn_graph(u0, w.k, dil[0], out=bufs[0])
+    keys0 = api.pool_keys(u0, w.H, w.W, w.pool_r) if w.pool_r > 1 else None
+    api.knn_graph(u0, w.k, dil[0], keys=keys0, out=bufs[0])
     xs, us, graphs, cur = [x0d], [], [], 0
     for l in range(L):
         idx_next, nxt = None, cur
@@ -115,7 +129,8 @@ def _run_blocks(w, L, x0d, params_d, same_stream=False):
         torch.cuda.synchronize()
         graphs.append(bufs[cur].clone())
         x_out, u_out = la.vig_block(xs[-1], bufs[cur], params_d[l], ws, idx_next=idx_next,
-                                    dilation_next=dil[l + 1] if idx_next is not None else 1)
+                                    dilation_next=dil[l + 1] if idx_next is not None else 1,
+                                    **_grid(w))
         torch.cuda.synchronize()
         us.append(u_out.clone())
         xs.append(x_out)
@@ -125,9 +140,11 @@ def _run_blocks(w, L, x0d, params_d, same_stream=False):
     return xs, us, graphs
 
 
-@pytest.mark.parametrize("name,B,L", [("vig_ti", 4, 6), ("vig_b", 2, 5), ("single", 1, 1)])
+@pytest.mark.parametrize("name,B,L", [("vig_ti", 4, 6), ("vig_b", 2, 5), ("single", 1, 1),
+                                      ("pyr_s1", 2, 3), ("pyr_s2", 2, 3)])
 def test_vig_blocks_teacher_forced(name, B, L):
     require_gpu()
+    from paper_2604_21290_amd import api
     w = _workload(name, B)
     x0 = I.make_features(w)
     ps = [I.make_vig_params(w, l) for l in range(L)]
@@ -142,16 +159,24 @@ def test_vig_blocks_teacher_forced(name, B, L):
         check_close(hu[l], O.linear_ref(hx[l], ph[l]["W_in"], ph[l]["b_in"]), w.dtype,
                     f"{name} U^{l}")
         # the graph used by block l: G(U^0) for l <= 1, else G(U^(l-1)), on stored U
-        src = hu[0] if l == 0 else hu[l - 1]
+        # and, at pyramid stages, on the stored keys pooled from it
+        s_l = 0 if l == 0 else l - 1
+        src = hu[s_l]
+        keys = None
+        if w.pool_r > 1:
+            keys = from_dev(api.pool_keys(us[s_l], w.H, w.W, w.pool_r)).value
+            check_close(keys, O.pool_keys_ref(src, w.H, w.W, w.pool_r), w.dtype,
+                        f"{name} keys of U^{s_l}")
         g = graphs[l].cpu().numpy()
-        check_idx(g, O.knn_distances(src), w.k, w.dilations[l], label=f"{name} graph {l}")
+        check_idx(g, O.knn_distances(src, keys), w.k, w.dilations[l], label=f"{name} graph {l}")
         # X^(l+1) from the stored X^l and the GPU's graph
-        ref = O.vig_block_ref(hx[l], g, ph[l])
+        ref = O.vig_block_ref(hx[l], g, ph[l], **_grid(w))
         rel = check_close(hx[l + 1], ref, w.dtype, f"{name} block {l}")
         _say(name, "block", l, "rel", rel)
 
 
-@pytest.mark.parametrize("name,B,L", [("vig_ti", 4, 6), ("vig_b", 2, 5)])
+@pytest.mark.parametrize("name,B,L", [("vig_ti", 4, 6), ("vig_b", 2, 5), ("pyr_s1", 2, 3),
+                                      ("pyr_s2", 2, 3)])
 def test_vig_stack_matches_blocks(name, B, L):
     require_gpu()
     from paper_2604_21290_amd import api
@@ -164,49 +189,54 @@ def test_vig_stack_matches_blocks(name, B, L):
     outs = {}
     for name_s, sc in (("fused", api.GL_SCHED_LOOKAHEAD_FUSED), ("two_stream", api.GL_SCHED_LOOKAHEAD)):
         _say("vig stack", name, name_s)
-        outs[name_s] = la.vig_stack(x0d, pd, dil, w.k, schedule=sc)
+        outs[name_s] = la.vig_stack(x0d, pd, dil, w.k, schedule=sc, **_grid(w))
     torch.cuda.synchronize()
     la.close()
     for k_, v in outs.items():
         assert torch.equal(v, xs[-1]), f"{name}: stack ({k_}) differs from block-by-block"
 
 
-def test_vig_standard_schedule_teacher_forced():
+@pytest.mark.parametrize("name", ["vig_ti", "pyr_s2"])
+def test_vig_standard_schedule_teacher_forced(name):
     require_gpu()
     from paper_2604_21290_amd import api
-    w = _workload("vig_ti", 2)
+    w = _workload(name, 2)
     L = 3
     x0d = to_dev(I.make_features(w))
     ps = [I.make_vig_params(w, l) for l in range(L)]
     pd = [_dev_params(p) for p in ps]
     dil = list(w.dilations[:L])
     la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.current_stream())
-    ws = api.vig_workspace(x0d, w.k)
-    # block by block: graph from this block's own U
+    ws = api.vig_workspace(x0d, w.k, **_grid(w))
+    # block by block: graph from this block's own U (and its pooled keys)
     xs = [x0d]
     for l in range(L):
         u = api.linear(xs[-1], pd[l]["W_in"], pd[l]["b_in"])
-        idx = api.knn_graph(u, w.k, dil[l])
-        x_out, u_out = la.vig_block(xs[-1], idx, pd[l], ws)
+        keys = api.pool_keys(u, w.H, w.W, w.pool_r) if w.pool_r > 1 else None
+        idx = api.knn_graph(u, w.k, dil[l], keys=keys)
+        x_out, u_out = la.vig_block(xs[-1], idx, pd[l], ws, **_grid(w))
         torch.cuda.synchronize()
         assert torch.equal(u, u_out)
-        ref = O.vig_block_ref(from_dev(xs[-1]).value, idx.cpu().numpy(), _host_params(ps[l]))
-        check_close(from_dev(x_out).value, ref, w.dtype, f"standard block {l}")
-        check_idx(idx.cpu().numpy(), O.knn_distances(from_dev(u).value), w.k, dil[l],
-                  label=f"standard graph {l}")
+        ref = O.vig_block_ref(from_dev(xs[-1]).value, idx.cpu().numpy(), _host_params(ps[l]),
+                              **_grid(w))
+        check_close(from_dev(x_out).value, ref, w.dtype, f"{name} standard block {l}")
+        check_idx(idx.cpu().numpy(),
+                  O.knn_distances(from_dev(u).value, None if keys is None else from_dev(keys).value),
+                  w.k, dil[l], label=f"{name} standard graph {l}")
         xs.append(x_out)
-    st = la.vig_stack(x0d, pd, dil, w.k, schedule=api.GL_SCHED_STANDARD)
+    st = la.vig_stack(x0d, pd, dil, w.k, schedule=api.GL_SCHED_STANDARD, **_grid(w))
     torch.cuda.synchronize()
     la.close()
     assert torch.equal(st, xs[-1])
 
 
-def test_vig_zero_branches_are_identity():
+@pytest.mark.parametrize("name", ["vig_ti", "pyr_s2"])
+def test_vig_zero_branches_are_identity(name):
     """W_out = 0 and W_2 = 0, no biases: every schedule returns X^0 bit for bit."""
     require_gpu()
     from paper_2604_21290_amd import api
-    w = _workload("vig_ti", 2)
-    L = 4
+    w = _workload(name, 2)
+    L = min(4, w.L)
     x0d = to_dev(I.make_features(w))
     pd = []
     for l in range(L):
@@ -216,7 +246,7 @@ def test_vig_zero_branches_are_identity():
         pd.append(p)
     la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
     for sc in (api.GL_SCHED_LOOKAHEAD_FUSED, api.GL_SCHED_LOOKAHEAD, api.GL_SCHED_STANDARD):
-        out = la.vig_stack(x0d, pd, list(w.dilations[:L]), w.k, schedule=sc)
+        out = la.vig_stack(x0d, pd, list(w.dilations[:L]), w.k, schedule=sc, **_grid(w))
         torch.cuda.synchronize()
         assert torch.equal(out, x0d), sc
     la.close()
