@@ -529,11 +529,14 @@ def full_block(args, w, api, I, dev, torch) -> dict:
     la.close()
     # algorithmic flop per layer: Gram + MRConv FC + FC1 + FC2 + FFN (C -> 4C -> C)
     flops = 2.0 * B * N * w.M * C + 2.0 * B * N * C * (2 * C + C + C + 8 * C)
-    best = res["fused"]
+    # the fastest schedule (the same arithmetic and graphs in each); the
+    # kernel records above are the fused schedule's
+    name = max(res, key=lambda n: res[n]["layers_per_s"])
+    best = res[name]
     peak = PEAK_TFLOPS[w.dtype]
     tf = flops / (best["ms_per_step"] / L * 1e-3) / 1e12
     return {"layers_per_s": best["layers_per_s"], "ms_per_step": best["ms_per_step"],
-            "schedule": "fused", "schedules": res, "kernels": kern,
+            "schedule": name, "schedules": res, "kernels": kern,
             "flop_per_layer": flops, "tflops": tf, "mfma_frac": tf / peak,
             "entry": "gl_vig_stack"}
 
