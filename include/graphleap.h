@@ -366,7 +366,7 @@ typedef struct {
 
 /* Bytes of the workspace gl_vig_block and gl_vig_stack need for an H x W
  * node grid (N = H*W) whose keys are pooled pool_r x pool_r (1: none).  They
- * carve sigma-input, Y, the FFN's hidden rows (that region also serves the
+ * carve sigma(U~), Y, the FFN's hidden rows (that region also serves the
  * two-pass MRConv) and the pooled keys of U out of it, and the stack also U,
  * two feature buffers and two graphs.  0 when the shape is invalid. */
 size_t gl_vig_workspace_bytes(int B, int H, int W, int C, int pool_r, int k, gl_dtype dt);
@@ -382,6 +382,8 @@ size_t gl_vig_workspace_bytes(int B, int H, int W, int C, int pool_r, int k, gl_
  *   Ut = MRConv(U; keys, idx_use)  (W_upd, b_upd)
  *   Y = GELU(Ut) W_out^T + b_out + x_in
  *   x_out = GELU(Y W_1^T + b_1) W_2^T + b_2 + Y
+ * Every GELU is taken in fp32 before its output is rounded to dt: MRConv
+ * stores GELU(Ut), FFN1 stores GELU(Y W_1^T + b_1).
  * Key pooling is the pyramid stages' (Sec. IV-E), as in gl_graphleap_block.
  * Enqueues on the update stream after waiting for the handle's previous
  * build.  x_in, x_out, u_out [B, N, C]; idx_use, idx_next [B, N, k] int32

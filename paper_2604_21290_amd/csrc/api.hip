@@ -798,7 +798,7 @@ hipError_t run_linear(const void* x, int R, int K, const void* W, const void* bi
 
 size_t round256(size_t v) { return (v + 255) & ~size_t(255); }
 
-// Workspace carve-up: sigma-input Ut, Y, FFN hidden H (block and stack), the
+// Workspace carve-up: sigma(Ut) (MRConv's output), Y, FFN hidden H (block and stack), the
 // pooled keys of U (pyramid stages), then U, two feature buffers and two
 // graphs (stack only).
 struct VigWs {
@@ -901,9 +901,13 @@ gl_status enqueue_vig_block(gl_lookahead_t h, const void* x_in, const VigGrid& g
   void* mws = block_ws(B, N, C, k, dt, rt, w.hid);
   const bool fused = schedule == GL_SCHED_LOOKAHEAD_FUSED && idx_next &&
                      !gl::knn_separate(M, C, dtb) && !mws;
+  // MRConv writes sigma(U~) (GELU before its one rounding): FC2 is its only
+  // reader, so the GELU is paid once per element instead of once per FC2
+  // output-column tile
+  gl::MrArgs ma = gl::make_mr_args(u, keys, idx_use, p.W_upd, p.b_upd, w.ut, B, N, M, C, C, k);
+  ma.act_out = 1;
   if (fused) {
     const gl::KnnArgs ka = gl::make_knn_args(u, keys, B, N, C, M, k, dil_next, idx_next);
-    const gl::MrArgs ma = gl::make_mr_args(u, keys, idx_use, p.W_upd, p.b_upd, w.ut, B, N, M, C, C, k);
     s = timed_launch(h, GL_TIME_FUSED, "block launch", [&](hipEvent_t e0, hipEvent_t e1) {
       return gl::launch_block(ka, ma, dtb, rt, h->su, e0, e1);
     });
@@ -924,12 +928,11 @@ gl_status enqueue_vig_block(gl_lookahead_t h, const void* x_in, const VigGrid& g
       }
     }
     s = timed_launch(h, GL_TIME_UPDATE, "mrconv launch", [&](hipEvent_t e0, hipEvent_t e1) {
-      return gl::launch_mrconv(u, keys, idx_use, p.W_upd, p.b_upd, w.ut, B, N, M, C, C, k, dtb, rt,
-                               mws, h->su, e0, e1);
+      return gl::launch_mrconv_args(ma, dtb, rt, mws, h->su, e0, e1);
     });
     if (s != GL_OK) return s;
   }
-  if ((s = lin("linear launch (FC2)", w.ut, C, p.W_out, p.b_out, C, 1, 0, x_in, w.y)) != GL_OK)
+  if ((s = lin("linear launch (FC2)", w.ut, C, p.W_out, p.b_out, C, 0, 0, x_in, w.y)) != GL_OK)
     return s;
   if ((s = lin("linear launch (FFN1)", w.y, C, p.W_1, p.b_1, 4 * C, 0, 1, nullptr, w.hid)) != GL_OK)
     return s;

@@ -162,6 +162,7 @@ MrArgs make_mr_args(const void* x, const void* keys, const int32_t* idx, const v
   a.k = k;
   a.heads = 1;
   a.col_tiles = 0;
+  a.act_out = 0;
   return a;
 }
 

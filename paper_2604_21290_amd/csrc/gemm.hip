@@ -5,8 +5,9 @@
 //     the contraction axis), where the fused MRConv tile would stream all of W
 //     through every 16- or 32-node workgroup;
 //   * FC1, FC2 + residual and the FFN of the full ViG block (Eq. 11, 14, 15):
-//     act_in = GELU gives sigma(U~) W_out^T, act_out = GELU the FFN's hidden
-//     layer, residual the two skip connections.
+//     act_out = GELU gives the FFN's hidden layer (and, on the wide MRConv
+//     update, the full block's sigma(U~)), residual the two skip connections;
+//     act_in = GELU is gl_linear's GELU on A.
 // A workgroup owns a 64 x 64 or 128 x 128 output tile, so W is read once per
 // 64 or 128 rows and A once per 64 or 128 output channels.
 //   - 4 waves in a 2 x 2 layout, or 8 in a 4 x 2 layout; each wave holds its
@@ -273,185 +274,10 @@ const void* gemm_fn(int v) {
   return fns[v];
 }
 
-// ---------------------------------------------------------------------------
-// Row-streaming GEMM for short contractions in bf16 with a GELU on A (FC2's
-// sigma(U~) W_out^T at the pyramid stages, K = C = 80 or 160).  The square
-// tiles above apply act_in to A once per 64 output channels and stage W again
-// for every 64 rows.  Here a workgroup stages all of W in LDS once (K <= 192,
-// Cout a multiple of 16, at most kRowsLds bytes), owns 16 * NW * RT rows and
-// every output channel, and reads each row of A from HBM exactly once,
-// straight into MFMA operand registers (both operands are K-contiguous: one
-// 16-byte vector per lane is an operand slice), where act_in is applied once.
-//   The product is formed transposed, out^T = W A^T, so lane (g, t) of a
-// 16 x 16 tile holds output row t, channels 4g..4g+3, and writes them as one
-// 8-byte vector.  Channels past K are zero on both sides; act_in is rounded
-// back to bf16 and the epilogue is the square tiles' (+ bias, act_out,
-// + residual in fp32, rounded once), so both kernels give the same bits.
-//   Measured against the square tiles on MI355X: FC2 at the first pyramid
-// stage (R = 100352, K = Cout = 80) 20.0 -> 14.9 us, at the second (R = 25088,
-// 160) 14.8 -> 12.6 us.  Without act_in it was no faster (FC1 11.3 against
-// 12.4 us at the first stage, 9.8 against 8.3 us at the second), and at
-// 128 rows per workgroup a ViG-Ti layer (R = 6272) fills too few CUs.
-constexpr int kRowsLds = 80 * 1024;  // LDS bytes of the staged W, at most
-constexpr int kRowsNW = 4, kRowsRT = 2;
-
-template <int KS>
-struct RowsCfg {
-  static constexpr int kRowW = KS * 64 + 16;  // LDS stride of a W row (16-byte reads conflict-free)
-};
-
-template <int ACT_IN, int ACT_OUT, int KS, int NW, int RT>
-__global__ __launch_bounds__(64 * NW) void gemm_rows_kernel(GemmArgs a) {
-  extern __shared__ __align__(16) char smem[];
-  constexpr int kRowW = RowsCfg<KS>::kRowW, NT = 64 * NW, VPR = KS * 4;  // 16-byte vectors per W row
-  constexpr int kBatch = 8;  // W vectors per thread per batch of loads
-  const int R = a.R, Cout = a.Cout, rowb = a.K * 2;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, t = lane & 15;
-  const int m0 = blockIdx.x * (16 * NW * RT) + w * (16 * RT);
-  const char* Ab = static_cast<const char*>(a.A);
-  const char* Wb = static_cast<const char*>(a.W);
-
-  // this wave's rows of A, requested first: they arrive while W is staged
-  uint4 af[RT][KS];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const size_t row = (size_t)min(m0 + rt * 16 + t, R - 1);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int off = ks * 64 + g * 16;
-      af[rt][ks] = *reinterpret_cast<const uint4*>(Ab + row * rowb + (off < rowb ? off : 0));
-    }
-  }
-  // all of W, in batches of 8 loads per thread (one or two batches for the
-  // layers this kernel takes); channels past K are stored as zeros
-  const int nvec = Cout * VPR;
-  for (int b0 = 0; b0 < nvec; b0 += NT * kBatch) {
-    u32x4 wr[kBatch];
-#pragma unroll
-    for (int i = 0; i < kBatch; ++i) {
-      const int v = b0 + tid + NT * i, n = v / VPR, sb = (v - n * VPR) * 16;
-      if (v < nvec)
-        wr[i] = *reinterpret_cast<const u32x4*>(Wb + (size_t)n * rowb + (sb < rowb ? sb : 0));
-    }
-#pragma unroll
-    for (int i = 0; i < kBatch; ++i) {
-      const int v = b0 + tid + NT * i;
-      if (v < nvec) {
-        asm volatile("" : "+v"(wr[i]));
-        const int n = v / VPR, sb = (v - n * VPR) * 16;
-        *reinterpret_cast<u32x4*>(smem + n * kRowW + sb) = sb < rowb ? wr[i] : u32x4{0, 0, 0, 0};
-      }
-    }
-  }
-  // channels past K (the last k-step's upper lanes) are zero in A too, so that
-  // a non-finite value beyond the row cannot reach the sum; act_in on the rest
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (ks * 64 + g * 16 >= rowb) af[rt][ks] = uint4{0, 0, 0, 0};
-      else if (ACT_IN) af[rt][ks] = __builtin_bit_cast(uint4, gelu_vec<1>(__builtin_bit_cast(u32x4, af[rt][ks])));
-    }
-  __syncthreads();
-
-  const uint16_t* bias = static_cast<const uint16_t*>(a.bias);
-  const uint16_t* res = static_cast<const uint16_t*>(a.residual);
-  uint16_t* out = static_cast<uint16_t*>(a.out);
-  for (int n0 = 0; n0 < Cout; n0 += 64) {
-    const int nj = min(4, (Cout - n0) >> 4);  // 16-channel tiles in this chunk (wave-uniform)
-    // the residual of this chunk does not depend on the product: request it first
-    uint2 rs[RT][4];
-    if (res) {
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (j < nj)
-            rs[rt][j] = *reinterpret_cast<const uint2*>(
-                res + (size_t)min(m0 + rt * 16 + t, R - 1) * Cout + n0 + j * 16 + 4 * g);
-    }
-    f32x4 acc[RT][4];
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[rt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      uint4 wf[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (j < nj)
-          wf[j] = *reinterpret_cast<const uint4*>(smem + (n0 + j * 16 + t) * kRowW + ks * 64 + g * 16);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (j < nj)
-#pragma unroll
-          for (int rt = 0; rt < RT; ++rt) acc[rt][j] = mfma_bf16(wf[j], af[rt][ks], acc[rt][j]);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (j >= nj) continue;
-      const int col = n0 + j * 16 + 4 * g;
-      float bn[4] = {0.f, 0.f, 0.f, 0.f};
-      if (bias) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) bn[v] = bf16_bits_to_f32(bias[col + v]);
-      }
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        const int row = m0 + rt * 16 + t;
-        float y[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          y[v] = acc[rt][j][v] + bn[v];
-          if (ACT_OUT) y[v] = gelu_f32(y[v]);
-        }
-        if (res) {
-          y[0] += bf16_bits_to_f32(rs[rt][j].x & 0xffffu);
-          y[1] += bf16_bits_to_f32(rs[rt][j].x >> 16);
-          y[2] += bf16_bits_to_f32(rs[rt][j].y & 0xffffu);
-          y[3] += bf16_bits_to_f32(rs[rt][j].y >> 16);
-        }
-        if (row < R)
-          *reinterpret_cast<uint2*>(out + (size_t)row * Cout + col) =
-              uint2{f32x2_to_bf16x2_bits(y[0], y[1]), f32x2_to_bf16x2_bits(y[2], y[3])};
-      }
-    }
-  }
-}
-
-template <int NW, int RT>
-const void* gemm_rows_fn(int act_in, int act_out, int ks) {
-#define GL_ROWS_ROW(KS)                                                              \
-  {(const void*)&gemm_rows_kernel<0, 0, KS, NW, RT>, (const void*)&gemm_rows_kernel<0, 1, KS, NW, RT>, \
-   (const void*)&gemm_rows_kernel<1, 0, KS, NW, RT>, (const void*)&gemm_rows_kernel<1, 1, KS, NW, RT>}
-  static const void* const fns[6][4] = {GL_ROWS_ROW(1), GL_ROWS_ROW(2), GL_ROWS_ROW(3),
-                                        GL_ROWS_ROW(4), GL_ROWS_ROW(5), GL_ROWS_ROW(6)};
-#undef GL_ROWS_ROW
-  return fns[ks - 1][act_in * 2 + act_out];
-}
-
-// The row-streaming GEMM takes the product: bf16 with a GELU on A, 8-byte
-// aligned out and residual, K <= 192, Cout % 16 == 0, W within kRowsLds bytes
-// of LDS, and at least 128 workgroups of rows.
-bool gemm_rows_ok(const GemmArgs& a, int dt_bf16) {
-  if (!dt_bf16 || !a.act_in || a.K > 192 || a.Cout % 16) return false;
-  if ((reinterpret_cast<uintptr_t>(a.out) | reinterpret_cast<uintptr_t>(a.residual)) % 8) return false;
-  if ((a.R + 16 * kRowsNW * kRowsRT - 1) / (16 * kRowsNW * kRowsRT) < 128) return false;
-  const int ks = (a.K * 2 + 63) / 64;
-  return (size_t)a.Cout * (ks * 64 + 16) <= (size_t)kRowsLds;
-}
-
 hipError_t launch_gemm_nt(const GemmArgs& a, int dt_bf16, hipStream_t stream, hipEvent_t ev0,
                           hipEvent_t ev1) {
   const int v = (dt_bf16 ? 4 : 0) + (a.act_in ? 2 : 0) + (a.act_out ? 1 : 0);
   const size_t rowb = (size_t)a.K * (dt_bf16 ? 2 : 4);
-  if (gemm_rows_ok(a, dt_bf16)) {
-    const int ks = (a.K * 2 + 63) / 64, rows = 16 * kRowsNW * kRowsRT;
-    const dim3 grid((unsigned)((a.R + rows - 1) / rows)), block(64 * kRowsNW);
-    return launch_with_smem(gemm_rows_fn<kRowsNW, kRowsRT>(a.act_in, a.act_out, ks), grid, block,
-                            (size_t)a.Cout * (ks * 64 + 16), stream, ev0, ev1, a);
-  }
   // large tiles once they alone give every CU a tile and K is long
   const long tiles128 = (long)((a.R + 127) / 128) * ((a.Cout + 127) / 128);
   if (tiles128 >= 256 && rowb >= 1024) {

@@ -31,6 +31,8 @@ struct MrArgs {
   int heads;          // > 1: W is block-diagonal by heads (Cout == C); zero blocks are skipped
   int col_tiles;      // > 0: each workgroup computes col_tiles 16-column output tiles of its
                       // nodes (small grids: the output columns split over several workgroups)
+  int act_out;        // 1: GELU on each output before its one rounding (the full block's
+                      // sigma(U~), which only FC2 reads); dense updates only
 };
 
 struct GemmArgs {

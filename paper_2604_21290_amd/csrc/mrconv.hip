@@ -186,7 +186,8 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
     ga.R = a.R;
     ga.K = 2 * C;
     ga.Cout = Cout;
-    ga.act_in = ga.act_out = 0;
+    ga.act_in = 0;
+    ga.act_out = a.act_out;
     return launch_gemm_nt(ga, dt_bf16, stream, nullptr, ev1);
   }
   const int TM = 16 * rt;

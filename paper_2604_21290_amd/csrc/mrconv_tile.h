@@ -285,7 +285,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
         batch(bw, s0);
       }
     }
-    // -- epilogue: + bias, round once, store ------------------------------------
+    // -- epilogue: + bias, [GELU], round once, store -----------------------------
     // a full tile (all TM nodes below R, Cout a multiple of 16; uniform)
     // stores without per-lane guards
     const bool full = row0 + TM <= R && (Cout & 15) == 0;
@@ -301,7 +301,8 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
       }
       auto put = [&](int rt, int v) {
         const size_t o = (size_t)(row0 + rt * 16 + 4 * g + v) * Cout + n;
-        const float y = acc[rt][c4][v] + bn;
+        float y = acc[rt][c4][v] + bn;
+        if (a.act_out) y = gelu_f32(y);
         if (DT) static_cast<uint16_t*>(a.out)[o] = (uint16_t)f32_to_bf16_bits(y);
         else static_cast<float*>(a.out)[o] = y;
       };

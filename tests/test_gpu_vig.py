@@ -57,11 +57,11 @@ LIN = [
     ("k80_fc2_gelu_in_residual", 20001, 80, 80, 1, 0, True, True, I.BF16),
     ("k96_ragged_cols", 3001, 96, 99, 0, 0, True, False, I.BF16),
     ("k128_one_stage_8_waves", 4097, 128, 200, 0, 1, True, True, I.BF16),
-    # the row-streaming kernel (GELU on A, K <= 192, Cout % 16 == 0): one to
-    # six k-steps, channels past K in the last one, ragged rows
-    ("rows_k8_gelu_in", 16400, 8, 48, 1, 0, True, False, I.BF16),
-    ("rows_k40_gelu_in_cout16", 20000, 40, 16, 1, 0, False, True, I.BF16),
-    ("rows_k192_gelu_in_out", 16500, 192, 192, 1, 1, True, True, I.BF16),
+    # GELU on A over one to six k-steps, channels past K in the last one,
+    # ragged rows
+    ("k8_gelu_in", 16400, 8, 48, 1, 0, True, False, I.BF16),
+    ("k40_gelu_in_cout16", 20000, 40, 16, 1, 0, False, True, I.BF16),
+    ("k192_gelu_in_out", 16500, 192, 192, 1, 1, True, True, I.BF16),
 ]
 
 
