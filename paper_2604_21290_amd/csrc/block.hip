@@ -43,7 +43,7 @@ __device__ __forceinline__ bool block_role_is_build(int i, int nb, int nu, int* 
 // rows); that variant takes 74 KB of LDS, so two workgroups per CU, and is
 // compiled for two waves per SIMD, which leaves it the registers for the
 // tile's second staging set and for a one-round gather.
-template <int DT, int R, int RT, int KB, int WK>
+template <int DT, int R, int RT, int KB, int WK, bool ACT>
 __device__ __forceinline__ void block_body(char* smem, const KnnArgs& ka, const MrArgs& ma, int nb, int nu) {
   constexpr int ES = DT ? 2 : 4;
   int j;
@@ -61,50 +61,56 @@ __device__ __forceinline__ void block_body(char* smem, const KnnArgs& ka, const 
     }
   } else {
     j = xcd_remap(j, nu);
-    mrconv_tile<DT, RT, KB, false, (WK > 0) && kBlockWideT3>(smem, ma, j * 16 * RT);
+    mrconv_tile<DT, RT, KB, false, (WK > 0) && kBlockWideT3, false, false, ACT>(smem, ma, j * 16 * RT);
   }
 }
 
-template <int DT, int R, int RT, int KB, int WK>
+// ACT: the update role's GELU epilogue (ma.act_out, the full block).
+template <int DT, int R, int RT, int KB, int WK, bool ACT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 8))) void block_kernel(KnnArgs ka, MrArgs ma, int nb, int nu) {
   extern __shared__ __align__(16) char smem[];
-  block_body<DT, R, RT, KB, WK>(smem, ka, ma, nb, nu);
+  block_body<DT, R, RT, KB, WK, ACT>(smem, ka, ma, nb, nu);
 }
 
-template <int DT, int R, int RT, int KB, int WK>
+template <int DT, int R, int RT, int KB, int WK, bool ACT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kBlockWideWaves, 8))) void block_kernel_wide(KnnArgs ka, MrArgs ma, int nb, int nu) {
   extern __shared__ __align__(16) char smem[];
-  block_body<DT, R, RT, KB, WK>(smem, ka, ma, nb, nu);
+  block_body<DT, R, RT, KB, WK, ACT>(smem, ka, ma, nb, nu);
 }
 
-template <int DT, int R, int RT, int WK>
+template <int DT, int R, int RT, int WK, bool ACT>
 const void* block_fn_kb(int KB) {
   if constexpr (WK > 0) {
     switch (KB) {
-      case 9: return (const void*)&block_kernel_wide<DT, R, RT, 9, WK>;
-      case 16: return (const void*)&block_kernel_wide<DT, R, RT, 16, WK>;
-      case 32: return (const void*)&block_kernel_wide<DT, R, RT, 32, WK>;
-      default: return (const void*)&block_kernel_wide<DT, R, RT, 64, WK>;
+      case 9: return (const void*)&block_kernel_wide<DT, R, RT, 9, WK, ACT>;
+      case 16: return (const void*)&block_kernel_wide<DT, R, RT, 16, WK, ACT>;
+      case 32: return (const void*)&block_kernel_wide<DT, R, RT, 32, WK, ACT>;
+      default: return (const void*)&block_kernel_wide<DT, R, RT, 64, WK, ACT>;
     }
   } else {
     switch (KB) {
-      case 9: return (const void*)&block_kernel<DT, R, RT, 9, WK>;
-      case 16: return (const void*)&block_kernel<DT, R, RT, 16, WK>;
-      case 32: return (const void*)&block_kernel<DT, R, RT, 32, WK>;
-      default: return (const void*)&block_kernel<DT, R, RT, 64, WK>;
+      case 9: return (const void*)&block_kernel<DT, R, RT, 9, WK, ACT>;
+      case 16: return (const void*)&block_kernel<DT, R, RT, 16, WK, ACT>;
+      case 32: return (const void*)&block_kernel<DT, R, RT, 32, WK, ACT>;
+      default: return (const void*)&block_kernel<DT, R, RT, 64, WK, ACT>;
     }
   }
 }
 
-template <int DT, int R, int WK>
+template <int DT, int R, int WK, bool ACT>
 const void* block_fn_rt(int RT, int KB) {
-  return RT == 2 ? block_fn_kb<DT, R, 2, WK>(KB) : block_fn_kb<DT, R, 1, WK>(KB);
+  return RT == 2 ? block_fn_kb<DT, R, 2, WK, ACT>(KB) : block_fn_kb<DT, R, 1, WK, ACT>(KB);
+}
+
+template <int DT, int WK, bool ACT>
+const void* block_fn_r(int R, int RT, int KB) {
+  return R == 1 ? block_fn_rt<DT, 1, WK, ACT>(RT, KB)
+                : R == 2 ? block_fn_rt<DT, 2, WK, ACT>(RT, KB) : block_fn_rt<DT, 4, WK, ACT>(RT, KB);
 }
 
 template <int DT, int WK = 0>
-const void* block_fn(int R, int RT, int KB) {
-  return R == 1 ? block_fn_rt<DT, 1, WK>(RT, KB)
-                : R == 2 ? block_fn_rt<DT, 2, WK>(RT, KB) : block_fn_rt<DT, 4, WK>(RT, KB);
+const void* block_fn(int R, int RT, int KB, int act) {
+  return act ? block_fn_r<DT, WK, true>(R, RT, KB) : block_fn_r<DT, WK, false>(R, RT, KB);
 }
 
 // Key rows the build role stages when it is the LDS-staged tile (the
@@ -127,9 +133,10 @@ hipError_t launch_block(const KnnArgs& ka, const MrArgs& ma, int dt_bf16, int rt
   const size_t smem = std::max(wide ? wsm : knn_smem_bytes(ka.C, dt_bf16),
                                mrconv_smem_bytes(ma.C, ma.k, dt_bf16, rt));
   const int R = knn_list_regs(ka.KK), KB = mrconv_k_bucket(ma.k);
-  const void* fn = wk == 224 ? block_fn<1, 224>(R, rt, KB)
-                   : wk == 128 ? block_fn<1, 128>(R, rt, KB)
-                   : dt_bf16 ? block_fn<1>(R, rt, KB) : block_fn<0>(R, rt, KB);
+  const int act = ma.act_out;
+  const void* fn = wk == 224 ? block_fn<1, 224>(R, rt, KB, act)
+                   : wk == 128 ? block_fn<1, 128>(R, rt, KB, act)
+                   : dt_bf16 ? block_fn<1>(R, rt, KB, act) : block_fn<0>(R, rt, KB, act);
   const dim3 grid(nb + nu), block(256);
   struct {
     KnnArgs ka;

@@ -27,34 +27,34 @@ bool mrconv_use_lean(int C, int Cout, int row_tiles) {
 
 int mrconv_k_bucket(int k) { return k <= 9 ? 9 : k <= 16 ? 16 : k <= 32 ? 32 : 64; }
 
-template <int DT, int RT, int KB>
+template <int DT, int RT, int KB, bool ACT = false>
 __global__ __launch_bounds__(kMrThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void mrconv_kernel(MrArgs a) {
   extern __shared__ __align__(16) char smem[];
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
-  mrconv_tile<DT, RT, KB>(smem, a, blk * 16 * RT);
+  mrconv_tile<DT, RT, KB, false, false, false, false, ACT>(smem, a, blk * 16 * RT);
 }
 
 // Narrow layers over many node tiles: one output tile per wave and pass and
 // one gather task per thread (78 VGPRs at k <= 9: six waves per SIMD).
-template <int DT, int RT, int KB>
+template <int DT, int RT, int KB, bool ACT = false>
 __global__ __launch_bounds__(kMrThreads) __attribute__((amdgpu_waves_per_eu(4, 8))) void mrconv_lean_kernel(MrArgs a) {
   extern __shared__ __align__(16) char smem[];
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
-  mrconv_tile<DT, RT, KB, false, false, false, true>(smem, a, blk * 16 * RT);
+  mrconv_tile<DT, RT, KB, false, false, false, true, ACT>(smem, a, blk * 16 * RT);
 }
 
 // Small grids: workgroup blk computes output-column group blk % ncg (a.col_tiles
 // 16-column tiles) of node tile blk / ncg.  Few workgroups run, so the kernel is
 // not held to three waves per SIMD.
-template <int DT, int RT, int KB>
+template <int DT, int RT, int KB, bool ACT = false>
 __global__ __launch_bounds__(kMrThreads) void mrconv_cols_kernel(MrArgs a) {
   extern __shared__ __align__(16) char smem[];
   const int nct = (a.Cout + 15) >> 4;
   const int ncg = (nct + a.col_tiles - 1) / a.col_tiles;
   const int blk = blockIdx.x, cg = blk % ncg;
   const int tile0 = cg * a.col_tiles;
-  mrconv_tile<DT, RT, KB, false, false, true>(smem, a, (blk / ncg) * 16 * RT, tile0,
-                                              min(nct, tile0 + a.col_tiles));
+  mrconv_tile<DT, RT, KB, false, false, true, false, ACT>(smem, a, (blk / ncg) * 16 * RT, tile0,
+                                                          min(nct, tile0 + a.col_tiles));
 }
 
 // The multi-head update: the per-tile step tests need registers the
@@ -66,21 +66,21 @@ __global__ __launch_bounds__(kMrThreads) void mrconv_heads_kernel(MrArgs a) {
   mrconv_tile<DT, RT, KB, true>(smem, a, blk * 16 * RT);
 }
 
-template <int DT, int RT, bool HEADS = false, bool COLS = false, bool LEAN = false>
+template <int DT, int RT, bool HEADS = false, bool COLS = false, bool LEAN = false, bool ACT = false>
 const void* mrconv_fn_kb(int KB) {
   if constexpr (LEAN) {
     switch (KB) {
-      case 9: return (const void*)&mrconv_lean_kernel<DT, RT, 9>;
-      case 16: return (const void*)&mrconv_lean_kernel<DT, RT, 16>;
-      case 32: return (const void*)&mrconv_lean_kernel<DT, RT, 32>;
-      default: return (const void*)&mrconv_lean_kernel<DT, RT, 64>;
+      case 9: return (const void*)&mrconv_lean_kernel<DT, RT, 9, ACT>;
+      case 16: return (const void*)&mrconv_lean_kernel<DT, RT, 16, ACT>;
+      case 32: return (const void*)&mrconv_lean_kernel<DT, RT, 32, ACT>;
+      default: return (const void*)&mrconv_lean_kernel<DT, RT, 64, ACT>;
     }
   } else if constexpr (COLS) {
     switch (KB) {
-      case 9: return (const void*)&mrconv_cols_kernel<DT, RT, 9>;
-      case 16: return (const void*)&mrconv_cols_kernel<DT, RT, 16>;
-      case 32: return (const void*)&mrconv_cols_kernel<DT, RT, 32>;
-      default: return (const void*)&mrconv_cols_kernel<DT, RT, 64>;
+      case 9: return (const void*)&mrconv_cols_kernel<DT, RT, 9, ACT>;
+      case 16: return (const void*)&mrconv_cols_kernel<DT, RT, 16, ACT>;
+      case 32: return (const void*)&mrconv_cols_kernel<DT, RT, 32, ACT>;
+      default: return (const void*)&mrconv_cols_kernel<DT, RT, 64, ACT>;
     }
   } else if constexpr (HEADS) {
     switch (KB) {
@@ -91,12 +91,19 @@ const void* mrconv_fn_kb(int KB) {
     }
   } else {
     switch (KB) {
-      case 9: return (const void*)&mrconv_kernel<DT, RT, 9>;
-      case 16: return (const void*)&mrconv_kernel<DT, RT, 16>;
-      case 32: return (const void*)&mrconv_kernel<DT, RT, 32>;
-      default: return (const void*)&mrconv_kernel<DT, RT, 64>;
+      case 9: return (const void*)&mrconv_kernel<DT, RT, 9, ACT>;
+      case 16: return (const void*)&mrconv_kernel<DT, RT, 16, ACT>;
+      case 32: return (const void*)&mrconv_kernel<DT, RT, 32, ACT>;
+      default: return (const void*)&mrconv_kernel<DT, RT, 64, ACT>;
     }
   }
+}
+
+// The dense variants' table, with or without the GELU epilogue (a.act_out).
+template <int DT, int RT, bool COLS = false, bool LEAN = false>
+const void* mrconv_fn_act(int KB, int act) {
+  return act ? mrconv_fn_kb<DT, RT, false, COLS, LEAN, true>(KB)
+             : mrconv_fn_kb<DT, RT, false, COLS, LEAN, false>(KB);
 }
 
 // Gather-only workgroup of the two-pass MRConv: kMrGatherRows nodes.
@@ -168,7 +175,7 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
   void* out = a.out;
   const int KB = mrconv_k_bucket(k);
   // the multi-head update (W = per-head Wh) always takes the fused tile
-  if (a.heads > 1 && rt < 1) return hipErrorInvalidValue;
+  if (a.heads > 1 && (rt < 1 || a.act_out)) return hipErrorInvalidValue;
   if (a.heads <= 1 && mrconv_use_split(C, Cout, dt_bf16, rt, a.R)) {
     if (!split_ws) return hipErrorInvalidValue;
     const dim3 g1((a.R + kMrGatherRows - 1) / kMrGatherRows), blk(kMrThreads);
@@ -202,24 +209,25 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
   const int ncg = a.col_tiles ? (nct + a.col_tiles - 1) / a.col_tiles : 1;
   const dim3 grid(row_tiles * ncg), block(kMrThreads);
   const void* fn;
+  const int act = a.act_out;
   if (a.col_tiles > 0) {
-    fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2, false, true>(KB) : mrconv_fn_kb<1, 1, false, true>(KB))
-                 : (rt == 2 ? mrconv_fn_kb<0, 2, false, true>(KB) : mrconv_fn_kb<0, 1, false, true>(KB));
+    fn = dt_bf16 ? (rt == 2 ? mrconv_fn_act<1, 2, true>(KB, act) : mrconv_fn_act<1, 1, true>(KB, act))
+                 : (rt == 2 ? mrconv_fn_act<0, 2, true>(KB, act) : mrconv_fn_act<0, 1, true>(KB, act));
   } else if (a.heads > 1) {
     fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2, true>(KB) : mrconv_fn_kb<1, 1, true>(KB))
                  : (rt == 2 ? mrconv_fn_kb<0, 2, true>(KB) : mrconv_fn_kb<0, 1, true>(KB));
   } else if (mrconv_use_lean(a.C, Cout, row_tiles)) {
     // 64-node tiles when they fit 64 KB of LDS (measured 2-3 % faster than 32)
     if (mrconv_smem_bytes(C, k, dt_bf16, 4) <= 65536) {
-      fn = dt_bf16 ? mrconv_fn_kb<1, 4, false, false, true>(KB) : mrconv_fn_kb<0, 4, false, false, true>(KB);
+      fn = dt_bf16 ? mrconv_fn_act<1, 4, false, true>(KB, act) : mrconv_fn_act<0, 4, false, true>(KB, act);
       return launch_with_smem(fn, dim3((a.R + 63) / 64), block, mrconv_smem_bytes(C, k, dt_bf16, 4),
                               stream, ev0, ev1, a);
     }
-    fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2, false, false, true>(KB) : mrconv_fn_kb<1, 1, false, false, true>(KB))
-                 : (rt == 2 ? mrconv_fn_kb<0, 2, false, false, true>(KB) : mrconv_fn_kb<0, 1, false, false, true>(KB));
+    fn = dt_bf16 ? (rt == 2 ? mrconv_fn_act<1, 2, false, true>(KB, act) : mrconv_fn_act<1, 1, false, true>(KB, act))
+                 : (rt == 2 ? mrconv_fn_act<0, 2, false, true>(KB, act) : mrconv_fn_act<0, 1, false, true>(KB, act));
   } else {
-    fn = dt_bf16 ? (rt == 2 ? mrconv_fn_kb<1, 2>(KB) : mrconv_fn_kb<1, 1>(KB))
-                 : (rt == 2 ? mrconv_fn_kb<0, 2>(KB) : mrconv_fn_kb<0, 1>(KB));
+    fn = dt_bf16 ? (rt == 2 ? mrconv_fn_act<1, 2>(KB, act) : mrconv_fn_act<1, 1>(KB, act))
+                 : (rt == 2 ? mrconv_fn_act<0, 2>(KB, act) : mrconv_fn_act<0, 1>(KB, act));
   }
   return launch_with_smem(fn, grid, block, smem, stream, ev0, ev1, a);
 }

@@ -176,8 +176,10 @@ __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM
 // HEADS: the multi-head update (a.heads > 1), which skips the zero blocks of W.
 // COLS: only the 16-column output tiles tile0 .. tile_end-1 (tile_end within
 // the layer's tiles), the column group of a small grid.
+// ACT: GELU on each output before its rounding (a.act_out; compiled in only
+// for the full block's update, so the other updates carry none of its code).
 template <int DT, int RT, int KB, bool HEADS = false, bool T3 = false, bool COLS = false,
-          bool LEAN = false>
+          bool LEAN = false, bool ACT = false>
 __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row0, int tile0 = 0,
                                             int tile_end = 0) {
   constexpr int TM = 16 * RT;
@@ -302,7 +304,7 @@ __device__ __forceinline__ void mrconv_tile(char* smem, const MrArgs& a, int row
       auto put = [&](int rt, int v) {
         const size_t o = (size_t)(row0 + rt * 16 + 4 * g + v) * Cout + n;
         float y = acc[rt][c4][v] + bn;
-        if (a.act_out) y = gelu_f32(y);
+        if constexpr (ACT) y = gelu_f32(y);
         if (DT) static_cast<uint16_t*>(a.out)[o] = (uint16_t)f32_to_bf16_bits(y);
         else static_cast<float*>(a.out)[o] = y;
       };
