@@ -109,9 +109,13 @@ PYR_DIL = (1, 2, 1)
 
 
 def _workload(name, B):
-    w = I.with_batch(I.WORKLOADS[name], B)
+    """name[:f32] at batch B; an ":f32" suffix runs the workload in fp32."""
+    base, _, dt = name.partition(":")
+    w = I.with_batch(I.WORKLOADS[base], B)
     if w.pool_r > 1:
         w = dataclasses.replace(w, dilations=PYR_DIL)
+    if dt == "f32":
+        w = dataclasses.replace(w, dtype=I.F32)
     return w
 
 
@@ -152,7 +156,7 @@ def _run_blocks(w, L, x0d, params_d, same_stream=False):
 
 
 @pytest.mark.parametrize("name,B,L", [("vig_ti", 4, 6), ("vig_b", 2, 5), ("single", 1, 1),
-                                      ("pyr_s1", 2, 3), ("pyr_s2", 2, 3)])
+                                      ("pyr_s1", 2, 3), ("pyr_s2", 2, 3), ("pyr_s2:f32", 1, 3)])
 def test_vig_blocks_teacher_forced(name, B, L):
     require_gpu()
     from paper_2604_21290_amd import api
@@ -187,7 +191,7 @@ def test_vig_blocks_teacher_forced(name, B, L):
 
 
 @pytest.mark.parametrize("name,B,L", [("vig_ti", 4, 6), ("vig_b", 2, 5), ("pyr_s1", 2, 3),
-                                      ("pyr_s2", 2, 3)])
+                                      ("pyr_s2", 2, 3), ("pyr_s2:f32", 1, 3)])
 def test_vig_stack_matches_blocks(name, B, L):
     require_gpu()
     from paper_2604_21290_amd import api
@@ -260,4 +264,31 @@ def test_vig_zero_branches_are_identity(name):
         out = la.vig_stack(x0d, pd, list(w.dilations[:L]), w.k, schedule=sc, **_grid(w))
         torch.cuda.synchronize()
         assert torch.equal(out, x0d), sc
+    la.close()
+
+
+def test_vig_pooled_shape_errors():
+    """Pooling windows that do not divide the grid or leave fewer keys than k,
+    a grid that does not match N, and a short workspace are refused before
+    anything is enqueued."""
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = _workload("pyr_s2", 1)
+    x0d = to_dev(I.make_features(w))
+    pd = [_dev_params(I.make_vig_params(w, 0))]
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    ws = api.vig_workspace(x0d, w.k, w.H, w.W, w.pool_r)
+    idx = torch.zeros((1, w.N, w.k), dtype=torch.int32, device="cuda")
+    with pytest.raises(api.GraphLeapError, match="BAD_SHAPE"):
+        la.vig_block(x0d, idx, pd[0], ws, H=w.H, W=w.W, pool_r=3)      # 3 does not divide 28
+    with pytest.raises(api.GraphLeapError, match="BAD_SHAPE"):
+        la.vig_stack(x0d, pd, [1], w.k, ws=ws, H=w.H, W=w.W, pool_r=0)
+    with pytest.raises(api.GraphLeapError, match="grid"):
+        la.vig_stack(x0d, pd, [1], w.k, ws=ws, H=w.H, W=w.W + 1, pool_r=1)  # H*W != N
+    with pytest.raises(api.GraphLeapError, match="BAD_K"):
+        la.vig_stack(x0d, pd, [1], w.k, ws=ws, H=w.H, W=w.W, pool_r=14)     # M = 4 < k = 9
+    small = ws[: ws.numel() // 2]
+    with pytest.raises(api.GraphLeapError, match="BAD_SHAPE"):
+        la.vig_stack(x0d, pd, [1], w.k, ws=small, H=w.H, W=w.W, pool_r=w.pool_r)
+    torch.cuda.synchronize()
     la.close()
