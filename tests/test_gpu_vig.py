@@ -292,3 +292,42 @@ def test_vig_pooled_shape_errors():
         la.vig_stack(x0d, pd, [1], w.k, ws=small, H=w.H, W=w.W, pool_r=w.pool_r)
     torch.cuda.synchronize()
     la.close()
+
+
+@pytest.mark.parametrize("name,B", [("vig_ti", 4), ("pyr_s2", 2)])
+def test_vig_stack_hip_graph_replay(name, B):
+    """The fused-schedule full-block stack captured in a HIP graph: every
+    replay, with eager work and synchronisations between replays, equals the
+    eager run.  Everything lives in the caller's workspace (at the pyramid
+    stage the pooled keys too), so the capture holds no allocation."""
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = _workload(name, B)
+    L = min(4, w.L)
+    x0d = to_dev(I.make_features(w))
+    pd = [_dev_params(I.make_vig_params(w, l)) for l in range(L)]
+    dil = list(w.dilations[:L])
+    s = torch.cuda.Stream()
+    la = api.Lookahead(s, s)
+    ws = api.vig_workspace(x0d, w.k, **_grid(w))
+    ref = torch.empty_like(x0d)
+    with torch.cuda.stream(s):
+        la.vig_stack(x0d, pd, dil, w.k, schedule=api.GL_SCHED_LOOKAHEAD_FUSED, ws=ws, x_out=ref,
+                     **_grid(w))
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    out = torch.empty_like(x0d)
+    with torch.cuda.graph(g, stream=s):
+        la.vig_stack(x0d, pd, dil, w.k, schedule=api.GL_SCHED_LOOKAHEAD_FUSED, ws=ws, x_out=out,
+                     **_grid(w))
+    for r in range(4):
+        out.zero_()
+        junk = api.linear(x0d, pd[0]["W_in"])      # eager work between replays
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            g.replay()
+        torch.cuda.synchronize()
+        _say(name, "graph replay", r)
+        assert torch.equal(out, ref), f"{name}: replay {r} differs"
+        del junk
+    la.close()
