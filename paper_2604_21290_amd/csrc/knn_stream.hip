@@ -1,9 +1,9 @@
 // Dilated kNN graph build with keys streamed through LDS, for large key sets
 // (Sec. II-B Eq. 4; Sec. IV-B; Alg. 2).
 //
-// One workgroup = 4 waves = 64 query rows of one image; wave w owns rows
-// 16w .. 16w+15 and keeps their MFMA A operands (all contraction steps) and
-// inverse norms in registers for the whole kernel.
+// One workgroup = NW waves (4 or 8) = 16 NW query rows of one image; wave w
+// owns rows 16w .. 16w+15 and keeps their MFMA A operands (all contraction
+// steps) and inverse norms in registers for the whole kernel.
 //   1. Keys arrive in chunks of KC rows, loaded cooperatively (16-byte vectors,
 //      fully coalesced) into registers while the previous chunk is used, then
 //      stored to LDS; each key's distance scale factors are computed once per
@@ -32,17 +32,18 @@
 
 namespace gl {
 
-constexpr int kStRows = 64;      // query rows per workgroup
 constexpr int kStCap = 128;      // candidate slots per row
 constexpr int kStSlots = kStCap / 16;  // layers of 16 in a full row buffer
 constexpr int kStRowStride = kStCap + 2;  // words per row of slots (rows 4 apart change bank)
 constexpr int kStGroup = 4;      // key tiles computed together (independent MFMA chains)
-constexpr int kStThreads = 256;
-// Narrow rows (<= 4 contraction steps) run two workgroups per CU; wider rows
-// are register-bound to one, which then gets more LDS and a deeper prefetch.
+// Four-wave workgroups: narrow rows (<= 4 contraction steps) run two per CU;
+// wider rows are register-bound to one, which then gets more LDS and a deeper
+// prefetch.  Eight-wave workgroups run one per CU and take the LDS of one.
 constexpr int kStWideKS = 12;
 __host__ __device__ constexpr int st_max_vec(int KS) { return KS >= kStWideKS ? 20 : 10; }
-__host__ __device__ constexpr int st_lds_budget(int KS) { return KS >= kStWideKS ? 150 * 1024 : 80 * 1024; }
+__host__ __device__ constexpr int st_lds_budget(int KS, int NW) {
+  return KS >= kStWideKS || NW == 8 ? 150 * 1024 : 80 * 1024;
+}
 
 struct StreamGeom {
   int KC, kstride;
@@ -54,42 +55,43 @@ struct StreamGeom {
 // steps the kernel runs (channels past C stay zero) plus 16 bytes that move
 // consecutive rows to other banks.  KC is a multiple of 64 (whole groups of 4
 // tiles), as large as the budget allows, at least 64.
-__host__ __device__ inline StreamGeom stream_geom(int C, int dt_bf16, int KS) {
+__host__ __device__ inline StreamGeom stream_geom(int C, int dt_bf16, int KS, int NW) {
   StreamGeom s;
   const int rowb = C * (dt_bf16 ? 2 : 4);
+  const int rows = 16 * NW;
   s.kstride = KS * 64 + 16;  // a contraction step is 64 bytes in either type
-  const int fixed = kStRows * kStRowStride * 4 + kStRows * 4;
-  int kc = (st_lds_budget(KS) - fixed) / (s.kstride + 8);
-  const int kv = st_max_vec(KS) * kStThreads * 16 / rowb;  // prefetchable rows
+  const int fixed = rows * kStRowStride * 4 + rows * 4;
+  int kc = (st_lds_budget(KS, NW) - fixed) / (s.kstride + 8);
+  const int kv = st_max_vec(KS) * 64 * NW * 16 / rowb;  // prefetchable rows
   kc = (kc < kv ? kc : kv) / 64 * 64;
   s.KC = kc > 256 ? 256 : kc < 64 ? 64 : kc;
   s.keys = 0;
   s.scales = s.keys + (size_t)s.KC * s.kstride;
   s.cand = s.scales + (size_t)s.KC * 8;
-  s.tau = s.cand + (size_t)kStRows * kStRowStride * 4;
-  s.total = s.tau + kStRows * 4;
+  s.tau = s.cand + (size_t)rows * kStRowStride * 4;
+  s.total = s.tau + rows * 4;
   return s;
 }
 
-template <int DT, int MV>
+template <int DT, int MV, int NT>
 __device__ __forceinline__ void st_load_chunk(u32x4 (&regs)[MV], const char* kb, int k0,
                                               int M, int C, int CG, int nvec, int e0, int tid) {
   constexpr int ES = DT ? 2 : 4;
   constexpr int VEC = 16 / ES;
 #pragma unroll
   for (int i = 0; i < MV; ++i) {
-    const int e = min(e0 + tid + i * kStThreads, nvec - 1);
+    const int e = min(e0 + tid + i * NT, nvec - 1);
     const int r = e / CG, cg = e - r * CG;
     regs[i] = *reinterpret_cast<const u32x4*>(kb + ((size_t)min(k0 + r, M - 1) * C + cg * VEC) * ES);
   }
 }
 
-template <int MV>
+template <int MV, int NT>
 __device__ __forceinline__ void st_store_chunk(const u32x4 (&regs)[MV], char* kbuf,
                                                int kstride, int CG, int nvec, int e0, int tid) {
 #pragma unroll
   for (int i = 0; i < MV; ++i) {
-    const int e = e0 + tid + i * kStThreads;
+    const int e = e0 + tid + i * NT;
     const int ec = min(e, nvec - 1);
     const int r = ec / CG, cg = ec - r * CG;
     if (e < nvec) *reinterpret_cast<u32x4*>(kbuf + r * kstride + cg * 16) = regs[i];
@@ -100,13 +102,13 @@ __device__ __forceinline__ void st_store_chunk(const u32x4 (&regs)[MV], char* kb
 // are summed in the order of the in-register kernel (per 4-lane-group channel
 // slice over the contraction steps, then (s0 + s1) + (s2 + s3)), so both
 // kernels rank identical packed keys.
-template <int DT, int KS>
+template <int DT, int KS, int NT>
 __device__ __forceinline__ void st_chunk_scales(const char* kbuf, float2* ksc, int KC, int kstride,
                                                 int k0, int M, int C, float qscale, int tid) {
   constexpr int ES = DT ? 2 : 4;
   constexpr int KSTEP = DT ? 32 : 16;
   const int half = tid & 1;
-  for (int r0 = 0; r0 < KC; r0 += kStThreads / 2) {
+  for (int r0 = 0; r0 < KC; r0 += NT / 2) {
     const int r = r0 + (tid >> 1);
     const int rr = min(r, KC - 1);
     float sq[2] = {0.f, 0.f};
@@ -274,8 +276,9 @@ __device__ __forceinline__ void st_flush(uint32_t (&L)[4][R], float (&tS)[4], in
 // epilogue and are held to two waves per SIMD.  Medium rows need those
 // registers for their A operands and run one group at a time.  Wide rows
 // (KS >= kStWideKS) are at one wave per SIMD anyway and overlap again.
-template <int DT, int R, int KS>
+template <int DT, int R, int KS, int NW>
 __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int kstride, char* smem) {
+  constexpr int NT = 64 * NW, ROWS = 16 * NW;
   constexpr bool PIPE = KS <= 4 || KS >= kStWideKS;
   constexpr bool SPLIT = KS <= 4;  // B operands one epilogue ahead of their MFMAs
   constexpr int MV = st_max_vec(KS);
@@ -286,13 +289,13 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
   const float qscale = a.qscale;
   const float qmaxf = (float)a.qmax;
   const int ksteps = (C + KSTEP - 1) / KSTEP;
-  const int nqb = (N + kStRows - 1) / kStRows;
+  const int nqb = (N + ROWS - 1) / ROWS;
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
-  const int b = blk / nqb, q0 = (blk - b * nqb) * kStRows;
+  const int b = blk / nqb, q0 = (blk - b * nqb) * ROWS;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, t = lane & 15;
 
-  const StreamGeom geo = stream_geom(C, DT, KS);
+  const StreamGeom geo = stream_geom(C, DT, KS, NW);
   char* kbuf0 = smem + geo.keys;
   float2* ksc0 = reinterpret_cast<float2*>(smem + geo.scales);
   uint32_t* cand = reinterpret_cast<uint32_t*>(smem + geo.cand) + w * 16 * kStRowStride;
@@ -347,7 +350,7 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
   // -- zero pad of the key rows (channels C .. 32 KS); chunk stores leave it alone ----
   {
     const int padv = (kstride - 16 - C * ES) / 16;
-    for (int i = tid; i < KC * padv; i += kStThreads) {
+    for (int i = tid; i < KC * padv; i += NT) {
       const int r = i / padv;
       *reinterpret_cast<u32x4*>(kbuf0 + r * kstride + C * ES + (i - r * padv) * 16) = u32x4{0, 0, 0, 0};
     }
@@ -377,25 +380,26 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
   // ahead of the loop, the compiler's wait bookkeeping at the loop head keeps
   // treating their registers as pending and makes every chunk wait for the
   // next chunk's prefetch.
-  const bool prefetch = nvec <= MV * kStThreads;
+  const bool prefetch = nvec <= MV * NT;
   for (int c = 0; c < nchunks; ++c) {
     const int ch = chunk_at(c);
     const int chn = chunk_at(c + 1 < nchunks ? c + 1 : c);
     const int k0 = ch * KC;
     const int ntl = (min(KC, M - k0) + 15) >> 4;
     if (prefetch) {
-      if (c == 0) st_load_chunk<DT>(regs, kb, k0, M, C, CG, nvec, 0, tid);
-      st_store_chunk(regs, kbuf, kstride, CG, nvec, 0, tid);
+      if (c == 0) st_load_chunk<DT, MV, NT>(regs, kb, k0, M, C, CG, nvec, 0, tid);
+      st_store_chunk<MV, NT>(regs, kbuf, kstride, CG, nvec, 0, tid);
     } else {
-      for (int e0 = 0; e0 < nvec; e0 += MV * kStThreads) {
-        st_load_chunk<DT>(regs, kb, k0, M, C, CG, nvec, e0, tid);
-        st_store_chunk(regs, kbuf, kstride, CG, nvec, e0, tid);
+      for (int e0 = 0; e0 < nvec; e0 += MV * NT) {
+        st_load_chunk<DT, MV, NT>(regs, kb, k0, M, C, CG, nvec, e0, tid);
+        st_store_chunk<MV, NT>(regs, kbuf, kstride, CG, nvec, e0, tid);
       }
     }
     __syncthreads();
-    st_chunk_scales<DT, KS>(kbuf, ksc0, KC, kstride, k0, M, C, qscale, tid);
+    st_chunk_scales<DT, KS, NT>(kbuf, ksc0, KC, kstride, k0, M, C, qscale, tid);
     __syncthreads();
-    if (prefetch && c + 1 < nchunks) st_load_chunk<DT>(regs, kb, chn * KC, M, C, CG, nvec, 0, tid);
+    if (prefetch && c + 1 < nchunks)
+      st_load_chunk<DT, MV, NT>(regs, kb, chn * KC, M, C, CG, nvec, 0, tid);
     // Gram tiles of group t0 + 4 are issued before the epilogue of group t0
     // (independent MFMA chains run while the VALU filters).  All KC rows of the
     // key buffer hold finite values (the chunk loader repeats the last key),
@@ -502,16 +506,16 @@ __device__ __forceinline__ void knn_stream_body(const KnnArgs& a, int KC, int ks
   }
 }
 
-template <int DT, int R, int KS>
-__global__ __launch_bounds__(kStThreads) __attribute__((amdgpu_waves_per_eu(2, 8))) void knn_stream_kernel_narrow(KnnArgs a, int KC, int kstride) {
+template <int DT, int R, int KS, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2, 8))) void knn_stream_kernel_narrow(KnnArgs a, int KC, int kstride) {
   extern __shared__ __align__(16) char smem[];
-  knn_stream_body<DT, R, KS>(a, KC, kstride, smem);
+  knn_stream_body<DT, R, KS, NW>(a, KC, kstride, smem);
 }
 
-template <int DT, int R, int KS>
-__global__ __launch_bounds__(kStThreads) void knn_stream_kernel(KnnArgs a, int KC, int kstride) {
+template <int DT, int R, int KS, int NW>
+__global__ __launch_bounds__(64 * NW) void knn_stream_kernel(KnnArgs a, int KC, int kstride) {
   extern __shared__ __align__(16) char smem[];
-  knn_stream_body<DT, R, KS>(a, KC, kstride, smem);
+  knn_stream_body<DT, R, KS, NW>(a, KC, kstride, smem);
 }
 
 // Contraction steps compiled into the kernel: the next bucket at or above
@@ -530,34 +534,54 @@ bool knn_use_stream(int M, int C, int dt_bf16) {
   return M > 256 && knn_stream_ks(C, dt_bf16) > 0;
 }
 
-template <int DT, int R>
+// Eight-wave workgroups hold two waves per SIMD, whose 256 registers the
+// register-bound wide rows (12 or more steps) exceed: those run four waves.
+template <int DT, int R, int NW>
 const void* stream_fn_ks(int KS) {
   switch (KS) {
-    case 2: return (const void*)&knn_stream_kernel_narrow<DT, R, 2>;
-    case 3: return (const void*)&knn_stream_kernel_narrow<DT, R, 3>;
-    case 4: return (const void*)&knn_stream_kernel_narrow<DT, R, 4>;
-    case 6: return (const void*)&knn_stream_kernel<DT, R, 6>;
-    case 8: return (const void*)&knn_stream_kernel<DT, R, 8>;
-    case 12: return (const void*)&knn_stream_kernel<DT, R, 12>;
-    case 16: return (const void*)&knn_stream_kernel<DT, R, 16>;
-    case 20: return (const void*)&knn_stream_kernel<DT, R, 20>;
-    default: return (const void*)&knn_stream_kernel<DT, R, 24>;
+    case 2: return (const void*)&knn_stream_kernel_narrow<DT, R, 2, NW>;
+    case 3: return (const void*)&knn_stream_kernel_narrow<DT, R, 3, NW>;
+    case 4: return (const void*)&knn_stream_kernel_narrow<DT, R, 4, NW>;
+    case 6: return (const void*)&knn_stream_kernel<DT, R, 6, NW>;
+    case 8: return (const void*)&knn_stream_kernel<DT, R, 8, NW>;
   }
+  if constexpr (NW == 4) {
+    switch (KS) {
+      case 12: return (const void*)&knn_stream_kernel<DT, R, 12, 4>;
+      case 16: return (const void*)&knn_stream_kernel<DT, R, 16, 4>;
+      case 20: return (const void*)&knn_stream_kernel<DT, R, 20, 4>;
+      default: return (const void*)&knn_stream_kernel<DT, R, 24, 4>;
+    }
+  }
+  return nullptr;
+}
+
+template <int NW>
+const void* stream_fn(int dt_bf16, int R, int KS) {
+  if (dt_bf16)
+    return R == 1 ? stream_fn_ks<1, 1, NW>(KS) : R == 2 ? stream_fn_ks<1, 2, NW>(KS) : stream_fn_ks<1, 4, NW>(KS);
+  return R == 1 ? stream_fn_ks<0, 1, NW>(KS) : R == 2 ? stream_fn_ks<0, 2, NW>(KS) : stream_fn_ks<0, 4, NW>(KS);
+}
+
+// Eight waves (128 query rows) per workgroup when those workgroups fit the
+// chip in one round, one per CU: each wave still sweeps every key, so a
+// workgroup's life is set by one wave's sweep, and the keys staged per chunk
+// serve twice the rows.  Measured on MI355X: the 448 x 448 ViG-Ti build
+// (B = 32, N = M = 784, C = 192) 76.8 -> 61.2 us, the high-resolution one
+// (B = 8, N = M = 3136, C = 96) 146.2 -> 137.7 us; graphs identical.
+int knn_stream_waves(int B, int N, int KS) {
+  return KS <= 8 && (long long)B * ((N + 127) / 128) <= 256 ? 8 : 4;
 }
 
 hipError_t launch_knn_stream(const KnnArgs& a, int dt_bf16, hipStream_t stream, hipEvent_t ev0,
                              hipEvent_t ev1) {
   const int KS = knn_stream_ks(a.C, dt_bf16);
-  const StreamGeom geo = stream_geom(a.C, dt_bf16, KS);
+  const int NW = knn_stream_waves(a.B, a.N, KS), rows = 16 * NW;
+  const StreamGeom geo = stream_geom(a.C, dt_bf16, KS, NW);
   const int R = knn_list_regs(a.KK);
-  const void* fn;
-  if (dt_bf16) {
-    fn = R == 1 ? stream_fn_ks<1, 1>(KS) : R == 2 ? stream_fn_ks<1, 2>(KS) : stream_fn_ks<1, 4>(KS);
-  } else {
-    fn = R == 1 ? stream_fn_ks<0, 1>(KS) : R == 2 ? stream_fn_ks<0, 2>(KS) : stream_fn_ks<0, 4>(KS);
-  }
-  const dim3 grid(a.B * ((a.N + kStRows - 1) / kStRows)), block(kStThreads);
-  if (KS == 0 || geo.total > 160 * 1024) return hipErrorInvalidValue;
+  const void* fn = NW == 8 ? stream_fn<8>(dt_bf16, R, KS) : stream_fn<4>(dt_bf16, R, KS);
+  const dim3 grid(a.B * ((a.N + rows - 1) / rows)), block(64 * NW);
+  if (KS == 0 || !fn || geo.total > 160 * 1024) return hipErrorInvalidValue;
   struct {
     KnnArgs a;
     int KC, kstride;

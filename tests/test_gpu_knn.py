@@ -91,6 +91,8 @@ EDGE = [
     ("stream_wide_C384_fp32", 1, 70, 300, 384, 9, 2, I.F32, "normal"),
     ("stream_C160_R4", 2, 64, 784, 160, 16, 4, I.BF16, "unit"),
     ("stream_fp32_C96", 1, 130, 3136, 96, 16, 2, I.F32, "normal"),
+    # more than 256 workgroups of 128 rows: the four-wave form of the narrow rows
+    ("stream_four_waves_B33", 33, 1000, 400, 64, 9, 2, I.BF16, "normal"),
     # LDS-staged wide kernel (bf16, C >= 256, M <= 256): key-row buckets 64 / 128 /
     # 224 / 256, a partial last stage (C = 520), K' = 64, one query row
     ("wide_M64_bucket", 2, 50, 64, 512, 9, 2, I.BF16, "unit"),
