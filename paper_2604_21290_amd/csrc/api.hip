@@ -798,9 +798,9 @@ hipError_t run_linear(const void* x, int R, int K, const void* W, const void* bi
 
 size_t round256(size_t v) { return (v + 255) & ~size_t(255); }
 
-// Workspace carve-up: sigma(Ut) (MRConv's output), Y, FFN hidden H (block and stack), the
-// pooled keys of U (pyramid stages), then U, two feature buffers and two
-// graphs (stack only).
+// Workspace carve-up: sigma(Ut) (MRConv's output), Y, FFN hidden H (block and
+// stack), the pooled keys of U (pyramid stages), then U, two feature buffers
+// and two graphs (stack only).
 struct VigWs {
   char* ut;
   char* y;

@@ -559,8 +559,10 @@ const void* stream_fn_ks(int KS) {
 template <int NW>
 const void* stream_fn(int dt_bf16, int R, int KS) {
   if (dt_bf16)
-    return R == 1 ? stream_fn_ks<1, 1, NW>(KS) : R == 2 ? stream_fn_ks<1, 2, NW>(KS) : stream_fn_ks<1, 4, NW>(KS);
-  return R == 1 ? stream_fn_ks<0, 1, NW>(KS) : R == 2 ? stream_fn_ks<0, 2, NW>(KS) : stream_fn_ks<0, 4, NW>(KS);
+    return R == 1 ? stream_fn_ks<1, 1, NW>(KS)
+           : R == 2 ? stream_fn_ks<1, 2, NW>(KS) : stream_fn_ks<1, 4, NW>(KS);
+  return R == 1 ? stream_fn_ks<0, 1, NW>(KS)
+         : R == 2 ? stream_fn_ks<0, 2, NW>(KS) : stream_fn_ks<0, 4, NW>(KS);
 }
 
 // Eight waves (128 query rows) per workgroup when those workgroups fit the
