@@ -29,7 +29,7 @@
 
 namespace gl {
 
-constexpr int kRsRows = 64;  // query rows per workgroup (16 per wave)
+constexpr int kRsRows = 64;  // query rows per four-wave workgroup (16 per wave)
 
 // LDS layout: key rows [KT*16][stride bytes], 64 zero bytes, then the scale
 // pairs (-2 r_j 2^(30-ib), (1 + n_j) 2^(30-ib)) [KT*16] as float2.  A row
@@ -58,16 +58,17 @@ bool knn_use_resident(int B, int N, int M, int C, int dt_bf16) {
 
 // Five contraction steps (C > 128) stage 70 KB of keys, two workgroups per CU,
 // so that variant is compiled for two waves per SIMD.
-template <int R, int KS, int KT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KS > 4 ? 2 : 4, 8))) void knn_resident_kernel(KnnArgs a) {
+template <int R, int KS, int KT, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(KS > 4 ? 2 : 4, 8))) void knn_resident_kernel(KnnArgs a) {
+  constexpr int NT = 64 * NW, ROWS = 16 * NW;
   extern __shared__ __align__(16) char smem[];
   constexpr int NK = KT * 16;  // key rows staged
   // key tiles that are whole for every M of this bucket (M > 0, 64, 128, 208)
   constexpr int kFull = KT == 4 ? 0 : KT == 8 ? 4 : KT == 13 ? 8 : 13;
   const int N = a.N, C = a.C, M = a.M, k = a.k, dil = a.dil, KK = a.KK, ib = a.ib;
-  const int nqt = (N + kRsRows - 1) / kRsRows;
+  const int nqt = (N + ROWS - 1) / ROWS;
   const int blk = xcd_remap(blockIdx.x, gridDim.x);
-  const int b = blk / nqt, q0 = (blk - b * nqt) * kRsRows;
+  const int b = blk / nqt, q0 = (blk - b * nqt) * ROWS;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, t = lane & 15;
   const int rowb = 2 * C, stride = resident_stride(C), nvec = C / 8;
@@ -92,12 +93,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KS > 4 ? 2 
   //    contiguous range of global memory.
   const int total = NK * nvec;
   const uint32_t magic = (65536u + nvec - 1) / nvec;  // i / nvec = (i * magic) >> 16 for i < 4096
-  constexpr int NV = (NK * KS * 4 + 255) / 256;      // passes for the widest rows of KS steps
+  constexpr int NV = (NK * KS * 4 + NT - 1) / NT;    // passes for the widest rows of KS steps
   uint4 st[NV];
   int dst[NV];
 #pragma unroll
   for (int u = 0; u < NV; ++u) {
-    const int i = min(tid + 256 * u, total - 1);
+    const int i = min(tid + NT * u, total - 1);
     const int r = (int)(((uint32_t)i * magic) >> 16), v = i - r * nvec;
     dst[u] = r * stride + v * 16;
     st[u] = *reinterpret_cast<const uint4*>(kb + ((size_t)min(r, M - 1) * nvec + v) * 16);
@@ -236,33 +237,44 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KS > 4 ? 2 
   }
 }
 
-template <int R, int KS>
+template <int R, int KS, int NW>
 const void* resident_fn_tiles(int KT) {
   switch (KT) {
-    case 4: return (const void*)&knn_resident_kernel<R, KS, 4>;
-    case 8: return (const void*)&knn_resident_kernel<R, KS, 8>;
-    case 13: return (const void*)&knn_resident_kernel<R, KS, 13>;
-    default: return (const void*)&knn_resident_kernel<R, KS, 16>;
+    case 4: return (const void*)&knn_resident_kernel<R, KS, 4, NW>;
+    case 8: return (const void*)&knn_resident_kernel<R, KS, 8, NW>;
+    case 13: return (const void*)&knn_resident_kernel<R, KS, 13, NW>;
+    default: return (const void*)&knn_resident_kernel<R, KS, 16, NW>;
   }
 }
 
-template <int R>
+template <int R, int NW>
 const void* resident_fn_steps(int KS, int KT) {
   switch (KS) {
-    case 2: return resident_fn_tiles<R, 2>(KT);
-    case 3: return resident_fn_tiles<R, 3>(KT);
-    case 4: return resident_fn_tiles<R, 4>(KT);
-    default: return resident_fn_tiles<R, 5>(KT);
+    case 2: return resident_fn_tiles<R, 2, NW>(KT);
+    case 3: return resident_fn_tiles<R, 3, NW>(KT);
+    case 4: return resident_fn_tiles<R, 4, NW>(KT);
+    default: return resident_fn_tiles<R, 5, NW>(KT);
   }
 }
+
+template <int NW>
+const void* resident_fn(int R, int KS, int KT) {
+  return R == 1 ? resident_fn_steps<1, NW>(KS, KT)
+         : R == 2 ? resident_fn_steps<2, NW>(KS, KT) : resident_fn_steps<4, NW>(KS, KT);
+}
+
+// Eight waves (128 query rows) per workgroup when those workgroups fit the
+// chip in one round, one per CU, as in the streamed build: each wave's work is
+// the same, and the staged keys and their scales serve twice the rows.
+int knn_resident_waves(int B, int N) { return (long long)B * ((N + 127) / 128) <= 256 ? 8 : 4; }
 
 hipError_t launch_knn_resident(const KnnArgs& a, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
   const int R = knn_list_regs(a.KK), KS = (a.C + 31) / 32, KT = knn_resident_tiles(a.M);
-  const void* fn = R == 1 ? resident_fn_steps<1>(KS, KT)
-                   : R == 2 ? resident_fn_steps<2>(KS, KT) : resident_fn_steps<4>(KS, KT);
+  const int NW = knn_resident_waves(a.B, a.N), rows = 16 * NW;
+  const void* fn = NW == 8 ? resident_fn<8>(R, KS, KT) : resident_fn<4>(R, KS, KT);
   const size_t smem = KT == 4 ? resident_smem<4>(a.C) : KT == 8 ? resident_smem<8>(a.C)
                       : KT == 13 ? resident_smem<13>(a.C) : resident_smem<16>(a.C);
-  const dim3 grid(a.B * ((a.N + kRsRows - 1) / kRsRows)), block(256);
+  const dim3 grid(a.B * ((a.N + rows - 1) / rows)), block(64 * NW);
   return launch_with_smem(fn, grid, block, smem, stream, ev0, ev1, a);
 }
 
