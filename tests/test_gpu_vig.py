@@ -109,12 +109,16 @@ PYR_DIL = (1, 2, 1)
 
 
 def _workload(name, B):
-    """name[:f32] at batch B; an ":f32" suffix runs the workload in fp32."""
-    base, _, dt = name.partition(":")
+    """name[:opt] at batch B; ":f32" runs the workload in fp32, ":pool2" pools
+    its keys 2 x 2 (at C = 640 the update then takes the two-pass form with
+    pooled keys and the GELU in its GEMM's epilogue)."""
+    base, _, opt = name.partition(":")
     w = I.with_batch(I.WORKLOADS[base], B)
+    if opt == "pool2":
+        w = dataclasses.replace(w, pool_r=2)
     if w.pool_r > 1:
         w = dataclasses.replace(w, dilations=PYR_DIL)
-    if dt == "f32":
+    if opt == "f32":
         w = dataclasses.replace(w, dtype=I.F32)
     return w
 
@@ -156,7 +160,8 @@ def _run_blocks(w, L, x0d, params_d, same_stream=False):
 
 
 @pytest.mark.parametrize("name,B,L", [("vig_ti", 4, 6), ("vig_b", 2, 5), ("single", 1, 1),
-                                      ("pyr_s1", 2, 3), ("pyr_s2", 2, 3), ("pyr_s2:f32", 1, 3)])
+                                      ("pyr_s1", 2, 3), ("pyr_s2", 2, 3), ("pyr_s2:f32", 1, 3),
+                                      ("vig_b:pool2", 2, 3)])
 def test_vig_blocks_teacher_forced(name, B, L):
     require_gpu()
     from paper_2604_21290_amd import api
@@ -191,7 +196,7 @@ def test_vig_blocks_teacher_forced(name, B, L):
 
 
 @pytest.mark.parametrize("name,B,L", [("vig_ti", 4, 6), ("vig_b", 2, 5), ("pyr_s1", 2, 3),
-                                      ("pyr_s2", 2, 3), ("pyr_s2:f32", 1, 3)])
+                                      ("pyr_s2", 2, 3), ("pyr_s2:f32", 1, 3), ("vig_b:pool2", 2, 3)])
 def test_vig_stack_matches_blocks(name, B, L):
     require_gpu()
     from paper_2604_21290_amd import api
