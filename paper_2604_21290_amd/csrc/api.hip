@@ -697,9 +697,18 @@ gl_status gl_graphleap_stack(gl_lookahead_t h, const void* x0, int B, int H, int
         s = timed_launch(h, GL_TIME_FUSED, "block launch", [&](hipEvent_t e0, hipEvent_t e1) {
           return gl::launch_block(ka, ma, dtb, rts[l], h->su, e0, e1);
         });
+      } else if (build && ws && gl::block_hosts_build(B, N, M, C, B * N, dtb)) {
+        // two-pass update (wide W): the build tiles and the gather tiles in one
+        // launch, then the GEMM pass; timed together as the block
+        next = 1 - cur;
+        const gl::KnnArgs ka = gl::make_knn_args(a.x_in, keys, B, N, C, M, k, dilations[l + 1],
+                                                 iw[next]);
+        s = timed_launch(h, GL_TIME_FUSED, "block launch", [&](hipEvent_t e0, hipEvent_t e1) {
+          hipError_t e = gl::launch_block_gather(ka, ma, ws, h->su, e0);
+          return e != hipSuccess ? e : gl::launch_mrconv_gemm(ma, dtb, ws, h->su, nullptr, e1);
+        });
       } else if (build) {
-        // large key sets or wide channels: the build kernel, then the update, in
-        // stream order
+        // large key sets: the build kernel, then the update, in stream order
         next = 1 - cur;
         s = timed_launch(h, GL_TIME_BUILD, "knn launch", [&](hipEvent_t e0, hipEvent_t e1) {
           return gl::launch_knn(a.x_in, keys, B, N, C, M, k, dilations[l + 1], dtb, iw[next], h->su,
@@ -910,6 +919,16 @@ gl_status enqueue_vig_block(gl_lookahead_t h, const void* x_in, const VigGrid& g
     const gl::KnnArgs ka = gl::make_knn_args(u, keys, B, N, C, M, k, dil_next, idx_next);
     s = timed_launch(h, GL_TIME_FUSED, "block launch", [&](hipEvent_t e0, hipEvent_t e1) {
       return gl::launch_block(ka, ma, dtb, rt, h->su, e0, e1);
+    });
+    if (s != GL_OK) return s;
+  } else if (schedule == GL_SCHED_LOOKAHEAD_FUSED && idx_next && mws &&
+             gl::block_hosts_build(B, N, M, C, R, dtb)) {
+    // two-pass update: the build tiles and the gather tiles in one launch, then
+    // the GEMM pass (with the GELU); timed together as the block
+    const gl::KnnArgs ka = gl::make_knn_args(u, keys, B, N, C, M, k, dil_next, idx_next);
+    s = timed_launch(h, GL_TIME_FUSED, "block launch", [&](hipEvent_t e0, hipEvent_t e1) {
+      hipError_t e = gl::launch_block_gather(ka, ma, mws, h->su, e0);
+      return e != hipSuccess ? e : gl::launch_mrconv_gemm(ma, dtb, mws, h->su, nullptr, e1);
     });
     if (s != GL_OK) return s;
   } else {

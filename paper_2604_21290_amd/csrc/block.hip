@@ -10,6 +10,11 @@
 //
 // Workgroup ids are split between the roles in groups of 8 (one per XCD), so
 // both roles spread over every XCD from the first wave of dispatch on.
+//
+// Updates in the two-pass form (wide W) cannot be a tile of this grid; their
+// first pass, the gather of [x_i | m_i] rows, also reads only X^l, so it
+// shares a grid with the build tiles instead (block_gather_kernel), and the
+// GEMM pass follows in stream order.
 #include "knn_tile.h"
 #include "knn_wide.h"
 #include "mrconv_tile.h"
@@ -19,6 +24,7 @@ namespace gl {
 constexpr int kBlockWideWaves = 2;     // waves per SIMD the LDS-staged variant is compiled for
 constexpr bool kBlockWideDB = true;    // its build role with two staging register sets
 constexpr bool kBlockWideT3 = true;    // its update role gathering in one round
+constexpr int kBlockGatherRows = 32;   // nodes per gather tile of block_gather_kernel
 
 // Role of dispatch id i among nb build and nu update workgroups; j is the
 // workgroup's index within its role.
@@ -119,6 +125,74 @@ const void* block_fn(int R, int RT, int KB, int act) {
 int block_wide_rows(const KnnArgs& ka, int dt_bf16) {
   if (!knn_use_wide(ka.M, ka.C, dt_bf16)) return 0;
   return ka.M <= 128 ? 128 : 224;
+}
+
+// The build tiles (LDS-staged, WK key rows) and the gather tiles of a
+// two-pass update in one grid.
+template <int R, int KB, int WK>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kBlockWideWaves, 8))) void block_gather_kernel(KnnArgs ka, MrArgs ma, void* xcat, int nb, int ng) {
+  extern __shared__ __align__(16) char smem[];
+  int j;
+  if (block_role_is_build(blockIdx.x, nb, ng, &j))
+    knn_wide_tile<R, kWdQW, WK, kBlockWideDB, true>(smem, ka, xcd_remap(j, nb));
+  else
+    mr_gather_tile<1, KB>(ma, xcd_remap(j, ng), kBlockGatherRows, reinterpret_cast<int32_t*>(smem),
+                          xcat);
+}
+
+template <int R, int WK>
+const void* block_gather_fn_kb(int KB) {
+  switch (KB) {
+    case 9: return (const void*)&block_gather_kernel<R, 9, WK>;
+    case 16: return (const void*)&block_gather_kernel<R, 16, WK>;
+    case 32: return (const void*)&block_gather_kernel<R, 32, WK>;
+    default: return (const void*)&block_gather_kernel<R, 64, WK>;
+  }
+}
+
+template <int WK>
+const void* block_gather_fn(int R, int KB) {
+  return R == 1 ? block_gather_fn_kb<1, WK>(KB)
+                : R == 2 ? block_gather_fn_kb<2, WK>(KB) : block_gather_fn_kb<4, WK>(KB);
+}
+
+// The LDS-staged build tile with at most 224 key rows (knn_separate's
+// complement among the LDS-staged shapes), and build and gather tiles that
+// fit the chip in one round at two workgroups per CU (the build tile's LDS):
+// past that the gather, which alone runs many workgroups per CU, loses more
+// to the shared LDS than the overlap gains (ViG-B: 15.3 K -> 14.5 K layers/s).
+bool block_hosts_build(int B, int N, int M, int C, int R, int dt_bf16) {
+  if (!knn_use_wide(M, C, dt_bf16) || M > 224) return false;
+  const long nb = (long)B * ((N + 16 * kWdQW - 1) / (16 * kWdQW));
+  const long ng = (R + kBlockGatherRows - 1) / kBlockGatherRows;
+  return nb + ng <= 512;
+}
+
+hipError_t launch_block_gather(const KnnArgs& ka, const MrArgs& ma, void* xcat,
+                               hipStream_t stream, hipEvent_t ev0) {
+  if (!knn_use_wide(ka.M, ka.C, 1) || ka.M > 224 || !xcat) return hipErrorInvalidValue;
+  const int wk = block_wide_rows(ka, 1);
+  const int qr = 16 * kWdQW;
+  const int nb = ka.B * ((ka.N + qr - 1) / qr);
+  const int ng = (ma.R + kBlockGatherRows - 1) / kBlockGatherRows;
+  const size_t wsm = wk == 128 ? WideGeom<kWdQW, 128>::kSmem : WideGeom<kWdQW, 224>::kSmem;
+  const size_t smem = std::max(wsm, (size_t)kBlockGatherRows * 64 * sizeof(int32_t));
+  const int R = knn_list_regs(ka.KK), KB = mrconv_k_bucket(ma.k);
+  const void* fn = wk == 224 ? block_gather_fn<224>(R, KB) : block_gather_fn<128>(R, KB);
+  struct {
+    KnnArgs ka;
+    MrArgs ma;
+    void* xcat;
+    int nb, ng;
+  } args{ka, ma, xcat, nb, ng};
+  void* argv[] = {&args.ka, &args.ma, &args.xcat, &args.nb, &args.ng};
+  if (smem > 65536) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+  }
+  const dim3 grid(nb + ng), block(256);
+  if (ev0) return hipExtLaunchKernel(fn, grid, block, argv, smem, stream, ev0, nullptr, 0);
+  return hipLaunchKernel(fn, grid, block, argv, smem, stream);
 }
 
 hipError_t launch_block(const KnnArgs& ka, const MrArgs& ma, int dt_bf16, int rt,

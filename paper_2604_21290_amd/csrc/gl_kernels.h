@@ -113,6 +113,9 @@ hipError_t launch_mrconv_args(const MrArgs& a, int dt_bf16, int rt, void* split_
                               hipStream_t stream, hipEvent_t ev0 = nullptr,
                               hipEvent_t ev1 = nullptr);
 bool mrconv_use_split(int C, int Cout, int dt_bf16, int rt, int R);
+// The GEMM pass alone of the two-pass form, on [x | m] rows already in split_ws.
+hipError_t launch_mrconv_gemm(const MrArgs& a, int dt_bf16, const void* split_ws,
+                              hipStream_t stream, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 int mrconv_col_tiles(int R, int Cout, int rt);
 size_t mrconv_split_ws_bytes(int R, int C, int dt_bf16);
 // Multi-head update with per-head weights Wh [H, hd, 2hd] on MFMA (hd a
@@ -131,6 +134,12 @@ MrArgs make_mr_args(const void* x, const void* keys, const int32_t* idx, const v
 // One block: the build tiles of ka and the update tiles of ma in one grid.
 hipError_t launch_block(const KnnArgs& ka, const MrArgs& ma, int dt_bf16, int rt,
                         hipStream_t stream, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// Two-pass updates (wide W): the build tiles of ka and the gather tiles of
+// ma, which write [x | m] rows to xcat, in one grid (bf16, a build the block
+// can host: block_hosts_build); launch_mrconv_gemm then finishes the update.
+bool block_hosts_build(int B, int N, int M, int C, int R, int dt_bf16);
+hipError_t launch_block_gather(const KnnArgs& ka, const MrArgs& ma, void* xcat,
+                               hipStream_t stream, hipEvent_t ev0 = nullptr);
 
 // r x r average (key pooling) or, with max_pool, maximum (inter-stage node
 // reduction) of the H x W node grid.

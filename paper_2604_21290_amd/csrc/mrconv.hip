@@ -107,22 +107,10 @@ const void* mrconv_fn_act(int KB, int act) {
 }
 
 // Gather-only workgroup of the two-pass MRConv: kMrGatherRows nodes.
-constexpr int kMrGatherRows = 16;
-
 template <int DT, int KB>
 __global__ __launch_bounds__(kMrThreads) void mr_gather_kernel(MrArgs a, void* xcat) {
   __shared__ int32_t sIdx[kMrGatherRows * 64];
-  constexpr int ES = DT ? 2 : 4;
-  const int row0 = xcd_remap(blockIdx.x, gridDim.x) * kMrGatherRows;
-  for (int e = threadIdx.x; e < kMrGatherRows * a.k; e += kMrThreads) {
-    const int r = e / a.k, tt = e - r * a.k, row = row0 + r;
-    const int j = row < a.R ? a.idx[(size_t)row * a.k + tt] : 0;
-    sIdx[e] = min(max(j, 0), a.M - 1) * (a.C * ES / 16);
-  }
-  __syncthreads();
-  const size_t stride = (size_t)2 * a.C * ES;
-  mr_gather_rows<DT, KB>(a, row0, kMrGatherRows, sIdx, static_cast<char*>(xcat) + row0 * stride,
-                         stride);
+  mr_gather_tile<DT, KB>(a, xcd_remap(blockIdx.x, gridDim.x), kMrGatherRows, sIdx, xcat);
 }
 
 template <int DT>
@@ -166,13 +154,27 @@ hipError_t launch_mrconv(const void* x, const void* keys, const int32_t* idx, co
                             rt, split_ws, stream, ev0, ev1);
 }
 
+// The second pass of the two-pass MRConv: out = act_out([x | m] W^T + b).
+hipError_t launch_mrconv_gemm(const MrArgs& a, int dt_bf16, const void* split_ws,
+                              hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  GemmArgs ga;
+  ga.A = split_ws;
+  ga.W = a.W;
+  ga.bias = a.bias;
+  ga.residual = nullptr;
+  ga.out = a.out;
+  ga.R = a.R;
+  ga.K = 2 * a.C;
+  ga.Cout = a.Cout;
+  ga.act_in = 0;
+  ga.act_out = a.act_out;
+  return launch_gemm_nt(ga, dt_bf16, stream, ev0, ev1);
+}
+
 hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split_ws,
                               hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
   MrArgs a = a0;
   const int C = a.C, Cout = a.Cout, k = a.k;
-  const void* W = a.W;
-  const void* bias = a.bias;
-  void* out = a.out;
   const int KB = mrconv_k_bucket(k);
   // the multi-head update (W = per-head Wh) always takes the fused tile
   if (a.heads > 1 && (rt < 1 || a.act_out)) return hipErrorInvalidValue;
@@ -184,18 +186,7 @@ hipError_t launch_mrconv_args(const MrArgs& a0, int dt_bf16, int rt, void* split
     hipError_t e = ev0 ? hipExtLaunchKernel(fg, g1, blk, argv, 0, stream, ev0, nullptr, 0)
                        : hipLaunchKernel(fg, g1, blk, argv, 0, stream);
     if (e != hipSuccess) return e;
-    GemmArgs ga;
-    ga.A = split_ws;
-    ga.W = W;
-    ga.bias = bias;
-    ga.residual = nullptr;
-    ga.out = out;
-    ga.R = a.R;
-    ga.K = 2 * C;
-    ga.Cout = Cout;
-    ga.act_in = 0;
-    ga.act_out = a.act_out;
-    return launch_gemm_nt(ga, dt_bf16, stream, nullptr, ev1);
+    return launch_mrconv_gemm(a, dt_bf16, split_ws, stream, nullptr, ev1);
   }
   const int TM = 16 * rt;
   const size_t smem = mrconv_smem_bytes(C, k, dt_bf16, rt);

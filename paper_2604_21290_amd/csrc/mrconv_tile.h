@@ -171,6 +171,26 @@ __device__ __forceinline__ void mr_gather_rows(const MrArgs& a, int row0, int TM
   }
 }
 
+// Gather-only tile of the two-pass MRConv: the [x_i | m_i] rows of TM nodes
+// from flattened node blk * TM, written to xcat [R, 2C].  sIdx: TM * k ints of
+// LDS.  Called by all 256 threads.
+constexpr int kMrGatherRows = 16;  // nodes per workgroup of the gather kernel
+
+template <int DT, int KB>
+__device__ __forceinline__ void mr_gather_tile(const MrArgs& a, int blk, int TM, int32_t* sIdx,
+                                               void* xcat) {
+  constexpr int ES = DT ? 2 : 4;
+  const int row0 = blk * TM;
+  for (int e = threadIdx.x; e < TM * a.k; e += kMrThreads) {
+    const int r = e / a.k, tt = e - r * a.k, row = row0 + r;
+    const int j = row < a.R ? a.idx[(size_t)row * a.k + tt] : 0;
+    sIdx[e] = min(max(j, 0), a.M - 1) * (a.C * ES / 16);
+  }
+  __syncthreads();
+  const size_t stride = (size_t)2 * a.C * ES;
+  mr_gather_rows<DT, KB>(a, row0, TM, sIdx, static_cast<char*>(xcat) + row0 * stride, stride);
+}
+
 // TM = 16*RT nodes starting at flattened node row0.  smem holds
 // mrconv_smem_bytes(C, k, RT) bytes.  Called by all 256 threads.
 // HEADS: the multi-head update (a.heads > 1), which skips the zero blocks of W.
