@@ -302,8 +302,10 @@ gl_status gl_graphleap_block(gl_lookahead_t h, const void* x_in, int B, int H, i
  *     all on the update stream (Eq. 5-7 with U = X).
  *   schedule GL_SCHED_LOOKAHEAD_FUSED: the lookahead graphs as above, but each
  *     block is one launch on the update stream whose grid holds both the
- *     build tiles of Ghat^(l+1) and the update tiles of X^(l+1); the results
- *     are bit-identical to GL_SCHED_LOOKAHEAD.
+ *     build tiles of Ghat^(l+1) and the update tiles of X^(l+1) (for updates
+ *     in the two-pass form, the gather tiles, with the GEMM pass launched
+ *     next; builds over large key sets run as their own launch first); the
+ *     results are bit-identical to GL_SCHED_LOOKAHEAD.
  *
  *   x0 [B, N, C] input, N = H*W.  Ws [L, C, 2C]; bs [L, C] or NULL.
  *   dilations: host array of L ints (the dilation of the block that uses
@@ -405,7 +407,8 @@ gl_status gl_vig_block(gl_lookahead_t h, const void* x_in, int B, int H, int W, 
  *     (Eq. 12 and Alg. 1's bootstrap); each build runs on the build stream
  *     while the rest of its block runs on the update stream.
  *   GL_SCHED_LOOKAHEAD_FUSED: the same graphs; one stream, each build in one
- *     launch with its block's MRConv (both read only U^l).
+ *     launch with its block's MRConv, or with the gather pass of a two-pass
+ *     MRConv (both read only U^l); builds over large key sets run alone.
  *   GL_SCHED_STANDARD: Ghat^l = G(U^l, d_l) (Eq. 6), serial.
  * With pool_r > 1 each graph ranks the keys pooled from the U it is built
  * from and each MRConv gathers the keys pooled from its own U (as
