@@ -336,3 +336,63 @@ def test_vig_stack_hip_graph_replay(name, B):
         assert torch.equal(out, ref), f"{name}: replay {r} differs"
         del junk
     la.close()
+
+
+@pytest.mark.parametrize("name", ["vig_ti", "vig_b", "pyr_s1", "pyr_s2"])
+def test_vig_block_full_size_sampled(name):
+    """One full block at the workload's full batch (the grids the benchmark
+    launches), teacher-forced: the GPU's graph of U^0 goes in, and the first
+    two images of X^1 and of the next graph G(U^0, d_1) are checked against
+    the oracle on the stored tensors."""
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = I.WORKLOADS[name]
+    d1 = 2
+    x0 = I.make_features(w)
+    p = I.make_vig_params(w, 0)
+    x0d, pd = to_dev(x0), _dev_params(p)
+    _say("vig full size", name, "B", w.B)
+    u0 = api.linear(x0d, pd["W_in"], pd["b_in"])
+    keys = api.pool_keys(u0, w.H, w.W, w.pool_r) if w.pool_r > 1 else None
+    idx0 = api.knn_graph(u0, w.k, 1, keys=keys)
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    ws = api.vig_workspace(x0d, w.k, **_grid(w))
+    idx1 = torch.empty_like(idx0)
+    x1, u_out = la.vig_block(x0d, idx0, pd, ws, idx_next=idx1, dilation_next=d1, **_grid(w))
+    torch.cuda.synchronize()
+    la.close()
+    assert torch.equal(u_out, u0)
+    nb = 2
+    hx0 = from_dev(x0d[:nb]).value
+    hu0 = from_dev(u0[:nb]).value
+    ph = _host_params(p)
+    g0 = idx0[:nb].cpu().numpy()
+    ref = O.vig_block_ref(hx0, g0, ph, **_grid(w))
+    check_close(from_dev(x1[:nb]).value, ref, w.dtype, f"{name} full-size block, 2 images")
+    hk = None if keys is None else from_dev(keys[:nb]).value
+    check_idx(idx1[:nb].cpu().numpy(), O.knn_distances(hu0, hk), w.k, d1,
+              label=f"{name} full-size next graph")
+
+
+@pytest.mark.parametrize("name", ["vig_ti", "vig_b", "vig_s", "pyr_s1", "pyr_s3"])
+def test_vig_stack_fused_equals_two_stream_full_size(name):
+    """At the workload's full batch and depth (the launch configurations the
+    benchmark times: one-launch blocks, build and gather sharing a launch,
+    separate launches), the fused schedule's full-block stack equals the
+    two-stream lookahead bit for bit."""
+    require_gpu()
+    from paper_2604_21290_amd import api
+    w = I.WORKLOADS[name]
+    x0d = to_dev(I.make_features(w))
+    pd = [_dev_params(I.make_vig_params(w, l)) for l in range(w.L)]
+    dil = list(w.dilations)
+    _say("vig stack full size", name, "B", w.B, "L", w.L)
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    ws = api.vig_workspace(x0d, w.k, **_grid(w))
+    fused = la.vig_stack(x0d, pd, dil, w.k, schedule=api.GL_SCHED_LOOKAHEAD_FUSED, ws=ws,
+                         **_grid(w))
+    two = la.vig_stack(x0d, pd, dil, w.k, schedule=api.GL_SCHED_LOOKAHEAD, ws=ws, **_grid(w))
+    torch.cuda.synchronize()
+    la.close()
+    assert torch.isfinite(fused.float()).all()
+    assert torch.equal(fused, two), f"{name}: fused full-block stack differs from two-stream"
