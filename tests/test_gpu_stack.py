@@ -5,6 +5,8 @@ Every block is teacher-forced: the graph it used is checked against the oracle
 kNN of the exact stored features (and pooled keys) it was built from, and its
 output against the oracle MRConv of its exact stored inputs.  Free-running
 fp64 stacks are not compared (near-tie flips may legitimately diverge)."""
+import zlib
+
 import numpy as np
 import pytest
 import torch
@@ -330,3 +332,36 @@ def test_stack_hip_graph_replay(name):
         assert torch.equal(out, ref), f"replay {r} differs"
         del junk
     la.close()
+
+
+# Two-pass updates (wide W) whose gather shares the fused schedule's launch
+# with the next build: both key-row buckets of the LDS-staged build (M <= 128
+# and up to 224), ragged node counts (R not a multiple of the 32-node gather
+# tile, query rows not a multiple of 32), k = 16 and dilations up to 3.
+TWO_PASS = [
+    # label, B, H, W, C, k, dilations
+    ("two_pass_M100_k16", 3, 10, 10, 320, 16, (1, 2, 3)),
+    ("two_pass_M196_ragged", 2, 14, 14, 384, 9, (1, 1, 2, 2)),
+    ("two_pass_M221_C640", 1, 13, 17, 640, 9, (1, 3)),
+]
+
+
+@pytest.mark.parametrize("case", TWO_PASS, ids=[c[0] for c in TWO_PASS])
+def test_two_pass_shared_launch(case):
+    require_gpu()
+    from paper_2604_21290_amd import api
+    label, B, H, W, C, k, dil = case
+    w = I.Workload(label, B, H, W, C, k, dil, I.BF16, seed=zlib.crc32(label.encode()) % 1000)
+    x0 = I.make_features(w)
+    Wst, bst = _weights(w, w.L, zero_bias=False)
+    x0d, Wd, bd = to_dev(x0), to_dev(Wst), to_dev(bst)
+    _say("two-pass shared launch", label)
+    xs, graphs = run_blocks(w, x0d, Wd, bd)
+    teacher_forced_checks(w, xs, graphs, Wst, bst)
+    la = api.Lookahead(torch.cuda.current_stream(), torch.cuda.Stream())
+    ws = api.make_stack_workspace(x0d, w.H, w.W, w.k, w.pool_r)
+    fused = la.stack(x0d, w.H, w.W, Wd, bd, list(w.dilations), w.k, w.pool_r,
+                     schedule=api.GL_SCHED_LOOKAHEAD_FUSED, ws=ws)
+    torch.cuda.synchronize()
+    la.close()
+    assert torch.equal(fused, xs[-1]), f"{label}: fused schedule differs from block-by-block"
