@@ -131,6 +131,8 @@ RESIDENT = [
     ("res_C128_wide_order", 16, 1600, 196, 128, 9, 1),
     ("res_C136_M150_KK18", 32, 800, 150, 136, 9, 2),
     ("res_C160_M256_KK64", 8, 3100, 256, 160, 16, 4),
+    # 8-wave workgroups of 128 rows (at most 256 of them), a 12-row last tile
+    ("res_8_waves_tail12", 2, 12300, 200, 64, 9, 2),
 ]
 
 
