@@ -54,7 +54,9 @@ struct StreamGeom {
 // candidate slots, per-row thresholds.  A key row holds the KS contraction
 // steps the kernel runs (channels past C stay zero) plus 16 bytes that move
 // consecutive rows to other banks.  KC is a multiple of 64 (whole groups of 4
-// tiles), as large as the budget allows, at least 64.
+// tiles), as large as the budget and the prefetch registers allow, at least
+// 64 and at most 384 (the eight-wave narrow rows: 384 at C = 96, where each
+// chunk boundary costs a barrier and a merge in every wave).
 __host__ __device__ inline StreamGeom stream_geom(int C, int dt_bf16, int KS, int NW) {
   StreamGeom s;
   const int rowb = C * (dt_bf16 ? 2 : 4);
@@ -64,7 +66,7 @@ __host__ __device__ inline StreamGeom stream_geom(int C, int dt_bf16, int KS, in
   int kc = (st_lds_budget(KS, NW) - fixed) / (s.kstride + 8);
   const int kv = st_max_vec(KS) * 64 * NW * 16 / rowb;  // prefetchable rows
   kc = (kc < kv ? kc : kv) / 64 * 64;
-  s.KC = kc > 256 ? 256 : kc < 64 ? 64 : kc;
+  s.KC = kc > 384 ? 384 : kc < 64 ? 64 : kc;
   s.keys = 0;
   s.scales = s.keys + (size_t)s.KC * s.kstride;
   s.cand = s.scales + (size_t)s.KC * 8;
